@@ -1,0 +1,127 @@
+/*
+ * CPU oracle: TurboQuant encode, written as the plain definition
+ * (test infrastructure only -- never linked into or called by the library).
+ *
+ * Section II-B, steps 1-5, for one float32 row x of length d:
+ *   1. normalise:  n = sqrt(sum_k x_k^2)        sequential float64 sum; every
+ *                                                square of a float32 is exact
+ *   2. rotate:     S_j = sum_k R[j,k] * x_k     sequential float64 sum over
+ *                                                k = 0..d-1; every product of
+ *                                                two float32 values is exact
+ *   3. quantise:   code_j = #{ i : fl64(t_i * n) <= S_j }
+ *                  i.e. the cell of S_j / n with a value on a boundary going
+ *                  to the upper cell; a zero row gets code L/2 everywhere
+ *   5. scale:      s = n / sqrt(sum_j c2[code_j]),  c2[c] = fl64(c_c * c_c),
+ *                  sequential float64 sum over j, stored as float32
+ *                  (the per-vector length-renormalisation scalar: the
+ *                  reconstruction s * R^T xhat has the length of x)
+ * Step 4 (bit packing) is done by the Python wrapper.
+ *
+ * Build with -ffp-contract=off so that no multiply-add is fused: the
+ * definition rounds every product and every sum on its own.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Returns 0 on success, -1 on bad arguments, -2 on a non-finite input row
+ * (its index is written to *bad_row). */
+int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
+               const double *bounds, int32_t L, uint8_t *codes,
+               double *norm_out, int64_t *bad_row)
+{
+    if (!X || !R || !bounds || !codes || n < 0 || d <= 0 || L < 2 || L > 256)
+        return -1;
+    /* R transposed in float64 so that the inner loop runs over j with k fixed:
+     * every S_j still accumulates k = 0, 1, ..., d-1 in order. */
+    double *RT = (double *)malloc(sizeof(double) * (size_t)d * (size_t)d);
+    if (!RT) return -1;
+    for (int32_t j = 0; j < d; ++j)
+        for (int32_t k = 0; k < d; ++k)
+            RT[(size_t)k * d + j] = (double)R[(size_t)j * d + k];
+    int status = 0;
+    int64_t first_bad = -1;
+
+#pragma omp parallel
+    {
+        double *S = (double *)malloc(sizeof(double) * (size_t)d);
+        double *T = (double *)malloc(sizeof(double) * (size_t)(L - 1));
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            const float *x = X + (size_t)i * d;
+            uint8_t *c = codes + (size_t)i * d;
+            int finite = 1;
+            double n2 = 0.0;
+            for (int32_t k = 0; k < d; ++k) {
+                double xk = (double)x[k];
+                if (!isfinite(xk)) finite = 0;
+                double sq = xk * xk;
+                n2 = n2 + sq;
+            }
+            if (!finite) {
+#pragma omp critical
+                {
+                    if (first_bad < 0 || i < first_bad) first_bad = i;
+                    status = -2;
+                }
+                continue;
+            }
+            double nrm = sqrt(n2);
+            if (norm_out) norm_out[i] = nrm;
+            if (nrm == 0.0) {
+                memset(c, L / 2, (size_t)d);
+                continue;
+            }
+            for (int32_t t = 0; t < L - 1; ++t) {
+                double p = bounds[t] * nrm;
+                T[t] = p;
+            }
+            for (int32_t j = 0; j < d; ++j) S[j] = 0.0;
+            for (int32_t k = 0; k < d; ++k) {
+                const double xk = (double)x[k];
+                const double *col = RT + (size_t)k * d;
+                for (int32_t j = 0; j < d; ++j) {
+                    double prod = col[j] * xk;
+                    S[j] = S[j] + prod;
+                }
+            }
+            for (int32_t j = 0; j < d; ++j) {
+                int cnt = 0;
+                for (int32_t t = 0; t < L - 1; ++t) cnt += (T[t] <= S[j]);
+                c[j] = (uint8_t)cnt;
+            }
+        }
+        free(S);
+        free(T);
+    }
+    free(RT);
+    if (status == -2 && bad_row) *bad_row = first_bad;
+    return status;
+}
+
+/* Length-renormalisation scalar (step 5) for rows already coded. */
+int tqo_scales(const uint8_t *codes, const double *norms, int64_t n, int32_t d,
+               const double *cents, int32_t L, float *scale_out)
+{
+    if (!codes || !norms || !cents || !scale_out || n < 0 || d <= 0 || L < 2)
+        return -1;
+    double c2[256];
+    for (int32_t c = 0; c < L; ++c) {
+        double v = cents[c] * cents[c];
+        c2[c] = v;
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const uint8_t *c = codes + (size_t)i * d;
+        if (norms[i] == 0.0) {
+            scale_out[i] = 0.0f;
+            continue;
+        }
+        double h2 = 0.0;
+        for (int32_t j = 0; j < d; ++j) h2 = h2 + c2[c[j]];
+        double s = norms[i] / sqrt(h2);
+        scale_out[i] = (float)s;
+    }
+    return 0;
+}

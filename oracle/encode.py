@@ -1,0 +1,100 @@
+"""TurboQuant encode and bit packing (oracle; test use only).
+
+Section II-B, steps 1-5.  The arithmetic of steps 1-3 and 5 is the plain C in
+csrc/tq_oracle.c (sequential float64, exact products, no fused multiply-add);
+this module marshals arguments and does step 4, bit packing.
+
+Bit packing (step 4; a 1536-d vector takes 768 bytes at 4 bits): the codes of
+a row form one little-endian bitstream, coordinate j occupying bits
+[b*j, b*j + b) least-significant bit first.  At b = 4 coordinate 2m is the low
+nibble and 2m+1 the high nibble of byte m.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+from .codebook import Codebook
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        path = _build.LIB
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_build.SRC):
+            path = _build.build(force=True)
+        lib = ctypes.CDLL(path)
+        P = ctypes.c_void_p
+        lib.tqo_encode.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P,
+                                   ctypes.c_int32, P, P, P]
+        lib.tqo_encode.restype = ctypes.c_int
+        lib.tqo_scales.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P,
+                                   ctypes.c_int32, P]
+        lib.tqo_scales.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def code_bytes_per_vector(d: int, bits: int) -> int:
+    """Packed size of one vector: d*b/8 bytes (768 at d=1536, b=4)."""
+    if (d * bits) % 8:
+        raise ValueError("d*bits must be a multiple of 8")
+    return d * bits // 8
+
+
+def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook):
+    """Encode float32 rows X [n, d] with rotation R32 [d, d] and codebook cb.
+
+    Returns (codes uint8 [n, d] unpacked, norms float64 [n], scales float32 [n]).
+    Raises ValueError on a non-finite row.
+    """
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    R32 = np.ascontiguousarray(R32, dtype=np.float32)
+    n, d = X.shape
+    if R32.shape != (d, d) or cb.d != d:
+        raise ValueError("shape mismatch")
+    L = cb.levels
+    bounds = np.ascontiguousarray(cb.bounds, dtype=np.float64)
+    cents = np.ascontiguousarray(cb.cents, dtype=np.float64)
+    codes = np.empty((n, d), dtype=np.uint8)
+    norms = np.empty(n, dtype=np.float64)
+    scales = np.empty(n, dtype=np.float32)
+    bad = ctypes.c_int64(-1)
+    lib = _load()
+    st = lib.tqo_encode(X.ctypes.data, n, d, R32.ctypes.data, bounds.ctypes.data,
+                        L, codes.ctypes.data, norms.ctypes.data, ctypes.byref(bad))
+    if st == -2:
+        raise ValueError("non-finite input in row %d" % bad.value)
+    if st != 0:
+        raise RuntimeError("tqo_encode failed (%d)" % st)
+    st = lib.tqo_scales(codes.ctypes.data, norms.ctypes.data, n, d,
+                        cents.ctypes.data, L, scales.ctypes.data)
+    if st != 0:
+        raise RuntimeError("tqo_scales failed (%d)" % st)
+    return codes, norms, scales
+
+
+def pack_codes(codes: np.ndarray, bits: int) -> np.ndarray:
+    """Unpacked codes [n, d] -> canonical LSB-first bitstream rows [n, d*b/8]."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    n, d = codes.shape
+    nbytes = code_bytes_per_vector(d, bits)
+    if np.any(codes >> bits):
+        raise ValueError("code out of range for %d bits" % bits)
+    bitplanes = (codes[:, :, None] >> np.arange(bits, dtype=np.uint8)) & 1
+    flat = bitplanes.reshape(n, d * bits)
+    return np.packbits(flat, axis=1, bitorder="little")[:, :nbytes]
+
+
+def unpack_codes(packed: np.ndarray, d: int, bits: int) -> np.ndarray:
+    """Canonical packed rows [n, d*b/8] -> unpacked codes [n, d]."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    n = packed.shape[0]
+    flat = np.unpackbits(packed, axis=1, bitorder="little")[:, : d * bits]
+    planes = flat.reshape(n, d, bits).astype(np.uint8)
+    return np.sum(planes << np.arange(bits, dtype=np.uint8), axis=2, dtype=np.uint8)

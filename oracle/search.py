@@ -1,0 +1,127 @@
+"""Query rotation, scoring, allowlist filter, top-k and recall (oracle; test use only).
+
+* Query (section II-B step 2): q' = R32 q in float64.  The query is not
+  normalised -- ranking does not depend on its length and the score then
+  estimates <q, x>.
+* Score (section II-B step 5, length-renormalised scoring):
+      score_i = s_i * sum_j c[code_ij] * q'_j            (float64)
+* Filter (section III-B): a vector is eligible for query q iff the bit of its
+  tenant is set in q's allowlist bitmap (tenant t is bit t & 63 of 64-bit word
+  t >> 6).  Only eligible vectors are scored; the GPU's per-block summaries are
+  an optimisation with no counterpart here.
+* Top-k (section III-B, heap insert): eligible vectors ordered by
+  (score descending, id ascending), the first min(k, #eligible) kept, the rest
+  of the k slots padded with id -1 and score -inf.
+* Exact ground truth (section IV-A): the same ordering of <q, x_i> computed in
+  float64 on the original float32 vectors; Recall@k = |approx & exact| /
+  min(k, #eligible), averaged over queries.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def rotate_queries(R32: np.ndarray, Q: np.ndarray) -> np.ndarray:
+    """q'_b = R32 q_b for every row of Q, float64."""
+    R = np.asarray(R32, dtype=np.float32).astype(np.float64)
+    Q = np.atleast_2d(np.asarray(Q, dtype=np.float32)).astype(np.float64)
+    return Q @ R.T
+
+
+def allowed_mask(tenants, allow_row) -> np.ndarray:
+    """Eligibility of every vector for one query's allowlist (None -> all)."""
+    if allow_row is None or tenants is None:
+        return None
+    t = np.asarray(tenants, dtype=np.int64)
+    words = np.asarray(allow_row, dtype=np.uint64)
+    w = t >> 6
+    if np.any(w >= words.shape[0]):
+        raise ValueError("tenant id beyond the allowlist")
+    return ((words[w] >> (t & 63).astype(np.uint64)) & np.uint64(1)).astype(bool)
+
+
+def scores_for_ids(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
+                   qrot: np.ndarray, ids) -> np.ndarray:
+    """score_i for the given vector ids against one rotated query (float64)."""
+    ids = np.asarray(ids, dtype=np.int64)
+    xhat = np.asarray(cents, dtype=np.float64)[codes[ids]]
+    return np.asarray(scales, dtype=np.float64)[ids] * (xhat @ qrot)
+
+
+def _order(scores: np.ndarray, ids: np.ndarray, k: int):
+    """(score desc, id asc) ordering, first k."""
+    o = np.lexsort((ids, -scores))[:k]
+    return ids[o], scores[o]
+
+
+def _pad(ids, sc, k):
+    out_i = np.full(k, -1, dtype=np.int64)
+    out_s = np.full(k, -np.inf, dtype=np.float64)
+    out_i[: len(ids)] = ids
+    out_s[: len(sc)] = sc
+    return out_i, out_s
+
+
+def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
+           R32: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,
+           chunk: int = 65536):
+    """Top-k over TurboQuant codes for every query.  Returns (ids int64 [nq,k],
+    scores float64 [nq,k])."""
+    if k <= 0:
+        raise ValueError("k must be positive")
+    qrot = rotate_queries(R32, Q)
+    nq = qrot.shape[0]
+    n = codes.shape[0]
+    cents = np.asarray(cents, dtype=np.float64)
+    sc_all = np.empty((nq, n), dtype=np.float64)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        xhat = cents[codes[s:e]]                         # [m, d]
+        sc_all[:, s:e] = (xhat @ qrot.T).T * np.asarray(scales[s:e], dtype=np.float64)[None, :]
+    ids_out = np.empty((nq, k), dtype=np.int64)
+    sc_out = np.empty((nq, k), dtype=np.float64)
+    all_ids = np.arange(n, dtype=np.int64)
+    for b in range(nq):
+        m = allowed_mask(tenants, None if allow is None else allow[b])
+        ids = all_ids if m is None else all_ids[m]
+        sc = sc_all[b] if m is None else sc_all[b][m]
+        i, s_ = _order(sc, ids, k)
+        ids_out[b], sc_out[b] = _pad(i, s_, k)
+    return ids_out, sc_out
+
+
+def exact_search(X: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,
+                 chunk: int = 65536):
+    """Brute-force exact inner-product top-k (float64 on float32 inputs)."""
+    Q64 = np.atleast_2d(np.asarray(Q, dtype=np.float32)).astype(np.float64)
+    n = X.shape[0]
+    nq = Q64.shape[0]
+    sc_all = np.empty((nq, n), dtype=np.float64)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        sc_all[:, s:e] = Q64 @ np.asarray(X[s:e], dtype=np.float32).astype(np.float64).T
+    ids_out = np.empty((nq, k), dtype=np.int64)
+    sc_out = np.empty((nq, k), dtype=np.float64)
+    all_ids = np.arange(n, dtype=np.int64)
+    for b in range(nq):
+        m = allowed_mask(tenants, None if allow is None else allow[b])
+        ids = all_ids if m is None else all_ids[m]
+        sc = sc_all[b] if m is None else sc_all[b][m]
+        i, s_ = _order(sc, ids, k)
+        ids_out[b], sc_out[b] = _pad(i, s_, k)
+    return ids_out, sc_out
+
+
+def recall_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int) -> float:
+    """Mean over queries of |approx & exact| / min(k, #eligible) (section IV-A;
+    #eligible is read off the exact list's padding)."""
+    approx_ids = np.atleast_2d(approx_ids)[:, :k]
+    exact_ids = np.atleast_2d(exact_ids)[:, :k]
+    vals = []
+    for a, e in zip(approx_ids, exact_ids):
+        e_set = set(int(v) for v in e if v >= 0)
+        if not e_set:
+            continue
+        a_set = set(int(v) for v in a if v >= 0)
+        vals.append(len(a_set & e_set) / len(e_set))
+    return float(np.mean(vals)) if vals else float("nan")

@@ -1,0 +1,92 @@
+"""Pins of the oracle's search (section II-B step 5, section III-B filtering,
+section IV-A ground truth): scores equal inner products with the scaled
+reconstruction computed without rotating the query; filtering equals search
+on the subset; padding, ties and exact-match cases."""
+import numpy as np
+
+import oracle
+import synth
+
+
+def _index(n=300, d=128, bits=4, seed=0):
+    cb = oracle.lloyd_max(d, bits)
+    R64, R32 = oracle.haar_rotation(d, 42)
+    X = np.random.default_rng(seed).standard_normal((n, d)).astype(np.float32)
+    codes, norms, scales = oracle.encode(X, R32, cb)
+    return cb, R32, X, codes, scales
+
+
+def test_score_is_inner_product_with_reconstruction():
+    """score_i = <q, s_i R^T xhat_i> in the original space.  Rotating the query
+    with R^T instead of R, or dropping the scale, breaks this."""
+    cb, R32, X, codes, scales = _index()
+    Q = np.random.default_rng(9).standard_normal((5, X.shape[1])).astype(np.float32)
+    recon = scales[:, None].astype(np.float64) * (cb.cents[codes] @ R32.astype(np.float64))
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=X.shape[0])
+    for b in range(Q.shape[0]):
+        direct = recon @ Q[b].astype(np.float64)
+        np.testing.assert_allclose(sc[b], direct[ids[b]], rtol=1e-12, atol=1e-12)
+        assert np.all(np.diff(sc[b]) <= 0)
+        assert sorted(ids[b].tolist()) == list(range(X.shape[0]))
+    qr = oracle.rotate_queries(R32, Q[:1])[0]
+    np.testing.assert_allclose(oracle.scores_for_ids(codes, scales, cb.cents, qr, ids[0, :7]),
+                               sc[0, :7], rtol=1e-13)
+
+
+def test_scores_estimate_the_true_inner_product():
+    cb, R32, X, codes, scales = _index(n=400, d=1536)
+    Q = np.random.default_rng(10).standard_normal((4, 1536)).astype(np.float32)
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=400)
+    exact = Q.astype(np.float64) @ X.astype(np.float64).T
+    for b in range(4):
+        rel = np.abs(sc[b] - exact[b, ids[b]]) / (np.linalg.norm(Q[b]) * np.linalg.norm(X[ids[b]], axis=1))
+        assert rel.max() < 0.02
+
+
+def test_filter_equals_subset_search():
+    cb, R32, X, codes, scales = _index(n=500)
+    T = 7
+    tenants = synth.zipf_tenants(500, T, seed=3)
+    allowed = [np.array([0, 3]), np.array([5]), np.array([1, 2, 4, 6])]
+    bm = synth.allowlist_bitmap(allowed, T)
+    Q = np.random.default_rng(11).standard_normal((3, 128)).astype(np.float32)
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=10, tenants=tenants, allow=bm)
+    for b in range(3):
+        sub = np.flatnonzero(np.isin(tenants, allowed[b]))
+        i2, s2 = oracle.search(codes[sub], scales[sub], cb.cents, R32, Q[b:b + 1], k=10)
+        valid = i2[0] >= 0
+        assert np.array_equal(ids[b][valid], sub[i2[0][valid]])
+        np.testing.assert_allclose(sc[b], s2[0], rtol=1e-13)
+
+
+def test_padding_empty_allowlist_and_large_k():
+    cb, R32, X, codes, scales = _index(n=20)
+    Q = np.random.default_rng(12).standard_normal((2, 128)).astype(np.float32)
+    tenants = np.zeros(20, dtype=np.uint16)
+    empty = np.zeros((2, 1), dtype=np.uint64)
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=5, tenants=tenants, allow=empty)
+    assert np.all(ids == -1) and np.all(np.isneginf(sc))
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=25)
+    assert np.all(ids[:, 20:] == -1) and np.all(np.isneginf(sc[:, 20:]))
+    assert np.all(ids[:, :20] >= 0)
+
+
+def test_ties_order_by_id():
+    cb, R32, X, codes, scales = _index(n=10)
+    codes = np.concatenate([codes, codes[[3, 3, 7]]])
+    scales = np.concatenate([scales, scales[[3, 3, 7]]])
+    Q = X[3:4]
+    ids, sc = oracle.search(codes, scales, cb.cents, R32, Q, k=13)
+    pos = {int(i): p for p, i in enumerate(ids[0])}
+    assert pos[3] < pos[10] < pos[11]
+    assert sc[0][pos[3]] == sc[0][pos[10]] == sc[0][pos[11]]
+    assert pos[7] < pos[12]
+
+
+def test_exact_search_and_recall():
+    X = np.random.default_rng(13).standard_normal((200, 64)).astype(np.float32)
+    ids, sc = oracle.exact_search(X, X[[5, 17]], k=3)
+    assert ids[0, 0] == 5 and ids[1, 0] == 17
+    assert sc[0, 0] == np.dot(X[5].astype(np.float64), X[5].astype(np.float64))
+    assert oracle.recall_at_k(ids, ids, 3) == 1.0
+    assert oracle.recall_at_k(np.array([[5, -1, -1]]), np.array([[5, 9, 2]]), 3) == 1 / 3
