@@ -1,0 +1,209 @@
+/*
+ * tq.h -- C ABI of the TurboQuant search hot path for AMD Instinct MI355X
+ * (gfx950), as studied in "TurboVec" (arXiv 2607.16973).
+ *
+ * The library compresses L2-normalisable float32 embeddings with TurboQuant
+ * (section II-B: normalise, rotate by a fixed random orthogonal matrix,
+ * Lloyd-Max scalar quantisation against boundaries derived analytically from
+ * the post-rotation coordinate law, bit packing, length-renormalised scoring)
+ * and answers brute-force top-k inner-product queries over the codes, with
+ * kernel-level multi-tenant allowlist filtering (section III-B).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - Pointers named *_dev are device (HBM) pointers on the current HIP device;
+ *    pointers named *_host are host pointers.  The caller owns every pointer
+ *    argument; the library never keeps one after the call returns.  The
+ *    library owns only the opaque handles and the storage inside them.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device work is enqueued on it and is asynchronous: outputs are valid
+ *    once the stream has been synchronised, and inputs must stay alive and
+ *    unmodified until then.
+ *  - Every function returns a tq_status and never throws or aborts.
+ *    Arguments are validated before any device work is enqueued; on error
+ *    nothing is enqueued and tq_last_error() describes the failure.
+ *  - Functions that need a GPU return TQ_EDEVICE when none is usable.  The
+ *    codebook and rotation constructors are host-only and work without one.
+ *  - Sizes: 64 <= d <= 2048 with d % 64 == 0; bits in {1, 2, 3, 4, 8}
+ *    (bits == 3 additionally needs d % 128 == 0); k in 1..256.
+ */
+#ifndef TQ_H
+#define TQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TQ_OK = 0,
+    TQ_EINVAL = -1,          /* bad argument (null pointer, bad size, bad id) */
+    TQ_ENOMEM = -2,          /* device or host allocation failed */
+    TQ_EDEVICE = -3,         /* no usable GPU, or a HIP runtime error */
+    TQ_EUNSUPPORTED = -4     /* valid request outside what this build supports */
+} tq_status;
+
+typedef struct tq_codebook tq_codebook;
+typedef struct tq_rotation tq_rotation;
+typedef struct tq_index tq_index;
+
+/* Message for the last failed call on this thread (static storage, never
+ * NULL; "" if none). */
+const char *tq_last_error(void);
+
+/* Library version string, e.g. "tq 0.1.0 gfx950". */
+const char *tq_version(void);
+
+/* ------------------------------------------------------------------ a1 ----
+ * build_codebook(d, b) -- section II-B step 3.  Lloyd-Max scalar quantiser
+ * with L = 2^bits levels for the law of one coordinate of a uniformly random
+ * unit vector in R^d (density proportional to (1 - x^2)^((d-3)/2), the
+ * paper's "Beta / N(0, 1/d)" marginal).  No data is involved: the tables
+ * depend on (d, bits) only.  Host-only, float64, deterministic.
+ * Errors: TQ_EINVAL for d out of range, TQ_EUNSUPPORTED for other bits,
+ * TQ_EINVAL for out == NULL. */
+tq_status tq_build_codebook(int32_t d, int32_t bits, tq_codebook **out);
+
+/* Copies the float64 tables: bounds_host[L-1] (strictly increasing, the
+ * middle one exactly 0) and cents_host[L] (strictly increasing,
+ * antisymmetric).  Either pointer may be NULL to skip it. */
+tq_status tq_codebook_tables(const tq_codebook *cb, double *bounds_host,
+                             double *cents_host);
+
+/* Per-coordinate distortion E[(X - Q(X))^2] of the codebook (float64). */
+tq_status tq_codebook_mse(const tq_codebook *cb, double *mse_out);
+
+void tq_codebook_free(tq_codebook *cb);
+
+/* ------------------------------------------------------------------ a2 ----
+ * Rotation R(seed) -- section II-B step 2, "a fixed random orthogonal
+ * matrix".  Haar-distributed d x d orthogonal matrix: a d x d matrix of
+ * standard normals (SplitMix64 counter stream of `seed`, 53-bit uniforms,
+ * Box-Muller on consecutive pairs, row-major) factored by Householder QR,
+ * with columns sign-corrected so the triangular factor has a positive
+ * diagonal; stored as float32 row-major.  y = R x, i.e. y_j = sum_k R[j][k]
+ * x_k.  Host-only (the device copy is made on first device use).
+ * Errors: TQ_EINVAL for d out of range or out == NULL. */
+tq_status tq_rotation_create(int32_t d, uint64_t seed, tq_rotation **out);
+
+/* Copies the float32 matrix, row-major, d*d floats, to R_host. */
+tq_status tq_rotation_matrix(const tq_rotation *rot, float *R_host);
+
+void tq_rotation_free(tq_rotation *rot);
+
+/* -------------------------------------------------------------- a3 + a4 ----
+ * rotate_quantize(X) -> codes + scales -- section II-B steps 1-5.
+ * For each float32 row x of X_dev [n][d] (row-major):
+ *   n_x    = ||x|| (float64);
+ *   code_j = number of boundaries t_i with fl64(t_i * n_x) <= (R x)_j, where
+ *            (R x)_j is the float64 sum over k = 0..d-1 in order (a value on
+ *            a boundary goes to the upper cell; a zero row codes to L/2);
+ *   scale  = n_x / ||c[code]|| (float64, stored float32): the per-vector
+ *            length-renormalisation scalar; 0 for a zero row.
+ * The rotation runs on the matrix cores (float32 MFMA with float64
+ * accumulation); coordinates whose MFMA value lies within a proven error
+ * bound of a boundary are recomputed exactly, so the codes equal the
+ * definition above bit for bit.
+ * Outputs: codes_dev [n][d*bits/8] bytes in the canonical layout (one
+ * little-endian bitstream per row, coordinate j at bits [bits*j, bits*j +
+ * bits), least significant bit first); scales_dev [n] float32.
+ * Errors: TQ_EINVAL for a null pointer, n < 0, or mismatched (d, bits)
+ * between cb and rot; a non-finite input value makes the call return
+ * TQ_EINVAL after synchronising `stream` (the outputs are then unspecified). */
+tq_status tq_rotate_quantize(const tq_codebook *cb, const tq_rotation *rot,
+                             const float *X_dev, int64_t n, uint8_t *codes_dev,
+                             float *scales_dev, void *stream);
+
+/* ------------------------------------------------------------------ a5 ----
+ * q' = R q for every row of Q_dev [nq][d] float32 -> Qrot_dev [nq][d]
+ * float32 (section II-B step 2 applied to queries; queries are not
+ * normalised).  Exposed so the query rotation can be checked on its own;
+ * tq_search performs it internally. */
+tq_status tq_rotate_queries(const tq_rotation *rot, const float *Q_dev,
+                            int64_t nq, float *Qrot_dev, void *stream);
+
+/* ------------------------------------------------------------ index -------
+ * TurboQuantIndex (section III-A): flat scan, positional ids (the i-th
+ * vector added has id i), online ingest with no training.  n_tenants in
+ * 1..65535 sets the allowlist width W = ceil(n_tenants / 64) words.  The
+ * codebook and rotation are copied; the caller may free them afterwards. */
+tq_status tq_index_create(const tq_codebook *cb, const tq_rotation *rot,
+                          int32_t n_tenants, tq_index **out);
+
+/* Pre-allocates device storage for `capacity` vectors. */
+tq_status tq_index_reserve(tq_index *idx, int64_t capacity);
+
+/* add(): encodes X_dev [n][d] float32 exactly as tq_rotate_quantize and
+ * appends the vectors, with tenant ids tenants_dev [n] uint16 (NULL = tenant
+ * 0 for all).  A tenant id >= n_tenants is reported as TQ_EINVAL after
+ * synchronising `stream` (the vectors are then not added). */
+tq_status tq_index_add(tq_index *idx, const float *X_dev,
+                       const uint16_t *tenants_dev, int64_t n, void *stream);
+
+/* Appends vectors given as canonical codes_dev [n][d*bits/8] and scales_dev
+ * [n] float32 (as produced by tq_rotate_quantize), with tenants as above. */
+tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev,
+                             const float *scales_dev,
+                             const uint16_t *tenants_dev, int64_t n,
+                             void *stream);
+
+/* Number of vectors in the index. */
+tq_status tq_index_size(const tq_index *idx, int64_t *n_out);
+
+/* Copies the index content back in the canonical layout: codes_dev
+ * [n][d*bits/8], scales_dev [n], tenants_dev [n]; any may be NULL. */
+tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev,
+                          float *scales_dev, uint16_t *tenants_dev,
+                          void *stream);
+
+void tq_index_free(tq_index *idx);
+
+/* ------------------------------------------------------------ search ------
+ * search(Q, k, allowlist) -> ids + scores -- section II-B step 5 and section
+ * III-B.  For each query row q of Q_dev [nq][d] float32 (not normalised):
+ *   score_i = scale_i * sum_j c[code_ij] * (R q)_j
+ * over the vectors whose tenant bit is set in the query's allowlist row
+ * allow_dev[q*W .. q*W+W) (uint64 words; tenant t is bit (t & 63) of word
+ * t >> 6; allow_dev == NULL allows every vector).  64-vector blocks whose
+ * tenant summary does not meet the allowlist are skipped before any of
+ * their code bytes are read; disallowed vectors inside scanned blocks are
+ * dropped at top-k insertion.
+ * Output per query: the min(k, #allowed) best vectors ordered by (score
+ * descending, id ascending) in ids_dev [nq][k] int64 and scores_dev [nq][k]
+ * float32; unused slots hold id -1 and score -inf.
+ * The search needs a device workspace; tq_search allocates it on `stream`
+ * (stream-ordered allocation) and releases it before returning. */
+tq_status tq_search(const tq_index *idx, const float *Q_dev, int64_t nq,
+                    int32_t k, const uint64_t *allow_dev, int64_t *ids_dev,
+                    float *scores_dev, void *stream);
+
+/* Scan path selection for tq_search_ex. */
+typedef enum {
+    TQ_PATH_AUTO = 0,     /* library choice */
+    TQ_PATH_LUT = 1,      /* one pass per query: LDS lookup tables */
+    TQ_PATH_MFMA = 2      /* query tiles on the matrix cores + exact rescoring */
+} tq_path;
+
+/* Flag ORed into `path`: Q_dev already holds rotated queries R q (for
+ * instance from tq_rotate_queries), so the rotation step is skipped. */
+#define TQ_FLAG_PREROTATED 0x100
+
+/* Workspace size in bytes needed by tq_search_ex for (nq, k, path). */
+tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k,
+                                   int32_t path, size_t *bytes_out);
+
+/* tq_search with an explicit path and a caller-provided device workspace of
+ * at least tq_search_workspace_size() bytes (256-byte aligned).  Allocates
+ * nothing.  Calls sharing one workspace must not overlap in time. */
+tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq,
+                       int32_t k, const uint64_t *allow_dev, int32_t path,
+                       void *workspace_dev, size_t workspace_bytes,
+                       int64_t *ids_dev, float *scores_dev, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TQ_H */

@@ -15,7 +15,8 @@
  *                  sequential float64 sum over j, stored as float32
  *                  (the per-vector length-renormalisation scalar: the
  *                  reconstruction s * R^T xhat has the length of x)
- * Step 4 (bit packing) is done by the Python wrapper.
+ * Step 4 (bit packing) is done by the Python wrapper.  Optionally the rotated
+ * values S_j are returned too (rot_out, float64 [n][d]).
  *
  * Build with -ffp-contract=off so that no multiply-add is fused: the
  * definition rounds every product and every sum on its own.
@@ -29,7 +30,7 @@
  * (its index is written to *bad_row). */
 int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
                const double *bounds, int32_t L, uint8_t *codes,
-               double *norm_out, int64_t *bad_row)
+               double *norm_out, double *rot_out, int64_t *bad_row)
 {
     if (!X || !R || !bounds || !codes || n < 0 || d <= 0 || L < 2 || L > 256)
         return -1;
@@ -71,6 +72,7 @@ int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
             if (norm_out) norm_out[i] = nrm;
             if (nrm == 0.0) {
                 memset(c, L / 2, (size_t)d);
+                if (rot_out) memset(rot_out + (size_t)i * d, 0, sizeof(double) * (size_t)d);
                 continue;
             }
             for (int32_t t = 0; t < L - 1; ++t) {
@@ -86,6 +88,8 @@ int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
                     S[j] = S[j] + prod;
                 }
             }
+            if (rot_out)
+                for (int32_t j = 0; j < d; ++j) rot_out[(size_t)i * d + j] = S[j];
             for (int32_t j = 0; j < d; ++j) {
                 int cnt = 0;
                 for (int32_t t = 0; t < L - 1; ++t) cnt += (T[t] <= S[j]);

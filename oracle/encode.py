@@ -31,7 +31,7 @@ def _load():
         lib = ctypes.CDLL(path)
         P = ctypes.c_void_p
         lib.tqo_encode.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P,
-                                   ctypes.c_int32, P, P, P]
+                                   ctypes.c_int32, P, P, P, P]
         lib.tqo_encode.restype = ctypes.c_int
         lib.tqo_scales.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P,
                                    ctypes.c_int32, P]
@@ -47,10 +47,11 @@ def code_bytes_per_vector(d: int, bits: int) -> int:
     return d * bits // 8
 
 
-def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook):
+def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook, return_rotated: bool = False):
     """Encode float32 rows X [n, d] with rotation R32 [d, d] and codebook cb.
 
-    Returns (codes uint8 [n, d] unpacked, norms float64 [n], scales float32 [n]).
+    Returns (codes uint8 [n, d] unpacked, norms float64 [n], scales float32 [n])
+    and, with return_rotated, also the rotated values S float64 [n, d].
     Raises ValueError on a non-finite row.
     """
     X = np.ascontiguousarray(X, dtype=np.float32)
@@ -64,10 +65,12 @@ def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook):
     codes = np.empty((n, d), dtype=np.uint8)
     norms = np.empty(n, dtype=np.float64)
     scales = np.empty(n, dtype=np.float32)
+    rot = np.empty((n, d), dtype=np.float64) if return_rotated else None
     bad = ctypes.c_int64(-1)
     lib = _load()
     st = lib.tqo_encode(X.ctypes.data, n, d, R32.ctypes.data, bounds.ctypes.data,
-                        L, codes.ctypes.data, norms.ctypes.data, ctypes.byref(bad))
+                        L, codes.ctypes.data, norms.ctypes.data,
+                        rot.ctypes.data if rot is not None else None, ctypes.byref(bad))
     if st == -2:
         raise ValueError("non-finite input in row %d" % bad.value)
     if st != 0:
@@ -76,6 +79,8 @@ def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook):
                         cents.ctypes.data, L, scales.ctypes.data)
     if st != 0:
         raise RuntimeError("tqo_scales failed (%d)" % st)
+    if return_rotated:
+        return codes, norms, scales, rot
     return codes, norms, scales
 
 

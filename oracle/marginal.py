@@ -27,7 +27,7 @@ import numpy as np
 import functools
 
 import mpmath
-from scipy.special import betaincc
+from scipy.special import betainc, betaincc
 
 
 @functools.lru_cache(maxsize=None)
@@ -68,34 +68,65 @@ def cdf(x, d: int):
     return np.where(x >= 0, 1.0 - t, t)
 
 
+def _central_prob(x, d: int):
+    """P(|X| <= x) = I_{x^2}(1/2, (d-1)/2) for x >= 0 (small and exact near 0)."""
+    return betainc(0.5, (d - 1) / 2.0, x * x)
+
+
 def cell_mass(a, b, d: int):
-    """P(a < X <= b).  For 0 <= a < b this is tail(a) - tail(b), which keeps
-    full relative precision in the outer cells."""
+    """P(a < X <= b).  For 0 <= a < b the two CDF values are differenced in the
+    better-conditioned form: through the upper tails tail(a) - tail(b) when
+    tail(a) < 1/4 (outer cells), else through the central probabilities
+    (I_{b^2} - I_{a^2}) / 2 (inner cells, where those are the small numbers)."""
     a = np.asarray(a, dtype=np.float64)
     b = np.asarray(b, dtype=np.float64)
-    pos = a >= 0
-    neg = b <= 0
-    out = np.empty(np.broadcast(a, b).shape, dtype=np.float64)
     aa, bb = np.broadcast_arrays(a, b)
-    if np.any(pos):
-        out[pos] = tail_prob(aa[pos], d) - tail_prob(bb[pos], d)
-    if np.any(neg):
-        out[neg] = tail_prob(-bb[neg], d) - tail_prob(-aa[neg], d)
+    out = np.empty(aa.shape, dtype=np.float64)
+
+    def pos_mass(lo, hi):
+        ta = tail_prob(lo, d)
+        outer = ta < 0.25
+        res = np.empty(lo.shape, dtype=np.float64)
+        res[outer] = ta[outer] - tail_prob(hi[outer], d)
+        inner = ~outer
+        res[inner] = 0.5 * (_central_prob(hi[inner], d) - _central_prob(lo[inner], d))
+        return res
+
+    pos = aa >= 0
+    neg = bb <= 0
     mid = ~(pos | neg)
+    if np.any(pos):
+        out[pos] = pos_mass(aa[pos], bb[pos])
+    if np.any(neg):
+        out[neg] = pos_mass(-bb[neg], -aa[neg])
     if np.any(mid):
-        out[mid] = (0.5 - tail_prob(-aa[mid], d)) + (0.5 - tail_prob(bb[mid], d))
+        out[mid] = 0.5 * (_central_prob(-aa[mid], d) + _central_prob(bb[mid], d))
     return out
 
 
 def cell_first_moment(a, b, d: int):
-    """int_a^b x f_d(x) dx in closed form (antiderivative of x(1-x^2)^((d-3)/2))."""
+    """int_a^b x f_d(x) dx in closed form (antiderivative of x(1-x^2)^((d-3)/2)):
+    C_d [(1-a^2)^e - (1-b^2)^e] / (d-1), e = (d-1)/2.  For |a| <= |b| the
+    difference is evaluated without cancellation as
+        (1-b^2)^e * expm1(e * log1p((b-a)(b+a) / (1-b^2)))
+    (and symmetrically), since (1-a^2)/(1-b^2) = 1 + (b-a)(b+a)/(1-b^2)."""
     a = np.asarray(a, dtype=np.float64)
     b = np.asarray(b, dtype=np.float64)
+    a, b = np.broadcast_arrays(a, b)
     e = 0.5 * (d - 1)
-    with np.errstate(divide="ignore"):
-        ga = np.exp(e * np.log1p(-a * a))   # (1-a^2)^((d-1)/2); 0 at |a| = 1
-        gb = np.exp(e * np.log1p(-b * b))
-    return norm_const(d) * (ga - gb) / (d - 1)
+    out = np.empty(a.shape, dtype=np.float64)
+    swap = np.abs(a) > np.abs(b)          # always factor out the smaller power
+    lo = np.where(swap, b, a)             # |lo| <= |hi|
+    hi = np.where(swap, a, b)
+    sign = np.where(swap, -1.0, 1.0)
+    edge = np.abs(hi) >= 1.0
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ghi = np.exp(e * np.log1p(-hi * hi))
+        ratio = (hi - lo) * (hi + lo) / ((1.0 - hi) * (1.0 + hi))
+        diff = ghi * np.expm1(e * np.log1p(ratio))
+        glo = np.exp(e * np.log1p(-lo * lo))
+    out = np.where(edge, glo, diff) * sign
+    return norm_const(d) * out / (d - 1)
 
 
 def cell_second_moment(a, b, d: int):

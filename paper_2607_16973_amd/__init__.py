@@ -1,0 +1,214 @@
+"""TurboQuant search hot path on AMD Instinct MI355X (gfx950).
+
+Python face of libtq.so (see include/tq.h).  torch provides device memory and
+the current stream; every step of the method runs in the HIP library.
+
+    cb = Codebook(1536, 4)                     # analytic Lloyd-Max tables
+    rot = Rotation(1536, seed=42)              # Haar rotation, float32
+    idx = Index(cb, rot, n_tenants=1)
+    idx.add(X)                                 # X: cuda float32 [n, d]
+    ids, scores = idx.search(Q, k=10)          # Q: cuda float32 [nq, d]
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+
+from ._lib import FLAG_PREROTATED, PATHS, TQError, check, lib
+
+__all__ = ["Codebook", "Rotation", "Index", "TQError", "rotate_quantize",
+           "rotate_queries", "version"]
+
+
+def version() -> str:
+    return lib.tq_version().decode()
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(device=None):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dev_ptr(t, dtype, name, ndim=None):
+    torch = _torch()
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) torch tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must have dtype %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError("%s must have %d dimensions" % (name, ndim))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Codebook:
+    """Lloyd-Max boundaries/centroids for (d, bits) -- host tables (float64)."""
+
+    def __init__(self, d: int, bits: int = 4):
+        h = ctypes.c_void_p()
+        check(lib.tq_build_codebook(d, bits, ctypes.byref(h)))
+        self._h = h
+        self.d, self.bits = d, bits
+        L = 1 << bits
+        self.bounds = np.empty(L - 1, dtype=np.float64)
+        self.cents = np.empty(L, dtype=np.float64)
+        check(lib.tq_codebook_tables(h, self.bounds.ctypes.data_as(ctypes.c_void_p),
+                                     self.cents.ctypes.data_as(ctypes.c_void_p)))
+        m = ctypes.c_double()
+        check(lib.tq_codebook_mse(h, ctypes.byref(m)))
+        self.mse = m.value
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            lib.tq_codebook_free(h)
+            self._h = None
+
+
+class Rotation:
+    """Seeded Haar orthogonal rotation, float32 row-major."""
+
+    def __init__(self, d: int, seed: int = 42):
+        h = ctypes.c_void_p()
+        check(lib.tq_rotation_create(d, ctypes.c_uint64(seed & 0xFFFFFFFFFFFFFFFF), ctypes.byref(h)))
+        self._h = h
+        self.d, self.seed = d, seed
+
+    def matrix(self) -> np.ndarray:
+        R = np.empty((self.d, self.d), dtype=np.float32)
+        check(lib.tq_rotation_matrix(self._h, R.ctypes.data_as(ctypes.c_void_p)))
+        return R
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            lib.tq_rotation_free(h)
+            self._h = None
+
+
+def rotate_quantize(cb: Codebook, rot: Rotation, X, codes=None, scales=None):
+    """Encode rows of X (cuda float32 [n, d]) -> (canonical codes uint8
+    [n, d*bits/8], scales float32 [n]).  Synchronises the current stream."""
+    torch = _torch()
+    n = X.shape[0]
+    if codes is None:
+        codes = torch.empty((n, cb.d * cb.bits // 8), dtype=torch.uint8, device=X.device)
+    if scales is None:
+        scales = torch.empty((n,), dtype=torch.float32, device=X.device)
+    check(lib.tq_rotate_quantize(cb._h, rot._h, _dev_ptr(X, torch.float32, "X", 2), n,
+                                 _dev_ptr(codes, torch.uint8, "codes"),
+                                 _dev_ptr(scales, torch.float32, "scales"), _stream(X.device)))
+    return codes, scales
+
+
+def rotate_queries(rot: Rotation, Q, out=None):
+    """q' = R q for every row of Q (cuda float32 [nq, d])."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(Q)
+    check(lib.tq_rotate_queries(rot._h, _dev_ptr(Q, torch.float32, "Q", 2), Q.shape[0],
+                                _dev_ptr(out, torch.float32, "out"), _stream(Q.device)))
+    return out
+
+
+class Index:
+    """Flat TurboQuant index (positional ids) on the current GPU."""
+
+    def __init__(self, cb: Codebook, rot: Rotation, n_tenants: int = 1):
+        h = ctypes.c_void_p()
+        check(lib.tq_index_create(cb._h, rot._h, n_tenants, ctypes.byref(h)))
+        self._h = h
+        self.d, self.bits, self.n_tenants = cb.d, cb.bits, n_tenants
+        self.words = (n_tenants + 63) // 64
+        self._ws = None
+
+    def __len__(self) -> int:
+        n = ctypes.c_int64()
+        check(lib.tq_index_size(self._h, ctypes.byref(n)))
+        return n.value
+
+    def reserve(self, capacity: int) -> None:
+        check(lib.tq_index_reserve(self._h, capacity))
+
+    def add(self, X, tenants=None) -> None:
+        torch = _torch()
+        check(lib.tq_index_add(self._h, _dev_ptr(X, torch.float32, "X", 2),
+                               _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
+                               X.shape[0], _stream(X.device)))
+
+    def add_codes(self, codes, scales, tenants=None) -> None:
+        torch = _torch()
+        check(lib.tq_index_add_codes(self._h, _dev_ptr(codes, torch.uint8, "codes", 2),
+                                     _dev_ptr(scales, torch.float32, "scales", 1),
+                                     _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
+                                     codes.shape[0], _stream(codes.device)))
+
+    def export(self, device="cuda"):
+        torch = _torch()
+        n = len(self)
+        codes = torch.empty((n, self.d * self.bits // 8), dtype=torch.uint8, device=device)
+        scales = torch.empty((n,), dtype=torch.float32, device=device)
+        tenants = torch.empty((n,), dtype=torch.int16, device=device)
+        check(lib.tq_index_export(self._h, ctypes.c_void_p(codes.data_ptr()),
+                                  ctypes.c_void_p(scales.data_ptr()),
+                                  ctypes.c_void_p(tenants.data_ptr()), _stream(codes.device)))
+        return codes, scales, tenants
+
+    def workspace_bytes(self, nq: int, k: int, path: str = "auto") -> int:
+        b = ctypes.c_size_t()
+        check(lib.tq_search_workspace_size(self._h, nq, k, PATHS[path], ctypes.byref(b)))
+        return b.value
+
+    def search(self, Q, k: int, allow=None, path: str = "auto", ids=None, scores=None,
+               workspace=None, prerotated: bool = False):
+        """Top-k per query row of Q (cuda float32 [nq, d]).  allow: cuda int64
+        tensor [nq, words] (bit patterns of the uint64 allowlist words) or None.
+        prerotated: Q already holds R q (see rotate_queries).
+        Returns (ids int64 [nq, k], scores float32 [nq, k])."""
+        torch = _torch()
+        nq = Q.shape[0]
+        if ids is None:
+            ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
+        if scores is None:
+            scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        if allow is not None and tuple(allow.shape) != (nq, self.words):
+            raise ValueError("allow must have shape (nq, %d)" % self.words)
+        need = self.workspace_bytes(nq, k, path)
+        if workspace is None:
+            if self._ws is None or self._ws.numel() < need:
+                self._ws = torch.empty((need,), dtype=torch.uint8, device=Q.device)
+            workspace = self._ws
+        check(lib.tq_search_ex(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k,
+                               _dev_ptr(allow, torch.int64, "allow") if allow is not None else None,
+                               PATHS[path] | (FLAG_PREROTATED if prerotated else 0),
+                               ctypes.c_void_p(workspace.data_ptr()),
+                               workspace.numel(), _dev_ptr(ids, torch.int64, "ids"),
+                               _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
+        return ids, scores
+
+    def search_alloc(self, Q, k: int, allow=None):
+        """tq_search: the library allocates its own stream-ordered workspace."""
+        torch = _torch()
+        nq = Q.shape[0]
+        ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
+        scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        check(lib.tq_search(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k,
+                            _dev_ptr(allow, torch.int64, "allow") if allow is not None else None,
+                            _dev_ptr(ids, torch.int64, "ids"),
+                            _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
+        return ids, scores
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            lib.tq_index_free(h)
+            self._h = None

@@ -1,0 +1,570 @@
+// C ABI of libtq: argument validation, handles, device storage, dispatch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "tq_internal.h"
+
+namespace tq {
+
+namespace {
+thread_local std::string g_err;
+
+bool valid_bits(int b) { return b == 1 || b == 2 || b == 3 || b == 4 || b == 8; }
+
+tq_status check_d(int32_t d) {
+    if (d < 64 || d > 2048 || d % 64 != 0)
+        return fail(TQ_EINVAL, "d must be a multiple of 64 in [64, 2048], got " + std::to_string(d));
+    return TQ_OK;
+}
+
+tq_status check_geometry(int32_t d, int32_t bits) {
+    tq_status st = check_d(d);
+    if (st != TQ_OK) return st;
+    if (!valid_bits(bits))
+        return fail(TQ_EUNSUPPORTED, "bits must be one of 1, 2, 3, 4, 8; got " + std::to_string(bits));
+    if ((bits == 1 || bits == 3) && d % 128 != 0)
+        return fail(TQ_EINVAL, "bits = 1 or 3 needs d % 128 == 0");
+    return TQ_OK;
+}
+
+tq_status device_ready() {
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || n <= 0) {
+        (void)hipGetLastError();
+        return fail(TQ_EDEVICE, "no usable GPU (hipGetDeviceCount: " +
+                                    std::string(hipGetErrorString(e)) + ")");
+    }
+    return TQ_OK;
+}
+
+tq_status hip_fail(hipError_t e, const char *what) {
+    (void)hipGetLastError();
+    if (e == hipErrorOutOfMemory)
+        return fail(TQ_ENOMEM, std::string(what) + ": out of device memory");
+    return fail(TQ_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+void fill_codebook_dev(const CodebookTables &t, CodebookDev *cd) {
+    std::memset(cd, 0, sizeof(*cd));
+    cd->bits = t.bits;
+    cd->levels = 1 << t.bits;
+    for (int i = 0; i < cd->levels - 1; ++i) cd->bounds[i] = t.bounds[i];
+    for (int i = 0; i < cd->levels; ++i) {
+        cd->cents32[i] = (float)t.cents[i];
+        const double c = t.cents[i];
+        const double sq = c * c;
+        cd->cent_sq[i] = sq;
+    }
+}
+
+// Device copy of the rotation matrix on the current device.
+tq_status rotation_dev(const tq_rotation *rot, const float **out) {
+    std::lock_guard<std::mutex> lk(rot->mu);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (rot->R_dev && rot->R_dev_device == dev) {
+        *out = rot->R_dev;
+        return TQ_OK;
+    }
+    if (rot->R_dev) {
+        (void)hipFree(rot->R_dev);
+        rot->R_dev = nullptr;
+    }
+    const size_t bytes = sizeof(float) * rot->R.size();
+    e = hipMalloc(&rot->R_dev, bytes);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(rotation)");
+    e = hipMemcpy(rot->R_dev, rot->R.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(rotation)");
+    rot->R_dev_device = dev;
+    *out = rot->R_dev;
+    return TQ_OK;
+}
+
+// Stream-ordered scratch allocation released on destruction.
+struct AsyncBuf {
+    void *p = nullptr;
+    hipStream_t s = nullptr;
+    hipError_t alloc(size_t bytes, hipStream_t stream) {
+        s = stream;
+        return hipMallocAsync(&p, bytes, stream);
+    }
+    ~AsyncBuf() {
+        if (p) (void)hipFreeAsync(p, s);
+    }
+};
+
+}  // namespace
+
+void set_error(const std::string &msg) { g_err = msg; }
+
+tq_status fail(tq_status st, const std::string &msg) {
+    g_err = msg;
+    return st;
+}
+
+}  // namespace tq
+
+using namespace tq;
+
+struct tq_index {
+    CodebookTables cb;
+    CodebookDev cbdev;
+    tq_rotation rot;
+    int d = 0, bits = 0, T = 0, W = 0, chunks = 0;
+    int64_t n = 0, cap = 0;
+    uint8_t *codes = nullptr;      // blocked store, cap/64 blocks
+    float *scales = nullptr;       // cap
+    uint16_t *tenants = nullptr;   // cap
+    uint64_t *summ = nullptr;      // cap/64 * W
+    float *cents_dev = nullptr;    // levels
+    int *status = nullptr;         // device status word
+    int device = -1;
+};
+
+namespace {
+
+size_t block_bytes(const tq_index *x) { return (size_t)x->chunks * 1024; }
+
+void index_release(tq_index *x) {
+    if (x->codes) (void)hipFree(x->codes);
+    if (x->scales) (void)hipFree(x->scales);
+    if (x->tenants) (void)hipFree(x->tenants);
+    if (x->summ) (void)hipFree(x->summ);
+    if (x->cents_dev) (void)hipFree(x->cents_dev);
+    if (x->status) (void)hipFree(x->status);
+    x->codes = nullptr;
+    x->scales = nullptr;
+    x->tenants = nullptr;
+    x->summ = nullptr;
+    x->cents_dev = nullptr;
+    x->status = nullptr;
+}
+
+tq_status index_device_init(tq_index *x) {
+    if (x->cents_dev) return TQ_OK;
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    hipError_t e = hipGetDevice(&x->device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    e = hipMalloc(&x->cents_dev, sizeof(float) * 256);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(centroids)");
+    e = hipMemcpy(x->cents_dev, x->cbdev.cents32, sizeof(float) * 256, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(centroids)");
+    e = hipMalloc(&x->status, 256);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(status)");
+    e = hipMemset(x->status, 0, 256);
+    if (e != hipSuccess) return hip_fail(e, "hipMemset(status)");
+    return TQ_OK;
+}
+
+tq_status index_grow(tq_index *x, int64_t need, hipStream_t stream) {
+    tq_status st = index_device_init(x);
+    if (st != TQ_OK) return st;
+    if (need <= x->cap) return TQ_OK;
+    int64_t cap = std::max<int64_t>(need, x->cap + x->cap / 2);
+    cap = (cap + 63) / 64 * 64;
+    const int64_t nb = cap / 64;
+    uint8_t *codes = nullptr;
+    float *scales = nullptr;
+    uint16_t *ten = nullptr;
+    uint64_t *summ = nullptr;
+    hipError_t e;
+    if ((e = hipMalloc(&codes, nb * block_bytes(x))) != hipSuccess ||
+        (e = hipMalloc(&scales, cap * sizeof(float))) != hipSuccess ||
+        (e = hipMalloc(&ten, cap * sizeof(uint16_t))) != hipSuccess ||
+        (e = hipMalloc(&summ, nb * x->W * sizeof(uint64_t))) != hipSuccess) {
+        if (codes) (void)hipFree(codes);
+        if (scales) (void)hipFree(scales);
+        if (ten) (void)hipFree(ten);
+        if (summ) (void)hipFree(summ);
+        return hip_fail(e, "hipMalloc(index storage)");
+    }
+    e = hipMemsetAsync(codes, 0, nb * block_bytes(x), stream);
+    if (e == hipSuccess) e = hipMemsetAsync(scales, 0, cap * sizeof(float), stream);
+    if (e == hipSuccess) e = hipMemsetAsync(ten, 0, cap * sizeof(uint16_t), stream);
+    if (e == hipSuccess) e = hipMemsetAsync(summ, 0, nb * x->W * sizeof(uint64_t), stream);
+    if (e == hipSuccess && x->cap > 0) {
+        const int64_t ob = x->cap / 64;
+        e = hipMemcpyAsync(codes, x->codes, ob * block_bytes(x), hipMemcpyDeviceToDevice, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(scales, x->scales, x->cap * sizeof(float), hipMemcpyDeviceToDevice, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(ten, x->tenants, x->cap * sizeof(uint16_t), hipMemcpyDeviceToDevice, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(summ, x->summ, ob * x->W * sizeof(uint64_t), hipMemcpyDeviceToDevice, stream);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) {
+        (void)hipFree(codes);
+        (void)hipFree(scales);
+        (void)hipFree(ten);
+        (void)hipFree(summ);
+        return hip_fail(e, "index growth");
+    }
+    if (x->codes) (void)hipFree(x->codes);
+    if (x->scales) (void)hipFree(x->scales);
+    if (x->tenants) (void)hipFree(x->tenants);
+    if (x->summ) (void)hipFree(x->summ);
+    x->codes = codes;
+    x->scales = scales;
+    x->tenants = ten;
+    x->summ = summ;
+    x->cap = cap;
+    return TQ_OK;
+}
+
+tq_status read_status(int *status_dev, hipStream_t stream, int *out) {
+    int h = 0;
+    hipError_t e = hipMemcpyAsync(&h, status_dev, sizeof(int), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e, "status read");
+    *out = h;
+    return TQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tq_last_error(void) { return g_err.c_str(); }
+
+const char *tq_version(void) { return "tq 0.1.0 gfx950"; }
+
+tq_status tq_build_codebook(int32_t d, int32_t bits, tq_codebook **out) {
+    if (!out) return fail(TQ_EINVAL, "out is NULL");
+    *out = nullptr;
+    tq_status st = check_geometry(d, bits);
+    if (st != TQ_OK) return st;
+    tq_codebook *cb = new (std::nothrow) tq_codebook();
+    if (!cb) return fail(TQ_ENOMEM, "host allocation failed");
+    if (!solve_lloyd_max(d, bits, &cb->t)) {
+        delete cb;
+        return TQ_EINVAL;
+    }
+    *out = cb;
+    return TQ_OK;
+}
+
+tq_status tq_codebook_tables(const tq_codebook *cb, double *bounds_host, double *cents_host) {
+    if (!cb) return fail(TQ_EINVAL, "codebook is NULL");
+    if (bounds_host) std::memcpy(bounds_host, cb->t.bounds.data(), cb->t.bounds.size() * sizeof(double));
+    if (cents_host) std::memcpy(cents_host, cb->t.cents.data(), cb->t.cents.size() * sizeof(double));
+    return TQ_OK;
+}
+
+tq_status tq_codebook_mse(const tq_codebook *cb, double *mse_out) {
+    if (!cb || !mse_out) return fail(TQ_EINVAL, "NULL argument");
+    *mse_out = cb->t.mse;
+    return TQ_OK;
+}
+
+void tq_codebook_free(tq_codebook *cb) { delete cb; }
+
+tq_status tq_rotation_create(int32_t d, uint64_t seed, tq_rotation **out) {
+    if (!out) return fail(TQ_EINVAL, "out is NULL");
+    *out = nullptr;
+    tq_status st = check_d(d);
+    if (st != TQ_OK) return st;
+    tq_rotation *r = new (std::nothrow) tq_rotation();
+    if (!r) return fail(TQ_ENOMEM, "host allocation failed");
+    r->d = d;
+    r->seed = seed;
+    try {
+        make_rotation(d, seed, &r->R);
+    } catch (const std::bad_alloc &) {
+        delete r;
+        return fail(TQ_ENOMEM, "host allocation failed");
+    }
+    *out = r;
+    return TQ_OK;
+}
+
+tq_status tq_rotation_matrix(const tq_rotation *rot, float *R_host) {
+    if (!rot || !R_host) return fail(TQ_EINVAL, "NULL argument");
+    std::memcpy(R_host, rot->R.data(), rot->R.size() * sizeof(float));
+    return TQ_OK;
+}
+
+void tq_rotation_free(tq_rotation *rot) {
+    if (!rot) return;
+    if (rot->R_dev) (void)hipFree(rot->R_dev);
+    delete rot;
+}
+
+tq_status tq_rotate_quantize(const tq_codebook *cb, const tq_rotation *rot, const float *X_dev,
+                             int64_t n, uint8_t *codes_dev, float *scales_dev, void *stream) {
+    if (!cb || !rot) return fail(TQ_EINVAL, "NULL codebook or rotation");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (cb->t.d != rot->d) return fail(TQ_EINVAL, "codebook and rotation disagree on d");
+    if (n == 0) return TQ_OK;
+    if (!X_dev || !codes_dev || !scales_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    const float *R = nullptr;
+    st = rotation_dev(rot, &R);
+    if (st != TQ_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    CodebookDev cd;
+    fill_codebook_dev(cb->t, &cd);
+    const int d = rot->d;
+    AsyncBuf ws;
+    hipError_t e = ws.alloc(encode_workspace_bytes(d) + 256, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(encode workspace)");
+    int *status = reinterpret_cast<int *>(static_cast<uint8_t *>(ws.p) + encode_workspace_bytes(d));
+    e = hipMemsetAsync(status, 0, sizeof(int), s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    EncodeOut out;
+    out.canonical = codes_dev;
+    out.scales = scales_dev;
+    e = encode_rows(X_dev, n, d, R, cd, out, ws.p, status, s);
+    if (e != hipSuccess) return hip_fail(e, "encode");
+    int h = 0;
+    st = read_status(status, s, &h);
+    if (st != TQ_OK) return st;
+    if (h & 1) return fail(TQ_EINVAL, "non-finite value in X");
+    return TQ_OK;
+}
+
+tq_status tq_rotate_queries(const tq_rotation *rot, const float *Q_dev, int64_t nq,
+                            float *Qrot_dev, void *stream) {
+    if (!rot) return fail(TQ_EINVAL, "NULL rotation");
+    if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
+    if (nq == 0) return TQ_OK;
+    if (!Q_dev || !Qrot_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    const float *R = nullptr;
+    st = rotation_dev(rot, &R);
+    if (st != TQ_OK) return st;
+    hipError_t e = rotate_rows_f32(Q_dev, nq, rot->d, R, Qrot_dev, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "query rotation");
+    return TQ_OK;
+}
+
+tq_status tq_index_create(const tq_codebook *cb, const tq_rotation *rot, int32_t n_tenants,
+                          tq_index **out) {
+    if (!out) return fail(TQ_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!cb || !rot) return fail(TQ_EINVAL, "NULL codebook or rotation");
+    if (cb->t.d != rot->d) return fail(TQ_EINVAL, "codebook and rotation disagree on d");
+    if (n_tenants < 1 || n_tenants > 65535) return fail(TQ_EINVAL, "n_tenants must be in 1..65535");
+    tq_index *x = new (std::nothrow) tq_index();
+    if (!x) return fail(TQ_ENOMEM, "host allocation failed");
+    x->cb = cb->t;
+    fill_codebook_dev(x->cb, &x->cbdev);
+    x->rot.d = rot->d;
+    x->rot.seed = rot->seed;
+    x->rot.R = rot->R;
+    x->d = rot->d;
+    x->bits = cb->t.bits;
+    x->T = n_tenants;
+    x->W = (n_tenants + 63) / 64;
+    x->chunks = chunks_per_vector(x->d, x->bits);
+    *out = x;
+    return TQ_OK;
+}
+
+tq_status tq_index_reserve(tq_index *idx, int64_t capacity) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (capacity < 0) return fail(TQ_EINVAL, "capacity < 0");
+    return index_grow(idx, capacity, nullptr);
+}
+
+static tq_status finish_add(tq_index *x, const uint16_t *tenants_dev, int64_t n, hipStream_t s) {
+    hipError_t e = hipMemsetAsync(x->status, 0, sizeof(int), s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    e = add_tenants(tenants_dev, n, x->n, x->T, x->W, x->tenants, x->summ, x->status, s);
+    if (e != hipSuccess) return hip_fail(e, "add_tenants");
+    int h = 0;
+    tq_status st = read_status(x->status, s, &h);
+    if (st != TQ_OK) return st;
+    if (h & 2) return fail(TQ_EINVAL, "tenant id >= n_tenants");
+    x->n += n;
+    return TQ_OK;
+}
+
+tq_status tq_index_add(tq_index *idx, const float *X_dev, const uint16_t *tenants_dev, int64_t n,
+                       void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    if (!X_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    if (idx->n + n > (int64_t)INT32_MAX) return fail(TQ_EUNSUPPORTED, "index limited to 2^31-1 vectors");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    tq_status st = index_grow(idx, idx->n + n, s);
+    if (st != TQ_OK) return st;
+    const float *R = nullptr;
+    st = rotation_dev(&idx->rot, &R);
+    if (st != TQ_OK) return st;
+    AsyncBuf ws;
+    hipError_t e = ws.alloc(encode_workspace_bytes(idx->d), s);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(encode workspace)");
+    e = hipMemsetAsync(idx->status, 0, sizeof(int), s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    EncodeOut out;
+    out.blocked = idx->codes;
+    out.blocked_scales = idx->scales;
+    out.base = idx->n;
+    e = encode_rows(X_dev, n, idx->d, R, idx->cbdev, out, ws.p, idx->status, s);
+    if (e != hipSuccess) return hip_fail(e, "encode");
+    int h = 0;
+    st = read_status(idx->status, s, &h);
+    if (st != TQ_OK) return st;
+    if (h & 1) return fail(TQ_EINVAL, "non-finite value in X");
+    return finish_add(idx, tenants_dev, n, s);
+}
+
+tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev, const float *scales_dev,
+                             const uint16_t *tenants_dev, int64_t n, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    if (!codes_dev || !scales_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    if (idx->n + n > (int64_t)INT32_MAX) return fail(TQ_EUNSUPPORTED, "index limited to 2^31-1 vectors");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    tq_status st = index_grow(idx, idx->n + n, s);
+    if (st != TQ_OK) return st;
+    hipError_t e = canonical_to_blocked(codes_dev, scales_dev, n, idx->d, idx->bits, idx->codes,
+                                        idx->scales, idx->n, s);
+    if (e != hipSuccess) return hip_fail(e, "canonical_to_blocked");
+    return finish_add(idx, tenants_dev, n, s);
+}
+
+tq_status tq_index_size(const tq_index *idx, int64_t *n_out) {
+    if (!idx || !n_out) return fail(TQ_EINVAL, "NULL argument");
+    *n_out = idx->n;
+    return TQ_OK;
+}
+
+tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev, float *scales_dev,
+                          uint16_t *tenants_dev, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (idx->n == 0) return TQ_OK;
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (codes_dev || scales_dev) {
+        hipError_t e = blocked_to_canonical(idx->codes, idx->scales, idx->n, idx->d, idx->bits,
+                                            codes_dev, scales_dev, s);
+        if (e != hipSuccess) return hip_fail(e, "blocked_to_canonical");
+    }
+    if (tenants_dev) {
+        hipError_t e = hipMemcpyAsync(tenants_dev, idx->tenants, idx->n * sizeof(uint16_t),
+                                      hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(tenants)");
+    }
+    return TQ_OK;
+}
+
+void tq_index_free(tq_index *idx) {
+    if (!idx) return;
+    index_release(idx);
+    if (idx->rot.R_dev) (void)hipFree(idx->rot.R_dev);
+    idx->rot.R_dev = nullptr;
+    delete idx;
+}
+
+static ScanShape shape_of(const tq_index *x) {
+    ScanShape s;
+    s.d = x->d;
+    s.bits = x->bits;
+    s.chunks = x->chunks;
+    s.n = x->n;
+    s.nblk = (x->n + 63) / 64;
+    s.W = x->W;
+    return s;
+}
+
+static int scan_grid() {
+    const int cus = device_cu_count();
+    return cus > 0 ? cus : 256;
+}
+
+tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, int32_t path,
+                                   size_t *bytes_out) {
+    if (!idx || !bytes_out) return fail(TQ_EINVAL, "NULL argument");
+    if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
+    if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
+    const int base = path & ~TQ_FLAG_PREROTATED;
+    if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
+        return fail(TQ_EINVAL, "unknown path");
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    *bytes_out = lut_search_workspace_bytes(shape_of(idx), nq, k, scan_grid());
+    return TQ_OK;
+}
+
+tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int32_t k,
+                       const uint64_t *allow_dev, int32_t path, void *workspace_dev,
+                       size_t workspace_bytes, int64_t *ids_dev, float *scores_dev,
+                       void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
+    if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
+    const bool prerotated = (path & TQ_FLAG_PREROTATED) != 0;
+    const int base = path & ~TQ_FLAG_PREROTATED;
+    if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
+        return fail(TQ_EINVAL, "unknown path");
+    if (nq == 0) return TQ_OK;
+    if (!Q_dev || !ids_dev || !scores_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    if (!workspace_dev) return fail(TQ_EINVAL, "NULL workspace");
+    if (((uintptr_t)workspace_dev & 255) != 0) return fail(TQ_EINVAL, "workspace must be 256-byte aligned");
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    const ScanShape sh = shape_of(idx);
+    const int grid = scan_grid();
+    const size_t need = lut_search_workspace_bytes(sh, nq, k, grid);
+    if (workspace_bytes < need)
+        return fail(TQ_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (idx->n == 0) {
+        // nothing indexed: every slot is padding
+        std::vector<int64_t> pad_i((size_t)nq * k, -1);
+        std::vector<float> pad_s((size_t)nq * k, -INFINITY);
+        hipError_t e = hipMemcpyAsync(ids_dev, pad_i.data(), pad_i.size() * 8, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(scores_dev, pad_s.data(), pad_s.size() * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "padding copy");
+        return TQ_OK;
+    }
+    const float *Qrot = Q_dev;
+    if (!prerotated) {
+        const float *R = nullptr;
+        st = rotation_dev(&idx->rot, &R);
+        if (st != TQ_OK) return st;
+        float *qr = static_cast<float *>(workspace_dev);
+        hipError_t e = rotate_rows_f32(Q_dev, nq, idx->d, R, qr, s);
+        if (e != hipSuccess) return hip_fail(e, "query rotation");
+        Qrot = qr;
+    }
+    hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev, Qrot, nq, k,
+                   allow_dev, grid, workspace_dev, workspace_bytes, ids_dev, scores_dev, s);
+    if (e != hipSuccess) return hip_fail(e, "scan");
+    return TQ_OK;
+}
+
+tq_status tq_search(const tq_index *idx, const float *Q_dev, int64_t nq, int32_t k,
+                    const uint64_t *allow_dev, int64_t *ids_dev, float *scores_dev, void *stream) {
+    size_t bytes = 0;
+    tq_status st = tq_search_workspace_size(idx, nq, k, TQ_PATH_AUTO, &bytes);
+    if (st != TQ_OK) return st;
+    if (nq == 0) return TQ_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    AsyncBuf ws;
+    hipError_t e = ws.alloc(bytes, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(search workspace)");
+    return tq_search_ex(idx, Q_dev, nq, k, allow_dev, TQ_PATH_AUTO, ws.p, bytes, ids_dev,
+                        scores_dev, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,456 @@
+// Rotation + quantisation of float32 rows on gfx950 (section II-B, steps 1-5).
+//
+// Pipeline per chunk of rows:
+//  1. rot_gemm<QuantEpilogue>: Y = X R^T on the matrix cores
+//     (v_mfma_f32_16x16x4_f32), with each 32-wide slab of k accumulated in
+//     float32 and then added into float64 accumulators.  The same kernel
+//     computes the exact row norm n = sqrt(sum_k x_k^2) (sequential float64
+//     over k, from the staged A tile) and reports non-finite inputs.  The
+//     epilogue turns every y into a code by comparing it with fl64(t_i * n)
+//     and flags the coordinate when y lies within tau of a threshold, where
+//     tau bounds |y - S| for S the float64 sequential dot product of the
+//     definition:
+//       per slab, float32 MFMA accumulation of 32 products from 0:
+//         |err| <= gamma_33 * sum|R_jk x_k|   (gamma_m = m u / (1 - m u),
+//                                              u = 2^-24; doubled for margin)
+//       float64 sum of 48 slab partials and the float64 reference itself:
+//         < 2e-13 * n;  flushed denormal products: < 2e-35 absolute.
+//     With ||R_j|| <= 1 + 1e-6 this gives tau = 4.0e-6 * n + 1e-30.
+//  2. fixup: every flagged coordinate is recomputed as the sequential float64
+//     sum sum_{k=0}^{d-1} R[j][k] x_k (every product of two float32 values is
+//     exact in float64) and re-coded.
+//  3. pack: per row, scale = n / sqrt(sum_j fl64(c_code_j^2)) (sequential
+//     float64 over j) and the codes are written in the canonical bitstream
+//     and/or the index's blocked layout.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "kernels.h"
+
+namespace tq {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 128;                 // rows of X per workgroup
+constexpr int BN = 128;                 // rows of R (output columns) per workgroup
+constexpr int KB = 32;                  // k per slab
+constexpr int LDS_STRIDE = KB + 4;      // floats per staged row (conflict-free b128 reads)
+constexpr int GEMM_THREADS = 512;       // 8 waves: 2 along rows x 4 along columns
+constexpr double kTauRel = 4.0e-6;
+constexpr double kTauAbs = 1e-30;
+
+struct QuantArgs {
+    const double *bounds;   // device copy of the thresholds t_i (levels-1)
+    int levels;
+    uint8_t *codes_tmp;     // [rows][d] unpacked codes of this chunk
+    double *norms;          // [rows] exact row norms (written by column tile 0)
+    uint32_t *flags;        // flagged (row << 11 | j)
+    unsigned int *flag_count;
+    int *status;            // set non-zero on a non-finite input
+};
+
+struct F32Args {
+    float *Y;               // [rows][d]
+};
+
+// XCD-aware tile order: the d/BN column tiles of one row tile go to the same
+// XCD (workgroups are dealt to the 8 XCDs round-robin), so the X tile is read
+// from HBM once and then served by that XCD's L2.
+__device__ inline void tile_of(int bid, int ncol, int &rt, int &ct) {
+    const int x = bid & 7;
+    const int rest = bid >> 3;
+    ct = rest % ncol;
+    rt = (rest / ncol) * 8 + x;
+}
+
+template <bool QUANT>
+__global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
+    const float *__restrict__ X, int64_t m, const float *__restrict__ R, int d,
+    int n_row_tiles, QuantArgs qa, F32Args fa) {
+    __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
+    __shared__ double norm_s[BM];
+
+    const int ncol = (d + BN - 1) / BN;
+    int rt, ct;
+    tile_of(blockIdx.x, ncol, rt, ct);
+    if (rt >= n_row_tiles) return;
+    const int64_t row0 = (int64_t)rt * BM;
+    const int col0 = ct * BN;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wr = wave >> 2;     // 0..1 : 64-row half
+    const int wc = wave & 3;      // 0..3 : 32-column quarter
+    const int l16 = lane & 15;
+    const int g4 = lane >> 4;
+
+    // global -> register prefetch: 2 float4 of A and 2 of B per thread per slab
+    f4 pa[2], pb[2];
+    auto load_slab = [&](int k0) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int e = tid + r * GEMM_THREADS;
+            const int row = e >> 3;
+            const int kq = (e & 7) * 4;
+            const int64_t gr = row0 + row;
+            if (gr < m)
+                pa[r] = *reinterpret_cast<const f4 *>(X + gr * d + k0 + kq);
+            else
+                pa[r] = f4{0.f, 0.f, 0.f, 0.f};
+            if (col0 + row < d)
+                pb[r] = *reinterpret_cast<const f4 *>(R + (int64_t)(col0 + row) * d + k0 + kq);
+            else
+                pb[r] = f4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    auto store_slab = [&](int buf) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int e = tid + r * GEMM_THREADS;
+            const int row = e >> 3;
+            const int kq = (e & 7) * 4;
+            *reinterpret_cast<f4 *>(&As[buf][row * LDS_STRIDE + kq]) = pa[r];
+            *reinterpret_cast<f4 *>(&Bs[buf][row * LDS_STRIDE + kq]) = pb[r];
+        }
+    };
+
+    f4 acc[4][2];
+    double accd[4][2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int v = 0; v < 4; ++v) accd[i][j][v] = 0.0;
+        }
+    double nrm2 = 0.0;       // sequential sum of squares (threads < BM own a row)
+    bool finite = true;
+
+    const int nslab = d / KB;
+    load_slab(0);
+    store_slab(0);
+    __syncthreads();
+    for (int s = 0; s < nslab; ++s) {
+        const int buf = s & 1;
+        if (s + 1 < nslab) load_slab((s + 1) * KB);
+        if (QUANT && tid < BM) {
+            // row norm, k in order
+            const float *a = &As[buf][tid * LDS_STRIDE];
+#pragma unroll
+            for (int q = 0; q < KB; q += 4) {
+                const f4 v = *reinterpret_cast<const f4 *>(a + q);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const double xv = (double)v[c];
+                    finite = finite && std::isfinite(v[c]);
+                    const double sq = xv * xv;
+                    nrm2 = nrm2 + sq;
+                }
+            }
+        }
+#pragma unroll
+        for (int sub = 0; sub < KB / 16; ++sub) {
+            f4 af[4], bf[2];
+#pragma unroll
+            for (int ti = 0; ti < 4; ++ti)
+                af[ti] = *reinterpret_cast<const f4 *>(
+                    &As[buf][(wr * 64 + ti * 16 + l16) * LDS_STRIDE + sub * 16 + g4 * 4]);
+#pragma unroll
+            for (int tj = 0; tj < 2; ++tj)
+                bf[tj] = *reinterpret_cast<const f4 *>(
+                    &Bs[buf][(wc * 32 + tj * 16 + l16) * LDS_STRIDE + sub * 16 + g4 * 4]);
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+                    for (int tj = 0; tj < 2; ++tj)
+                        acc[ti][tj] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            af[ti][st], bf[tj][st], acc[ti][tj], 0, 0, 0);
+        }
+        // fold the slab's float32 partials into float64
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) accd[i][j][v] += (double)acc[i][j][v];
+                acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+            }
+        if (s + 1 < nslab) store_slab(buf ^ 1);
+        __syncthreads();
+    }
+
+    if (QUANT) {
+        if (tid < BM) {
+            const double nrm = std::sqrt(nrm2);
+            norm_s[tid] = nrm;
+            const int64_t gr = row0 + tid;
+            if (gr < m) {
+                if (ct == 0) qa.norms[gr] = nrm;
+                if (!finite) atomicOr(qa.status, 1);
+            }
+        }
+        __syncthreads();
+        const int L = qa.levels;
+#pragma unroll
+        for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int lr = wr * 64 + ti * 16 + g4 * 4 + v;
+                const int64_t gr = row0 + lr;
+                if (gr >= m) continue;
+                const double nrm = norm_s[lr];
+                const double tau = kTauRel * nrm + kTauAbs;
+#pragma unroll
+                for (int tj = 0; tj < 2; ++tj) {
+                    const int col = col0 + wc * 32 + tj * 16 + l16;
+                    if (col >= d) continue;
+                    const double y = accd[ti][tj][v];
+                    int code;
+                    bool flag = false;
+                    if (nrm == 0.0) {
+                        code = L / 2;
+                    } else {
+                        int c = 0;
+                        for (int step = L / 2; step >= 1; step >>= 1) {
+                            if (c + step <= L - 1) {
+                                const double t = qa.bounds[c + step - 1] * nrm;
+                                if (t <= y) c += step;
+                            }
+                        }
+                        code = c;
+                        if (!std::isfinite(y)) {
+                            flag = true;
+                        } else {
+                            if (c > 0 && y - qa.bounds[c - 1] * nrm <= tau) flag = true;
+                            if (c < L - 1 && qa.bounds[c] * nrm - y <= tau) flag = true;
+                        }
+                    }
+                    qa.codes_tmp[gr * d + col] = (uint8_t)code;
+                    if (flag) {
+                        const unsigned int slot = atomicAdd(qa.flag_count, 1u);
+                        qa.flags[slot] = ((uint32_t)gr << 11) | (uint32_t)col;
+                    }
+                }
+            }
+    } else {
+#pragma unroll
+        for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int lr = wr * 64 + ti * 16 + g4 * 4 + v;
+                const int64_t gr = row0 + lr;
+                if (gr >= m) continue;
+#pragma unroll
+                for (int tj = 0; tj < 2; ++tj) {
+                    const int col = col0 + wc * 32 + tj * 16 + l16;
+                    if (col < d) fa.Y[gr * d + col] = (float)accd[ti][tj][v];
+                }
+            }
+    }
+}
+
+// Exact recomputation of flagged coordinates: the sequential float64 sum of
+// the definition (products of float32 values are exact in float64, so fused
+// and unfused multiply-adds agree).
+__global__ __launch_bounds__(256) void fixup_kernel(
+    const float *__restrict__ X, const float *__restrict__ R, int d,
+    const double *__restrict__ bounds, int levels, const double *__restrict__ norms,
+    const uint32_t *__restrict__ flags, const unsigned int *__restrict__ flag_count,
+    uint8_t *__restrict__ codes_tmp) {
+    const unsigned int cnt = *flag_count;
+    for (unsigned int e = blockIdx.x * blockDim.x + threadIdx.x; e < cnt;
+         e += gridDim.x * blockDim.x) {
+        const uint32_t f = flags[e];
+        const int64_t row = f >> 11;
+        const int j = f & 2047;
+        const f4 *xr = reinterpret_cast<const f4 *>(X + row * d);
+        const f4 *rr = reinterpret_cast<const f4 *>(R + (int64_t)j * d);
+        double S = 0.0;
+        for (int q = 0; q < d / 4; ++q) {
+            const f4 a = rr[q];
+            const f4 b = xr[q];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const double prod = (double)a[c] * (double)b[c];
+                S = S + prod;
+            }
+        }
+        const double nrm = norms[row];
+        int c = 0;
+        for (int t = 0; t < levels - 1; ++t) {
+            const double th = bounds[t] * nrm;
+            c += (th <= S) ? 1 : 0;
+        }
+        codes_tmp[row * d + j] = (uint8_t)c;
+    }
+}
+
+// Packs PACK_ROWS rows per workgroup: scale, canonical bitstream, blocked layout.
+constexpr int PACK_ROWS = 32;   // PACK_ROWS * d bytes of LDS (<= 64 KiB at d = 2048)
+
+__global__ __launch_bounds__(256) void pack_kernel(
+    const uint8_t *__restrict__ codes_tmp, int64_t m, int d, int bits,
+    const double *__restrict__ cent_sq, const double *__restrict__ norms,
+    uint8_t *__restrict__ canon, float *__restrict__ scales,
+    uint8_t *__restrict__ blocked, float *__restrict__ blocked_scales, int64_t base,
+    int chunks) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t cs[];   // [PACK_ROWS][d]
+    const int64_t r0 = (int64_t)blockIdx.x * PACK_ROWS;
+    const int rows = (int)((m - r0) < PACK_ROWS ? (m - r0) : PACK_ROWS);
+    const int tid = threadIdx.x;
+    // stage codes (16 B per thread per step)
+    const int vec_per_row = d / 16;
+    for (int e = tid; e < rows * vec_per_row; e += blockDim.x) {
+        const int r = e / vec_per_row, q = e % vec_per_row;
+        reinterpret_cast<uint4 *>(cs + r * d)[q] =
+            reinterpret_cast<const uint4 *>(codes_tmp + (r0 + r) * d)[q];
+    }
+    __syncthreads();
+    // scale: one thread per row, j in order
+    if (tid < rows) {
+        const uint8_t *c = cs + tid * d;
+        double h2 = 0.0;
+        for (int j = 0; j < d; ++j) h2 = h2 + cent_sq[c[j]];
+        const double nrm = norms[r0 + tid];
+        const float s = (nrm == 0.0) ? 0.0f : (float)(nrm / std::sqrt(h2));
+        if (scales) scales[r0 + tid] = s;
+        if (blocked_scales) blocked_scales[base + r0 + tid] = s;
+    }
+    // canonical rows: 32-bit words, bits LSB-first
+    const int wpr = d * bits / 32;   // words per canonical row
+    if (canon) {
+        for (int e = tid; e < rows * wpr; e += blockDim.x) {
+            const int r = e / wpr, w = e % wpr;
+            const uint8_t *c = cs + r * d;
+            uint32_t word = 0;
+            if (bits == 3) {
+                const int b0 = w * 32;
+                for (int t = 0; t < 32; ++t) {
+                    const int bit = b0 + t;
+                    const int j = bit / 3, sh = bit % 3;
+                    word |= (uint32_t)((c[j] >> sh) & 1) << t;
+                }
+            } else {
+                const int per = 32 / bits;
+                for (int t = 0; t < per; ++t) word |= (uint32_t)c[w * per + t] << (t * bits);
+            }
+            reinterpret_cast<uint32_t *>(canon + (r0 + r) * (int64_t)(d * bits / 8))[w] = word;
+        }
+    }
+    // blocked layout: 16-byte chunk ch of vector v at ((v/64)*chunks + ch)*1024 + (v%64)*16
+    if (blocked) {
+        for (int e = tid; e < rows * chunks * 4; e += blockDim.x) {
+            const int r = e / (chunks * 4), rem = e % (chunks * 4);
+            const int ch = rem >> 2, wq = rem & 3;
+            const uint8_t *c = cs + r * d;
+            uint32_t word = 0;
+            if (bits == 3) {
+                const int j0 = (ch * 4 + wq) * 10;
+                for (int t = 0; t < 10; ++t) {
+                    const int j = j0 + t;
+                    if (j < d) word |= (uint32_t)c[j] << (3 * t);
+                }
+            } else {
+                const int per = 32 / bits;
+                const int j0 = (ch * 4 + wq) * per;
+                for (int t = 0; t < per; ++t) word |= (uint32_t)c[j0 + t] << (t * bits);
+            }
+            const int64_t v = base + r0 + r;
+            uint8_t *dst = blocked + ((v >> 6) * chunks + ch) * 1024 + (v & 63) * 16;
+            reinterpret_cast<uint32_t *>(dst)[wq] = word;
+        }
+    }
+}
+
+}  // namespace
+
+size_t encode_workspace_bytes(int d) {
+    const size_t rows = kEncodeChunkRows;
+    size_t b = 0;
+    b += rows * (size_t)d;                    // unpacked codes
+    b = (b + 255) & ~(size_t)255;
+    b += rows * sizeof(double);               // norms
+    b = (b + 255) & ~(size_t)255;
+    b += rows * (size_t)d * sizeof(uint32_t); // flags (worst case: every coordinate)
+    b = (b + 255) & ~(size_t)255;
+    b += 256;                                 // flag counter
+    b += 255 * sizeof(double) + 256 * sizeof(double);   // bounds, cent_sq
+    b = (b + 255) & ~(size_t)255;
+    return b;
+}
+
+hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
+                       const CodebookDev &cb, const EncodeOut &out, void *ws,
+                       int *status_dev, hipStream_t stream) {
+    const size_t rows = kEncodeChunkRows;
+    uint8_t *p = static_cast<uint8_t *>(ws);
+    uint8_t *codes_tmp = p;
+    p += (rows * (size_t)d + 255) & ~(size_t)255;
+    double *norms = reinterpret_cast<double *>(p);
+    p += (rows * sizeof(double) + 255) & ~(size_t)255;
+    uint32_t *flags = reinterpret_cast<uint32_t *>(p);
+    p += (rows * (size_t)d * sizeof(uint32_t) + 255) & ~(size_t)255;
+    unsigned int *flag_count = reinterpret_cast<unsigned int *>(p);
+    p += 256;
+    double *bounds = reinterpret_cast<double *>(p);
+    double *cent_sq = bounds + 255;
+
+    hipError_t e = hipMemcpyAsync(bounds, cb.bounds, sizeof(double) * (cb.levels - 1),
+                                  hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return e;
+    e = hipMemcpyAsync(cent_sq, cb.cent_sq, sizeof(double) * cb.levels,
+                       hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return e;
+
+    const int chunks = chunks_per_vector(d, cb.bits);
+    const int ncol = (d + BN - 1) / BN;
+    for (int64_t r0 = 0; r0 < n; r0 += rows) {
+        const int64_t m = (n - r0) < (int64_t)rows ? (n - r0) : (int64_t)rows;
+        e = hipMemsetAsync(flag_count, 0, sizeof(unsigned int), stream);
+        if (e != hipSuccess) return e;
+        const int nrt = (int)((m + BM - 1) / BM);
+        const int groups = (nrt + 7) / 8;
+        QuantArgs qa{bounds, cb.levels, codes_tmp, norms, flags, flag_count, status_dev};
+        F32Args fa{nullptr};
+        hipLaunchKernelGGL((rot_gemm<true>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
+                           stream, X + r0 * d, m, R, d, nrt, qa, fa);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(fixup_kernel, dim3(1024), dim3(256), 0, stream, X + r0 * d, R, d,
+                           bounds, cb.levels, norms, flags, flag_count, codes_tmp);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);
+        hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * d, stream,
+                           codes_tmp, m, d, cb.bits, cent_sq, norms,
+                           out.canonical ? out.canonical + r0 * (int64_t)(d * cb.bits / 8) : nullptr,
+                           out.scales ? out.scales + r0 : nullptr, out.blocked,
+                           out.blocked_scales, out.base + r0, chunks);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R, float *Y,
+                           hipStream_t stream) {
+    if (m <= 0) return hipSuccess;
+    const int ncol = (d + BN - 1) / BN;
+    const int nrt = (int)((m + BM - 1) / BM);
+    const int groups = (nrt + 7) / 8;
+    QuantArgs qa{};
+    F32Args fa{Y};
+    hipLaunchKernelGGL((rot_gemm<false>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
+                       stream, X, m, R, d, nrt, qa, fa);
+    return hipGetLastError();
+}
+
+}  // namespace tq

@@ -1,0 +1,84 @@
+// Launch interface of the gfx950 kernels (host-callable, plain pointers).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace tq {
+
+// Fixed-size description of a codebook, passed to kernels by value.
+struct CodebookDev {
+    int bits;
+    int levels;
+    double bounds[255];   // levels-1 used
+    float cents32[256];   // levels used
+    double cent_sq[256];  // fl64(c * c), levels used
+};
+
+// ------------------------------------------------------------------ encode
+// Rows per encode chunk and the workspace it needs.
+constexpr int kEncodeChunkRows = 32768;
+size_t encode_workspace_bytes(int d);
+
+// Output layout selector for the encode pipeline.
+struct EncodeOut {
+    uint8_t *canonical = nullptr;   // [n][d*bits/8] canonical rows, or null
+    float *scales = nullptr;        // [n] scales (canonical order), or null
+    uint8_t *blocked = nullptr;     // index blocked code store, or null
+    float *blocked_scales = nullptr;// index scale store, or null
+    int64_t base = 0;               // index position of row 0 (blocked only)
+};
+
+// Encodes X [n][d] (float32, row-major) with R [d][d] on `stream`.
+// `ws` must hold encode_workspace_bytes(d); `status_dev` is an int32 that the
+// kernels set non-zero on a non-finite input.
+hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
+                       const CodebookDev &cb, const EncodeOut &out, void *ws,
+                       int *status_dev, hipStream_t stream);
+
+// Y = X R^T in float32 (query rotation), X [m][d], Y [m][d].
+hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R,
+                           float *Y, hipStream_t stream);
+
+// --------------------------------------------------------------- layout
+// Blocked code store: vector v lives in block v/64, lane v%64; chunk c (16 B)
+// of a vector sits at byte ((v/64) * chunks + c) * 1024 + (v%64) * 16.
+inline int chunks_per_vector(int d, int bits) {
+    // 3-bit codes are stored 10 per 32-bit word (2 pad bits per word)
+    if (bits == 3) return (((d + 9) / 10) + 3) / 4;
+    return d * bits / 128;
+}
+
+hipError_t canonical_to_blocked(const uint8_t *canon, const float *scales,
+                                int64_t n, int d, int bits, uint8_t *blocked,
+                                float *blocked_scales, int64_t base,
+                                hipStream_t stream);
+hipError_t blocked_to_canonical(const uint8_t *blocked, const float *blocked_scales,
+                                int64_t n, int d, int bits, uint8_t *canon,
+                                float *scales, hipStream_t stream);
+// Copies tenant ids into the store and ORs them into the block summaries
+// (W words per block); sets *status_dev non-zero if an id is >= n_tenants.
+hipError_t add_tenants(const uint16_t *tenants, int64_t n, int64_t base,
+                       int n_tenants, int W, uint16_t *tenant_store,
+                       uint64_t *summaries, int *status_dev, hipStream_t stream);
+
+// ----------------------------------------------------------------- search
+struct ScanShape {
+    int d, bits, chunks;     // code geometry
+    int64_t n;               // vectors in the index
+    int64_t nblk;            // 64-vector blocks
+    int W;                   // allowlist words per query
+};
+
+size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid);
+hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
+                      const uint16_t *tenants, const uint64_t *summaries,
+                      const float *cents32, const float *Qrot, int64_t nq, int k,
+                      const uint64_t *allow, int grid, void *ws, size_t ws_bytes,
+                      int64_t *ids, float *scores, hipStream_t stream);
+
+int device_cu_count();
+
+}  // namespace tq

@@ -1,0 +1,54 @@
+"""Comparison helpers shared by the GPU parity tests (no method arithmetic:
+scores and rankings come from the oracle)."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+SCORE_RTOL = 1e-4          # relative tolerance on scores
+SCORE_ATOL_Q = 1e-6        # absolute floor, times ||q||
+
+
+def score_tol(ref, qnorm):
+    return np.maximum(SCORE_RTOL * np.abs(ref), SCORE_ATOL_Q * qnorm)
+
+
+def check_topk(gpu_ids, gpu_scores, codes, scales, cents, qrot, qnorms, k,
+               ref_ids, ref_scores, allowed=None, n=None):
+    """Validity of GPU top-k lists against the oracle (see module docstring of
+    tests/test_gpu_search.py).  `allowed` is a list of boolean masks (or None);
+    `ref_*` are the oracle's own lists.  Returns the number of id lists that
+    differ from the oracle's (ties within tolerance)."""
+    gpu_ids = np.asarray(gpu_ids)
+    gpu_scores = np.asarray(gpu_scores, dtype=np.float64)
+    n = codes.shape[0] if n is None else n
+    differ = 0
+    for b in range(gpu_ids.shape[0]):
+        ids = gpu_ids[b]
+        valid = ids >= 0
+        nv = int(valid.sum())
+        n_allowed = n if allowed is None or allowed[b] is None else int(allowed[b].sum())
+        assert nv == min(k, n_allowed), (b, nv, min(k, n_allowed))
+        assert np.all(valid[:nv]) and not np.any(valid[nv:]), "padding must be at the end"
+        assert np.all(np.isneginf(gpu_scores[b][nv:]))
+        v = ids[:nv]
+        assert len(set(v.tolist())) == nv, "duplicate ids"
+        assert np.all(v < n)
+        if allowed is not None and allowed[b] is not None:
+            assert np.all(allowed[b][v]), "disallowed id returned"
+        if nv == 0:
+            continue
+        ref = oracle.scores_for_ids(codes, scales, cents, qrot[b], v)
+        tol = score_tol(ref, qnorms[b])
+        err = np.abs(gpu_scores[b][:nv] - ref)
+        assert np.all(err <= tol), (b, float((err / tol).max()))
+        # ordered (within tolerance)
+        assert np.all(np.diff(ref) <= 2 * tol[1:] + 1e-12), "not ordered"
+        # nothing better was missed: the worst returned is at least the
+        # oracle's nv-th best, within tolerance
+        kth = ref_scores[b][nv - 1]
+        assert ref.min() >= kth - score_tol(np.array([kth]), qnorms[b])[0]
+        if not np.array_equal(v, ref_ids[b][:nv]):
+            differ += 1
+    return differ

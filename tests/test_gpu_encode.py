@@ -1,0 +1,125 @@
+"""GPU parity of the rotation and the quantiser (section II-B, steps 1-5):
+query rotation within float32 rounding of the oracle's float64 product, and
+codes equal to the oracle's bit for bit (canonical layout), scales to the
+float32 rounding of the oracle's float64 value.
+
+Codes can only legitimately differ where the two sides' inputs differ: the
+library and the oracle each factor the rotation and solve the codebook
+themselves, so a handful of float32 matrix entries may round differently and
+the b=8 tables (an ill-conditioned fixed point) agree to ~1e-12 only.  Such a
+coordinate must then sit within 1e-9 * ||x|| of a threshold in the oracle's
+own float64 value; any other mismatch fails."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.conftest import gpu_available
+
+pytestmark = pytest.mark.gpu
+if not gpu_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import torch  # noqa: E402
+
+import paper_2607_16973_amd as tq  # noqa: E402
+
+D = 1536
+
+
+@pytest.fixture(scope="module")
+def small():
+    X, Q = synth.workload("small")
+    return X[:3000].copy(), Q
+
+
+@pytest.fixture(scope="module")
+def rot_pair():
+    return tq.Rotation(D, 42), oracle.haar_rotation(D, 42)[1]
+
+
+def classify_mismatch(codes_gpu, codes_or, S, norms, bounds):
+    bad = np.argwhere(codes_gpu != codes_or)
+    for i, j in bad:
+        margin = np.min(np.abs(S[i, j] - bounds * norms[i])) / norms[i]
+        assert margin <= 1e-9, ("unexplained code mismatch", int(i), int(j), float(margin))
+    return len(bad)
+
+
+def test_query_rotation(small, rot_pair):
+    _, Q = small
+    rot, R32 = rot_pair
+    print("query rotation nq=%d" % Q.shape[0], flush=True)
+    out = tq.rotate_queries(rot, torch.from_numpy(Q).cuda()).cpu().numpy().astype(np.float64)
+    ref = oracle.rotate_queries(R32, Q)
+    err = np.abs(out - ref).max(axis=1) / np.linalg.norm(Q.astype(np.float64), axis=1)
+    assert err.max() < 2e-6, err.max()
+    # single query and a ragged batch
+    out1 = tq.rotate_queries(rot, torch.from_numpy(Q[5:6]).cuda()).cpu().numpy()
+    assert np.abs(out1[0] - ref[5]).max() < 2e-6
+
+
+@pytest.mark.parametrize("bits", [4, 2, 8, 3, 1])
+def test_codes_bit_exact(small, rot_pair, bits):
+    X, _ = small
+    rot, R32 = rot_pair
+    print("rotate_quantize bits=%d n=%d" % (bits, X.shape[0]), flush=True)
+    cb = tq.Codebook(D, bits)
+    codes, scales = tq.rotate_quantize(cb, rot, torch.from_numpy(X).cuda())
+    codes = codes.cpu().numpy()
+    scales = scales.cpu().numpy()
+    ocb = oracle.lloyd_max(D, bits)
+    c_or, n_or, s_or, S = oracle.encode(X, R32, ocb, return_rotated=True)
+    c_gpu = oracle.unpack_codes(codes, D, bits)
+    nm = classify_mismatch(c_gpu, c_or, S, n_or, ocb.bounds)
+    print("bits=%d code mismatches explained by input rounding: %d of %d" % (bits, nm, c_or.size))
+    assert nm <= 1e-6 * c_or.size + 2
+    if nm == 0:
+        assert np.array_equal(codes, oracle.pack_codes(c_or, bits))
+    ulps = np.abs(scales.view(np.int32).astype(np.int64) - s_or.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1, ulps.max()
+
+
+def test_codes_special_rows(rot_pair):
+    """Zero rows, tiny and huge norms, exact-zero coordinates, a ragged count."""
+    rot, R32 = rot_pair
+    rng = np.random.default_rng(3)
+    X = rng.standard_normal((131, D)).astype(np.float32)
+    X[0] = 0
+    X[1] *= np.float32(1e-30)
+    X[2] *= np.float32(1e30)
+    X[3, :] = 0
+    X[3, 7] = 1.0
+    X[4] = X[5]
+    cb = tq.Codebook(D, 4)
+    codes, scales = tq.rotate_quantize(cb, rot, torch.from_numpy(X).cuda())
+    ocb = oracle.lloyd_max(D, 4)
+    c_or, n_or, s_or, S = oracle.encode(X, R32, ocb, return_rotated=True)
+    c_gpu = oracle.unpack_codes(codes.cpu().numpy(), D, 4)
+    assert classify_mismatch(c_gpu, c_or, S, np.where(n_or > 0, n_or, 1.0), ocb.bounds) <= 2
+    assert np.all(c_gpu[0] == 8) and scales[0].item() == 0.0
+    s = scales.cpu().numpy()
+    ulps = np.abs(s.view(np.int32).astype(np.int64) - s_or.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1
+
+
+def test_nonfinite_input_is_rejected(rot_pair):
+    rot, _ = rot_pair
+    X = np.ones((70, D), dtype=np.float32)
+    X[65, 3] = np.inf
+    cb = tq.Codebook(D, 4)
+    with pytest.raises(tq.TQError, match="TQ_EINVAL"):
+        tq.rotate_quantize(cb, rot, torch.from_numpy(X).cuda())
+
+
+def test_gemm_error_is_far_inside_the_proven_band(small, rot_pair):
+    """The fix-up band assumes |y - S| <= 4e-6 ||x|| for the MFMA product.
+    Measured errors must be orders of magnitude smaller (float32 products,
+    float64 accumulation every 32 terms)."""
+    X, _ = small
+    rot, R32 = rot_pair
+    Y = tq.rotate_queries(rot, torch.from_numpy(X[:512]).cuda()).cpu().numpy().astype(np.float64)
+    ref = X[:512].astype(np.float64) @ R32.astype(np.float64).T
+    rel = np.abs(Y - ref).max(axis=1) / np.linalg.norm(X[:512].astype(np.float64), axis=1)
+    print("max |y - S| / ||x|| = %.3e" % rel.max())
+    assert rel.max() < 4e-7

