@@ -22,6 +22,10 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtq.so")
 
 HIP_SOURCES = ["encode.hip", "scan.hip", "layout.hip", "api.cpp"]
+# Per-source extra flags.  The scan's prefetch ring must stay where it is
+# written: machine sinking would move every refill into the loop latch and
+# serialise the loads with the table lookups.
+EXTRA_FLAGS = {"scan.hip": ["-mllvm", "-disable-machine-sink"]}
 HOST_SOURCES = ["codebook.cpp", "rotation.cpp"]
 
 
@@ -55,7 +59,8 @@ def build(verbose: bool = False) -> str:
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         objs.append(obj)
-        jobs.append([hipcc] + hip_flags() + ["-c", os.path.join(CSRC, src), "-o", obj])
+        jobs.append([hipcc] + hip_flags() + EXTRA_FLAGS.get(src, []) +
+                    ["-c", os.path.join(CSRC, src), "-o", obj])
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         objs.append(obj)

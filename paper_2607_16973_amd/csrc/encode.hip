@@ -362,6 +362,7 @@ __global__ __launch_bounds__(256) void pack_kernel(
                 const int per = 32 / bits;
                 const int j0 = (ch * 4 + wq) * per;
                 for (int t = 0; t < per; ++t) word |= (uint32_t)c[j0 + t] << (t * bits);
+                if (blocked_rotated(bits)) word = rotl2(word);
             }
             const int64_t v = base + r0 + r;
             uint8_t *dst = blocked + ((v >> 6) * chunks + ch) * 1024 + (v & 63) * 16;

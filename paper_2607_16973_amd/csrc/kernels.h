@@ -45,6 +45,12 @@ hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R,
 // --------------------------------------------------------------- layout
 // Blocked code store: vector v lives in block v/64, lane v%64; chunk c (16 B)
 // of a vector sits at byte ((v/64) * chunks + c) * 1024 + (v%64) * 16.
+// For b in {1, 2, 4} every 32-bit word of a chunk holds the canonical word
+// rotated left by 2 bits (field t of 4 bits at bits [4t+2, 4t+6) mod 32), so
+// the scan gets each 4-bit field times 4 in a byte with one mask per half.
+__host__ __device__ inline bool blocked_rotated(int bits) { return bits == 1 || bits == 2 || bits == 4; }
+__host__ __device__ inline uint32_t rotl2(uint32_t w) { return (w << 2) | (w >> 30); }
+__host__ __device__ inline uint32_t rotr2(uint32_t w) { return (w >> 2) | (w << 30); }
 inline int chunks_per_vector(int d, int bits) {
     // 3-bit codes are stored 10 per 32-bit word (2 pad bits per word)
     if (bits == 3) return (((d + 9) / 10) + 3) / 4;

@@ -5,8 +5,9 @@
 // Blocked layout (index storage): vector v belongs to 64-vector block v/64,
 // lane v%64; its i-th 16-byte chunk sits at ((v/64)*chunks + i)*1024 +
 // (v%64)*16, so the 64 lanes of a wave read one contiguous KiB per chunk.
-// For b in {1,2,4,8} chunk i holds canonical bytes [16i, 16i+16); for b = 3
-// every 32-bit word holds 10 codes (bits 3t..3t+2 for code t, 2 pad bits).
+// For b in {1,2,4,8} chunk i holds canonical bytes [16i, 16i+16), each
+// 32-bit word rotated left by 2 bits when b in {1,2,4}; for b = 3 every
+// 32-bit word holds 10 codes (bits 3t..3t+2 for code t, 2 pad bits).
 // Block summaries: W = ceil(T/64) words per block, bit t set when some vector
 // of the block belongs to tenant t.
 #include <hip/hip_runtime.h>
@@ -40,7 +41,14 @@ __global__ void canon_to_blocked_kernel(const uint8_t *__restrict__ canon,
         uint4 *dst = reinterpret_cast<uint4 *>(blocked + ((v >> 6) * chunks + c) * 1024 + (v & 63) * 16);
         const uint8_t *row = canon + i * rowbytes;
         if (bits != 3) {
-            *dst = reinterpret_cast<const uint4 *>(row)[c];
+            uint4 q4 = reinterpret_cast<const uint4 *>(row)[c];
+            if (blocked_rotated(bits)) {
+                q4.x = rotl2(q4.x);
+                q4.y = rotl2(q4.y);
+                q4.z = rotl2(q4.z);
+                q4.w = rotl2(q4.w);
+            }
+            *dst = q4;
         } else {
             uint32_t w[4];
             for (int q = 0; q < 4; ++q) {
@@ -69,7 +77,14 @@ __global__ void blocked_to_canon_kernel(const uint8_t *__restrict__ blocked,
             const int64_t v = e / chunks;
             const int c = (int)(e % chunks);
             const uint4 *src = reinterpret_cast<const uint4 *>(blocked + ((v >> 6) * chunks + c) * 1024 + (v & 63) * 16);
-            if (canon) reinterpret_cast<uint4 *>(canon + v * rowbytes)[c] = *src;
+            uint4 w = *src;
+            if (blocked_rotated(bits)) {
+                w.x = rotr2(w.x);
+                w.y = rotr2(w.y);
+                w.z = rotr2(w.z);
+                w.w = rotr2(w.w);
+            }
+            if (canon) reinterpret_cast<uint4 *>(canon + v * rowbytes)[c] = w;
             if (c == 0 && scales) scales[v] = blocked_scales[v];
         }
     } else {

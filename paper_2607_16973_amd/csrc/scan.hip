@@ -32,7 +32,9 @@ namespace {
 
 constexpr int SCAN_THREADS = 1024;
 constexpr int SCAN_WAVES = SCAN_THREADS / 64;
-constexpr int PF = 4;   // 16-byte chunks in flight per lane
+// Scheduling-barrier mask: ALU, SALU, MFMA, LDS and transcendental
+// instructions may move across, memory loads and stores to HBM may not.
+constexpr int kKeepVmem = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
 
 enum Mode { NIBBLE = 0, TRIBIT = 1, BYTE = 2 };
 
@@ -46,22 +48,41 @@ struct ScanParams {
     const float *cents;         // [levels]
     float *cand_s;              // [nq][G][k]
     int *cand_i;
+    int *gbound;                // [nq] order keys of a k-th-best lower bound, all workgroups
     int64_t n, nblk;
     int d, bits, chunks, W, k, nq;
-    int lut_floats;             // floats of LDS used by the table
+    int lut_words;              // 32-bit words of LDS used by the table
 };
 
-__device__ inline float nib8(const float *__restrict__ L, uint32_t w) {
-    // 8 consecutive 4-bit fields, each indexing its own 16-entry row
-    float a = L[0 * 16 + ((w >> 0) & 15)];
-    float b = L[1 * 16 + ((w >> 4) & 15)];
-    float c = L[2 * 16 + ((w >> 8) & 15)];
-    float d = L[3 * 16 + ((w >> 12) & 15)];
-    a += L[4 * 16 + ((w >> 16) & 15)];
-    b += L[5 * 16 + ((w >> 20) & 15)];
-    c += L[6 * 16 + ((w >> 24) & 15)];
-    d += L[7 * 16 + ((w >> 28) & 15)];
-    return (a + b) + (c + d);
+// ---------------------------------------------------------------- tables
+// b in {1,2,4}: one row of 16 int32 entries per 4-bit field of the code
+// stream (row r covers coordinates r*g .. r*g+g-1, g = 4/b), holding
+// round(2^sh * sum_t c[code_t] q'_j) -- fixed point with a per-query power of
+// two 2^sh chosen so that every possible sum of one entry per row fits in
+// int32: sum_r max_c |entry| <= 2^sh max|c| sum_j |q'_j| + rows/2 < 2^31.
+// The integer sums are then exact; the only error is the rounding of each
+// entry, at most rows * 2^-(sh+1) in total.
+// b = 3: float32 rows of 8 entries c[code] q'_j per coordinate.
+// b = 8: the 256 float32 centroids followed by q' (multiplied on the fly).
+
+// Sum of 8 int32 table hits addressed by the 8 4-bit fields of a stored
+// word w (the canonical word rotated left by 2 bits); row t of the 8 rows
+// starting at Lb (64 bytes per row) is indexed by field t.
+__device__ inline int nib8(const char *__restrict__ Lb, uint32_t w) {
+    uint32_t lo = w & 0x3C3C3C3Cu;                                  // byte b: field 2b   times 4
+    uint32_t hi = __builtin_amdgcn_alignbit(w, w, 4) & 0x3C3C3C3Cu; // byte b: field 2b+1 times 4
+    // keep the byte-aligned form: each address is then one add with a byte
+    // select (SDWA) instead of a shift, a mask and an add per field
+    asm volatile("" : "+v"(lo), "+v"(hi));
+    const int a0 = *reinterpret_cast<const int *>(Lb + 0 * 64 + (lo & 0xFFu));
+    const int a1 = *reinterpret_cast<const int *>(Lb + 1 * 64 + (hi & 0xFFu));
+    const int a2 = *reinterpret_cast<const int *>(Lb + 2 * 64 + ((lo >> 8) & 0xFFu));
+    const int a3 = *reinterpret_cast<const int *>(Lb + 3 * 64 + ((hi >> 8) & 0xFFu));
+    const int a4 = *reinterpret_cast<const int *>(Lb + 4 * 64 + ((lo >> 16) & 0xFFu));
+    const int a5 = *reinterpret_cast<const int *>(Lb + 5 * 64 + ((hi >> 16) & 0xFFu));
+    const int a6 = *reinterpret_cast<const int *>(Lb + 6 * 64 + (lo >> 24));
+    const int a7 = *reinterpret_cast<const int *>(Lb + 7 * 64 + (hi >> 24));
+    return (a0 + a1 + a2) + (a3 + a4 + a5) + (a6 + a7);
 }
 
 __device__ inline float tri10(const float *__restrict__ L, uint32_t w) {
@@ -83,12 +104,15 @@ __device__ inline float byte4(const float *__restrict__ cents, const float *__re
     return a + b;
 }
 
+template <int MODE> struct AccOf { typedef float type; };
+template <> struct AccOf<NIBBLE> { typedef int type; };
+
 template <int MODE>
-__device__ inline float chunk_sum(const float *__restrict__ lds, int c, uint4 v, int d) {
-    if (MODE == NIBBLE) {
-        const float *L = lds + c * 32 * 16;
-        return (nib8(L, v.x) + nib8(L + 128, v.y)) + (nib8(L + 256, v.z) + nib8(L + 384, v.w));
-    } else if (MODE == TRIBIT) {
+__device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__ lds, int c, uint4 v) {
+    if constexpr (MODE == NIBBLE) {
+        const char *Lb = reinterpret_cast<const char *>(lds) + c * 2048;
+        return (nib8(Lb, v.x) + nib8(Lb + 512, v.y)) + (nib8(Lb + 1024, v.z) + nib8(Lb + 1536, v.w));
+    } else if constexpr (MODE == TRIBIT) {
         const float *L = lds + c * 40 * 8;
         return (tri10(L, v.x) + tri10(L + 80, v.y)) + (tri10(L + 160, v.z) + tri10(L + 240, v.w));
     } else {
@@ -99,129 +123,276 @@ __device__ inline float chunk_sum(const float *__restrict__ lds, int c, uint4 v,
     }
 }
 
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
+    return v;
+}
+
+// Builds the table for one query; returns the fixed-point exponent sh
+// (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.
 template <int MODE>
-__device__ void build_table(float *lds, const ScanParams &p, const float *__restrict__ q) {
+__device__ int build_table(float *lds, float *red, const ScanParams &p, const float *__restrict__ q) {
     const int tid = threadIdx.x;
-    if (MODE == NIBBLE) {
-        const int g = 4 / p.bits;              // coordinates per 4-bit field
-        const int mask = (1 << p.bits) - 1;
-        const int entries = p.lut_floats;      // positions * 16
-        for (int e = tid; e < entries; e += SCAN_THREADS) {
-            const int pos = e >> 4, c = e & 15;
-            float v = 0.f;
-            for (int t = 0; t < g; ++t) v += p.cents[(c >> (p.bits * t)) & mask] * q[pos * g + t];
-            lds[e] = v;
+    if constexpr (MODE == NIBBLE) {
+        float part = 0.f;
+        for (int j = tid; j < p.d; j += SCAN_THREADS) part += fabsf(q[j]);
+        part = wave_sum(part);
+        if ((tid & 63) == 0) red[tid >> 6] = part;
+        __syncthreads();
+        double tot = 0.0;
+#pragma unroll
+        for (int w = 0; w < SCAN_WAVES; ++w) tot += (double)red[w];
+        const int L = 1 << p.bits;
+        const double cmax = fmax(fabs((double)p.cents[0]), fabs((double)p.cents[L - 1]));
+        // bound with margin for the float32 partial sums above
+        const double B = cmax * tot * (1.0 + 1e-5);
+        int sh = 0;
+        if (B > 0.0) {
+            sh = (int)floor(log2((2147483647.0 - p.d) / B));
+            sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
         }
-    } else if (MODE == TRIBIT) {
-        const int entries = p.lut_floats;      // positions * 8
-        for (int e = tid; e < entries; e += SCAN_THREADS) {
+        const double scale = ldexp(1.0, sh);
+        const int g = 4 / p.bits;
+        const int mask = L - 1;
+        int *T = reinterpret_cast<int *>(lds);
+        // one thread per 16-entry row: the row's coordinates are read once
+        const int rows = p.lut_words >> 4;
+        for (int r = tid; r < rows; r += SCAN_THREADS) {
+            double qv[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) qv[t] = t < g ? (double)q[r * g + t] : 0.0;
+            int4 *row = reinterpret_cast<int4 *>(T + r * 16);
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) {
+                int e[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int c = c4 * 4 + u;
+                    double v = 0.0;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (t < g) v += (double)p.cents[(c >> (p.bits * t)) & mask] * qv[t];
+                    e[u] = (int)llrint(v * scale);
+                }
+                row[c4] = make_int4(e[0], e[1], e[2], e[3]);
+            }
+        }
+        return sh;
+    } else if constexpr (MODE == TRIBIT) {
+        for (int e = tid; e < p.lut_words; e += SCAN_THREADS) {
             const int j = e >> 3, c = e & 7;
             lds[e] = (j < p.d) ? p.cents[c] * q[j] : 0.f;
         }
+        return 0;
     } else {
         for (int e = tid; e < 256; e += SCAN_THREADS) lds[e] = p.cents[e];
         for (int e = tid; e < p.d; e += SCAN_THREADS) lds[256 + e] = q[e];
+        return 0;
     }
 }
 
-template <int MODE, int S>
-__global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
-    extern __shared__ __attribute__((aligned(16))) float lds[];
-    uint64_t *allow_s = reinterpret_cast<uint64_t *>(lds + p.lut_floats);
-    float *stage_s = lds;                                   // reused after the scan
-    int *stage_i = reinterpret_cast<int *>(lds + SCAN_WAVES * 64 * S);
+// Order-preserving map of float32 onto int32 (for atomicMax thresholds).
+__device__ inline int fkey(float f) {
+    const int b = __float_as_int(f);
+    return b >= 0 ? b : (b ^ 0x7FFFFFFF);
+}
+__device__ inline float unfkey(int k) { return __int_as_float(k >= 0 ? k : (k ^ 0x7FFFFFFF)); }
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int G = gridDim.x;
-    const int g = blockIdx.x;
-    const bool filtered = p.allow != nullptr;
-
-    for (int qi = 0; qi < p.nq; ++qi) {
-        build_table<MODE>(lds, p, p.qrot + (int64_t)qi * p.d);
-        if (filtered)
-            for (int w = tid; w < p.W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)qi * p.W + w];
-        __syncthreads();
-
-        float ls[S];
-        int li[S];
+template <int S>
+struct WaveTopK {
+    float ls[S];
+    int li[S];
+    float th_s;      // this wave's k-th best (or -inf while fewer than k)
+    int th_i;
+    int seen_g;      // last global bound read (order key)
+    __device__ void reset() {
 #pragma unroll
         for (int a = 0; a < S; ++a) {
             ls[a] = -INFINITY;
             li[a] = INT_MAX;
         }
-        float th_s = -INFINITY;
-        int th_i = INT_MAX;
-
-        for (int64_t blk = g + (int64_t)G * wave; blk < p.nblk; blk += (int64_t)G * SCAN_WAVES) {
-            if (filtered) {
-                bool hit = false;
-                for (int w = lane; w < p.W; w += 64)
-                    hit |= (p.summaries[blk * p.W + w] & allow_s[w]) != 0;
-                if (!__any(hit)) continue;      // nothing in this block can match
+        th_s = -INFINITY;
+        th_i = INT_MAX;
+        seen_g = fkey(-INFINITY);
+    }
+    // Offer one (score, id) per lane.  A score strictly below the bound --
+    // the best k-th score any wave of this workgroup (wg_key, LDS) or of any
+    // workgroup (g_key, global) has proven -- cannot reach the top k and is
+    // dropped before the sort.
+    __device__ void offer(float sc, int id, int lane, int k, int *wg_key, int *g_key) {
+        const int gk = __hip_atomic_load(g_key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        seen_g = gk > seen_g ? gk : seen_g;
+        const int bk = *wg_key > seen_g ? *wg_key : seen_g;
+        const float bound = unfkey(bk);
+        const bool cand = better(sc, id, th_s, th_i) && !(sc < bound);
+        if (__any(cand)) {
+            if (!cand) {
+                sc = -INFINITY;
+                id = INT_MAX;
             }
-            const uint4 *src = p.codes + blk * p.chunks * 64 + lane;
+            wave_sort64(sc, id, lane);
+            merge_sorted64<S>(ls, li, sc, id, lane);
+            rank_entry<S>(ls, li, k - 1, th_s, th_i);
+            if (th_s > -INFINITY) {
+                const int key = fkey(th_s);
+                if (lane == 0) atomicMax(wg_key, key);
+                if (key > seen_g) {
+                    if (lane == 0)
+                        __hip_atomic_fetch_max(g_key, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    seen_g = key;
+                }
+            }
+        }
+    }
+};
+
+__global__ void fill_keys(int *p, int64_t n, int v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+template <int MODE, int S, int PF>
+__global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    uint64_t *allow_s = reinterpret_cast<uint64_t *>(lds + p.lut_words);
+    int *misc = reinterpret_cast<int *>(allow_s + p.W);     // [0]: workgroup bound key
+    float *red = reinterpret_cast<float *>(misc + 4);        // 16 floats
+    float *stage_s = lds;                                     // reused after the scan
+    int *stage_i = reinterpret_cast<int *>(lds + SCAN_WAVES * 64 * S);
+    typedef typename AccOf<MODE>::type acc_t;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    // wave-uniform: lets the compiler keep block and chunk indices in SGPRs
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = gridDim.x;
+    const int g = blockIdx.x;
+    const bool filtered = p.allow != nullptr;
+    const int CH = p.chunks;
+
+    // contiguous block range of this wave
+    const int64_t gb0 = p.nblk * g / G, gb1 = p.nblk * (g + 1) / G;
+    const int64_t b0 = gb0 + (gb1 - gb0) * wave / SCAN_WAVES;
+    const int64_t b1 = gb0 + (gb1 - gb0) * (wave + 1) / SCAN_WAVES;
+
+    for (int qi = 0; qi < p.nq; ++qi) {
+        const int sh = build_table<MODE>(lds, red, p, p.qrot + (int64_t)qi * p.d);
+        if (filtered)
+            for (int w = tid; w < p.W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)qi * p.W + w];
+        if (tid == 0) misc[0] = fkey(-INFINITY);
+        __syncthreads();
+
+        WaveTopK<S> top;
+        top.reset();
+        int64_t blk = b0;
+        while (blk < b1) {
+            // next run of consecutive blocks to scan
+            int64_t r0 = blk, r1 = b1;
+            if (filtered) {
+                // skip blocks whose tenant summary misses the allowlist, then
+                // extend the run over blocks that meet it
+                for (; r0 < b1; ++r0) {
+                    bool hit = false;
+                    for (int w = lane; w < p.W; w += 64)
+                        hit |= (p.summaries[r0 * p.W + w] & allow_s[w]) != 0;
+                    if (__any(hit)) break;
+                }
+                for (r1 = r0 + 1; r1 < b1; ++r1) {
+                    bool hit = false;
+                    for (int w = lane; w < p.W; w += 64)
+                        hit |= (p.summaries[r1 * p.W + w] & allow_s[w]) != 0;
+                    if (!__any(hit)) break;
+                }
+                if (r0 >= b1) break;
+            }
+            // stream the run as one sequence of F 16-byte chunks per lane
+            // wave-uniform base of the run; each lane adds its fixed 16-byte slot
+            const uint4 *src = p.codes + r0 * CH * 64;
+            const int64_t F = (r1 - r0) * CH;
+            // Prefetch ring: the refill of buf[i] is issued as soon as chunk i
+            // has been consumed.  Scheduling barriers keep every load where it
+            // is written (in ring order), so each chunk waits only for its own
+            // load with PF-1 younger loads still in flight.
             uint4 buf[PF];
 #pragma unroll
-            for (int i = 0; i < PF; ++i)
-                if (i < p.chunks) buf[i] = src[i * 64];
-            float acc = 0.f;
-            for (int c0 = 0; c0 < p.chunks; c0 += PF) {
+            for (int i = 0; i < PF; ++i) {
+                buf[i] = (src + (int64_t)(i < F ? i : F - 1) * 64)[lane];
+                __builtin_amdgcn_sched_barrier(kKeepVmem);
+            }
+            int64_t f = 0;
+            for (int64_t b = r0; b < r1; ++b) {
+                // per-vector loads first: in-order completion means waiting
+                // for them later does not drain the chunk prefetches
+                const uint4 *bsrc = src + f * 64;    // this block's first chunk
+                const int64_t vid = b * 64 + lane;
+                const bool inside = vid < p.n;
+                const float scl = p.scales[vid];
+                const int ten = filtered ? (int)p.tenants[vid] : 0;
+                acc_t acc = 0;
+                for (int c0 = 0; c0 < CH; c0 += PF) {
 #pragma unroll
-                for (int i = 0; i < PF; ++i) {
-                    const int c = c0 + i;
-                    if (c < p.chunks) {
-                        const uint4 v = buf[i];
-                        if (c + PF < p.chunks) buf[i] = src[(c + PF) * 64];
-                        acc += chunk_sum<MODE>(lds, c, v, p.d);
+                    for (int i = 0; i < PF; ++i) {
+                        // consume buf[i] before it is refilled, so the refill
+                        // reuses its registers and only waits for this chunk
+                        acc += chunk_sum<MODE>(lds, c0 + i, buf[i]);
+                        // past the end of the run the refill reads the first
+                        // chunk of this block again: a cache hit, no HBM traffic
+                        const int64_t nf = f + c0 + i + PF;
+                        const uint4 *nsrc = nf < F ? src + nf * 64 : bsrc;
+                        buf[i] = nsrc[lane];
+                        __builtin_amdgcn_sched_barrier(kKeepVmem);
                     }
                 }
+                f += CH;
+                bool ok = inside;
+                if (ok && filtered) ok = (allow_s[ten >> 6] >> (ten & 63)) & 1ull;
+                float sc;
+                if constexpr (MODE == NIBBLE)
+                    sc = ldexpf((float)acc * scl, -sh);
+                else
+                    sc = acc * scl;
+                top.offer(ok ? sc : -INFINITY, ok ? (int)vid : INT_MAX, lane, p.k, misc,
+                          p.gbound + qi);
             }
-            const int64_t vid = blk * 64 + lane;
-            bool ok = vid < p.n;
-            if (ok && filtered) {
-                const int t = p.tenants[vid];
-                ok = (allow_s[t >> 6] >> (t & 63)) & 1ull;
-            }
-            float sc = ok ? acc * p.scales[vid] : -INFINITY;
-            int id = ok ? (int)vid : INT_MAX;
-            const bool cand = better(sc, id, th_s, th_i);
-            if (__any(cand)) {
-                if (!cand) {
-                    sc = -INFINITY;
-                    id = INT_MAX;
-                }
-                wave_sort64(sc, id, lane);
-                merge_sorted64<S>(ls, li, sc, id, lane);
-                rank_entry<S>(ls, li, p.k - 1, th_s, th_i);
-            }
+            blk = r1;
         }
         __syncthreads();   // table no longer needed: reuse LDS for the wave lists
+        // tree merge of the 16 wave lists
 #pragma unroll
         for (int a = 0; a < S; ++a) {
-            stage_s[wave * 64 * S + a * 64 + lane] = ls[a];
-            stage_i[wave * 64 * S + a * 64 + lane] = li[a];
+            stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
+            stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
         }
         __syncthreads();
-        if (wave == 0) {
-            for (int w = 1; w < SCAN_WAVES; ++w) {
+        for (int step = 1; step < SCAN_WAVES; step <<= 1) {
+            if ((wave & (2 * step - 1)) == 0) {
                 float os[S];
                 int oi[S];
+                const int w = wave + step;
 #pragma unroll
                 for (int a = 0; a < S; ++a) {
                     os[a] = stage_s[w * 64 * S + a * 64 + lane];
                     oi[a] = stage_i[w * 64 * S + a * 64 + lane];
                 }
-                merge_lists<S>(ls, li, os, oi, lane);
+                merge_lists<S>(top.ls, top.li, os, oi, lane);
+#pragma unroll
+                for (int a = 0; a < S; ++a) {
+                    stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
+                    stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
+                }
             }
+            __syncthreads();
+        }
+        if (wave == 0) {
             const int64_t base = ((int64_t)qi * G + g) * p.k;
 #pragma unroll
             for (int a = 0; a < S; ++a) {
                 const int r = a * 64 + lane;
                 if (r < p.k) {
-                    p.cand_s[base + r] = ls[a];
-                    p.cand_i[base + r] = li[a];
+                    p.cand_s[base + r] = top.ls[a];
+                    p.cand_i[base + r] = top.li[a];
                 }
             }
         }
@@ -287,14 +458,14 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
     }
 }
 
-int lut_floats_for(const ScanShape &s) {
+int lut_words_for(const ScanShape &s) {
     if (s.bits == 8) return 256 + s.d;
     if (s.bits == 3) return s.chunks * 40 * 8;
     return s.chunks * 32 * 16;
 }
 
 size_t lds_bytes_for(const ScanShape &s, int S) {
-    const size_t table = (size_t)lut_floats_for(s) * 4 + (size_t)s.W * 8;
+    const size_t table = (size_t)lut_words_for(s) * 4 + (size_t)s.W * 8 + 16 + 64;
     const size_t stage = (size_t)SCAN_WAVES * 64 * S * 8;
     return table > stage ? table : stage;
 }
@@ -307,24 +478,33 @@ int64_t query_chunk(int64_t nq, int k, int grid) {
     return nq < qc ? nq : qc;
 }
 
-template <int MODE, int S>
+template <int MODE, int S, int PF>
 hipError_t launch_scan(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<MODE, S>,
+        hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<MODE, S, PF>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((scan_kernel<MODE, S>), dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+    hipLaunchKernelGGL((scan_kernel<MODE, S, PF>), dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
     return hipGetLastError();
+}
+
+// Prefetch depth: 8 chunks in flight per lane when the chunk count allows.
+template <int MODE, int S>
+hipError_t launch_scan_pf(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
+    if (p.chunks % 8 == 0) return launch_scan<MODE, S, 8>(p, grid, lds, stream);
+    if (p.chunks % 4 == 0) return launch_scan<MODE, S, 4>(p, grid, lds, stream);
+    if (p.chunks % 2 == 0) return launch_scan<MODE, S, 2>(p, grid, lds, stream);
+    return launch_scan<MODE, S, 1>(p, grid, lds, stream);
 }
 
 template <int S>
 hipError_t launch_scan_mode(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
-    if (p.bits == 8) return launch_scan<BYTE, S>(p, grid, lds, stream);
-    if (p.bits == 3) return launch_scan<TRIBIT, S>(p, grid, lds, stream);
-    return launch_scan<NIBBLE, S>(p, grid, lds, stream);
+    if (p.bits == 8) return launch_scan_pf<BYTE, S>(p, grid, lds, stream);
+    if (p.bits == 3) return launch_scan_pf<TRIBIT, S>(p, grid, lds, stream);
+    return launch_scan_pf<NIBBLE, S>(p, grid, lds, stream);
 }
 
 }  // namespace
@@ -342,6 +522,8 @@ size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int gri
     b = (b + 255) & ~(size_t)255;
     b += (size_t)qc * grid * k * (sizeof(float) + sizeof(int));
     b = (b + 255) & ~(size_t)255;
+    b += (size_t)qc * sizeof(int);
+    b = (b + 255) & ~(size_t)255;
     return b + 256;
 }
 
@@ -355,6 +537,9 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
     p8 += ((size_t)nq * s.d * sizeof(float) + 255) & ~(size_t)255;   // rotated queries live here
     float *cand_s = reinterpret_cast<float *>(p8);
     int *cand_i = reinterpret_cast<int *>(cand_s + (size_t)qc * grid * k);
+    uint8_t *after = reinterpret_cast<uint8_t *>(cand_i + (size_t)qc * grid * k);
+    int *gbound = reinterpret_cast<int *>(
+        (reinterpret_cast<uintptr_t>(after) + 255) & ~(uintptr_t)255);
     (void)ws_bytes;
     const int S = k <= 64 ? 1 : (k <= 128 ? 2 : 4);
     for (int64_t q0 = 0; q0 < nq; q0 += qc) {
@@ -369,6 +554,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.cents = cents32;
         p.cand_s = cand_s;
         p.cand_i = cand_i;
+        p.gbound = gbound;
         p.n = s.n;
         p.nblk = s.nblk;
         p.d = s.d;
@@ -377,9 +563,12 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.W = s.W;
         p.k = k;
         p.nq = (int)m;
-        p.lut_floats = lut_floats_for(s);
+        p.lut_words = lut_words_for(s);
         const size_t lds = lds_bytes_for(s, S);
-        hipError_t e;
+        hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
+                           (int)(0x807FFFFFu));   // order key of -inf
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
         if (S == 1)
             e = launch_scan_mode<1>(p, grid, lds, stream);
         else if (S == 2)
