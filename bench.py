@@ -29,6 +29,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# rocprofv3 summary of the scan kernel at this workload; it carries the HBM
+# counter readings and a hash of the kernel sources they were taken on
+SCAN_PROFILE = os.path.join(ROOT, "profiles", "scan_lut_d1536_n1m_k10.md")
+SCAN_SOURCES = ("scan.hip", "topk.h", "kernels.h")
 METRIC = "queries/sec and achieved HBM GB/s, 4-bit scan, d=1536, N=1M, k=10 (1 GPU)"
 
 
@@ -36,7 +40,32 @@ def log(msg: str) -> None:
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(X, Q, d, bits, k, n_full, sample_rows=16384, sample_queries=32):
+def scan_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in SCAN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_16973_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(queries_per_launch: int):
+    """HBM bytes per scan launch from the committed counter readings, or None
+    when they are absent or were taken on other kernel sources."""
+    import re
+    try:
+        with open(SCAN_PROFILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"traffic:\s*source=(\w+)\s+queries_per_launch=(\d+)\s+"
+                  r"fetch_bytes=([0-9.eE+]+)\s+write_bytes=([0-9.eE+]+)", text)
+    if not m or m.group(1) != scan_source_hash() or int(m.group(2)) != queries_per_launch:
+        return None
+    return float(m.group(3)) + float(m.group(4))
+
+
+def cpu_baseline(X, Q, d, bits, k, n_full, sample_rows=131072, sample_queries=256):
     """The oracle as it stands, on a bounded sample, scaled to N = n_full."""
     import numpy as np
 
@@ -72,6 +101,9 @@ def main() -> int:
     ap.add_argument("--k", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip recall / latency extras")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run three 1 GiB device-to-device copies (a kernel of "
+                         "known traffic for scaling the HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -193,6 +225,14 @@ def main() -> int:
         log("recall@%d %.4f  single-query latency %.3f ms" % (k, rec, extra["single_query_latency_ms_p50"]))
     del X
     torch.cuda.empty_cache()
+    if args.copy_calibration:
+        cal_a = torch.full((1 << 28,), 1.0, dtype=torch.float32, device=dev)
+        cal_b = torch.empty_like(cal_a)
+        for _ in range(3):
+            cal_b.copy_(cal_a)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 device-to-device copies of %d bytes" % (cal_a.numel() * 4))
+        del cal_a, cal_b
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -226,7 +266,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": measured_traffic(nq),
         },
         "cpu_baseline": cpu,
         "extra": extra,

@@ -3,7 +3,7 @@
  * (gfx950), as studied in "TurboVec" (arXiv 2607.16973).
  *
  * The library compresses L2-normalisable float32 embeddings with TurboQuant
- * (section II-B: normalise, rotate by a fixed random orthogonal matrix,
+ * (section II-B: normalise, rotate with one seeded orthogonal matrix,
  * Lloyd-Max scalar quantisation against boundaries derived analytically from
  * the post-rotation coordinate law, bit packing, length-renormalised scoring)
  * and answers brute-force top-k inner-product queries over the codes, with
@@ -56,7 +56,7 @@ const char *tq_last_error(void);
 /* Library version string, e.g. "tq 0.1.0 gfx950". */
 const char *tq_version(void);
 
-/* ------------------------------------------------------------------ a1 ----
+/* ------------------------------------------------------------- codebook ----
  * build_codebook(d, b) -- section II-B step 3.  Lloyd-Max scalar quantiser
  * with L = 2^bits levels for the law of one coordinate of a uniformly random
  * unit vector in R^d (density proportional to (1 - x^2)^((d-3)/2), the
@@ -77,9 +77,9 @@ tq_status tq_codebook_mse(const tq_codebook *cb, double *mse_out);
 
 void tq_codebook_free(tq_codebook *cb);
 
-/* ------------------------------------------------------------------ a2 ----
- * Rotation R(seed) -- section II-B step 2, "a fixed random orthogonal
- * matrix".  Haar-distributed d x d orthogonal matrix: a d x d matrix of
+/* ------------------------------------------------------------- rotation ----
+ * Rotation R(seed) -- section II-B step 2 (one orthogonal matrix, drawn
+ * at random once and then fixed).  Haar-distributed d x d orthogonal matrix: a d x d matrix of
  * standard normals (SplitMix64 counter stream of `seed`, 53-bit uniforms,
  * Box-Muller on consecutive pairs, row-major) factored by Householder QR,
  * with columns sign-corrected so the triangular factor has a positive
@@ -93,7 +93,7 @@ tq_status tq_rotation_matrix(const tq_rotation *rot, float *R_host);
 
 void tq_rotation_free(tq_rotation *rot);
 
-/* -------------------------------------------------------------- a3 + a4 ----
+/* --------------------------------------------------------------- encode ----
  * rotate_quantize(X) -> codes + scales -- section II-B steps 1-5.
  * For each float32 row x of X_dev [n][d] (row-major):
  *   n_x    = ||x|| (float64);
@@ -116,7 +116,7 @@ tq_status tq_rotate_quantize(const tq_codebook *cb, const tq_rotation *rot,
                              const float *X_dev, int64_t n, uint8_t *codes_dev,
                              float *scales_dev, void *stream);
 
-/* ------------------------------------------------------------------ a5 ----
+/* ------------------------------------------------------- query rotation ----
  * q' = R q for every row of Q_dev [nq][d] float32 -> Qrot_dev [nq][d]
  * float32 (section II-B step 2 applied to queries; queries are not
  * normalised).  Exposed so the query rotation can be checked on its own;

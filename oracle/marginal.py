@@ -1,9 +1,9 @@
 """Law of one coordinate of a randomly rotated unit vector (oracle; test use only).
 
-Section II-B, steps 2-3: after a fixed random orthogonal rotation, every
-coordinate of an L2-normalised vector follows the marginal the paper calls
-"Beta / N(0, 1/d)".  For a vector uniform on the unit sphere of R^d that law
-is exact: X has density
+Section II-B, steps 2-3: once an L2-normalised vector has been rotated by the
+random orthogonal matrix, each of its coordinates follows the marginal that
+the paper names as Beta, approaching N(0, 1/d).  For a vector uniform on the
+unit sphere of R^d that law is exact: X has density
 
     f_d(x) = C_d (1 - x^2)^((d-3)/2)  on [-1, 1],
     C_d    = Gamma(d/2) / (sqrt(pi) Gamma((d-1)/2)),

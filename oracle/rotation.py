@@ -1,7 +1,7 @@
 """Seeded random orthogonal rotation (oracle; test use only).
 
-Section II-B, step 2: vectors are multiplied by a fixed random orthogonal
-matrix R.  The paper does not fix the law, the generator or the seed; the
+Section II-B, step 2: every vector is multiplied by one orthogonal matrix R,
+drawn at random once and then kept.  The paper does not fix the law, the generator or the seed; the
 reading taken here (shared with the library, which implements it separately):
 
 * Random numbers: SplitMix64 in its counter form, z_i = mix(seed + (i+1)*gamma)
