@@ -24,8 +24,11 @@ LIB = os.path.join(PKG, "libtq.so")
 HIP_SOURCES = ["encode.hip", "scan.hip", "layout.hip", "api.cpp"]
 # Per-source extra flags.  The scan's prefetch ring must stay where it is
 # written: machine sinking would move every refill into the loop latch and
-# serialise the loads with the table lookups.
-EXTRA_FLAGS = {"scan.hip": ["-mllvm", "-disable-machine-sink"]}
+# serialise the loads with the table lookups.  The atomic optimizer would
+# turn the one-lane work-claim atomics into wave-wide ones whose result is
+# read at once, stalling on the LDS round trip the scan hides.
+EXTRA_FLAGS = {"scan.hip": ["-mllvm", "-disable-machine-sink",
+                            "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
 HOST_SOURCES = ["codebook.cpp", "rotation.cpp"]
 
 

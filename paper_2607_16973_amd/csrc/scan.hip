@@ -107,11 +107,16 @@ __device__ inline float byte4(const float *__restrict__ cents, const float *__re
 template <int MODE> struct AccOf { typedef float type; };
 template <> struct AccOf<NIBBLE> { typedef int type; };
 
+// Sum of the 32 table hits of one 16-byte chunk; Lb is the chunk's 2 KiB of
+// table rows.
+__device__ inline int nib_chunk(const char *__restrict__ Lb, uint4 v) {
+    return (nib8(Lb, v.x) + nib8(Lb + 512, v.y)) + (nib8(Lb + 1024, v.z) + nib8(Lb + 1536, v.w));
+}
+
 template <int MODE>
 __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__ lds, int c, uint4 v) {
     if constexpr (MODE == NIBBLE) {
-        const char *Lb = reinterpret_cast<const char *>(lds) + c * 2048;
-        return (nib8(Lb, v.x) + nib8(Lb + 512, v.y)) + (nib8(Lb + 1024, v.z) + nib8(Lb + 1536, v.w));
+        return nib_chunk(reinterpret_cast<const char *>(lds) + c * 2048, v);
     } else if constexpr (MODE == TRIBIT) {
         const float *L = lds + c * 40 * 8;
         return (tri10(L, v.x) + tri10(L + 80, v.y)) + (tri10(L + 160, v.z) + tri10(L + 240, v.w));
@@ -129,56 +134,102 @@ __device__ inline float wave_sum(float v) {
     return v;
 }
 
+// 4-bit-field tables (b in {1, 2, 4}): row r of 16 entries covers
+// coordinates r*g .. r*g+g-1 (g = 4/b) and rows = d*b/4 <= 2048, so thread t
+// owns rows t and t + 1024.  Loads the thread's coordinates of q'.
+__device__ inline void load_nibble_query(const ScanParams &p, const float *__restrict__ q,
+                                         float (&qv)[2][4]) {
+    const int g = 4 / p.bits;
+    const int rows = p.lut_words >> 4;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+        const int r = threadIdx.x + m * SCAN_THREADS;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) qv[m][t] = (r < rows && t < g) ? q[r * g + t] : 0.f;
+    }
+}
+
+// Writes this wave's share of sum_j |q'_j| to red[wave] (16 floats of LDS).
+__device__ inline void nibble_abs_sum(float *red, const float (&qv)[2][4]) {
+    float part = 0.f;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) part += fabsf(qv[m][t]);
+    part = wave_sum(part);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
+}
+
+// Writes the int32 table from the coordinates loaded by load_nibble_query,
+// once red[] holds the 16 wave sums of |q'| (nibble_abs_sum, then a
+// barrier); returns the table's exponent sh.  The caller synchronises
+// before the table is read.
+//
+// Entries are rounded from float32 products: each is within 1/2 unit of
+// 2^sh c q' plus 2^-23 of its magnitude, so the summed error stays below
+// 2^-23 B + rows/2 units, B = max|c| sum_j |q'_j| -- far inside the score
+// tolerance.
+__device__ inline int build_nibble_table(float *lds, const float *red, const float *cents,
+                                         const ScanParams &p, const float (&qv)[2][4]) {
+    const int tid = threadIdx.x;
+    const int rows = p.lut_words >> 4;
+    const int L = 1 << p.bits;
+    // the levels: at most 16 (`cents` holds 16 values, unused ones finite)
+    float cl[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) cl[c] = cents[c];
+    double tot = 0.0;
+#pragma unroll
+    for (int w = 0; w < SCAN_WAVES; ++w) tot += (double)red[w];
+    const double cmax = fmax(fabs((double)cl[0]), fabs((double)cl[L - 1]));
+    // bound with margin for the float32 partial sums and products
+    const double B = cmax * tot * (1.0 + 1e-5);
+    int sh = 0;
+    if (B > 0.0) {
+        sh = (int)floor(log2((2147483647.0 - 2.0 * p.d) / B));
+        sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
+    }
+    const float scale = ldexpf(1.0f, sh);
+    int *T = reinterpret_cast<int *>(lds);
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+        const int r = tid + m * SCAN_THREADS;
+        if (r < rows) {
+            const float q0 = qv[m][0] * scale, q1 = qv[m][1] * scale;
+            const float q2 = qv[m][2] * scale, q3 = qv[m][3] * scale;
+            int e[16];
+            if (p.bits == 4) {
+#pragma unroll
+                for (int c = 0; c < 16; ++c) e[c] = (int)rintf(cl[c] * q0);
+            } else if (p.bits == 2) {
+#pragma unroll
+                for (int c = 0; c < 16; ++c) e[c] = (int)rintf(fmaf(cl[c & 3], q0, cl[c >> 2] * q1));
+            } else {
+#pragma unroll
+                for (int c = 0; c < 16; ++c)
+                    e[c] = (int)rintf(fmaf(cl[c & 1], q0, cl[(c >> 1) & 1] * q1) +
+                                      fmaf(cl[(c >> 2) & 1], q2, cl[c >> 3] * q3));
+            }
+            int4 *row = reinterpret_cast<int4 *>(T + r * 16);
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4)
+                row[c4] = make_int4(e[4 * c4], e[4 * c4 + 1], e[4 * c4 + 2], e[4 * c4 + 3]);
+        }
+    }
+    return sh;
+}
+
 // Builds the table for one query; returns the fixed-point exponent sh
 // (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.
 template <int MODE>
 __device__ int build_table(float *lds, float *red, const ScanParams &p, const float *__restrict__ q) {
     const int tid = threadIdx.x;
     if constexpr (MODE == NIBBLE) {
-        float part = 0.f;
-        for (int j = tid; j < p.d; j += SCAN_THREADS) part += fabsf(q[j]);
-        part = wave_sum(part);
-        if ((tid & 63) == 0) red[tid >> 6] = part;
+        float qv[2][4];
+        load_nibble_query(p, q, qv);
+        nibble_abs_sum(red, qv);
         __syncthreads();
-        double tot = 0.0;
-#pragma unroll
-        for (int w = 0; w < SCAN_WAVES; ++w) tot += (double)red[w];
-        const int L = 1 << p.bits;
-        const double cmax = fmax(fabs((double)p.cents[0]), fabs((double)p.cents[L - 1]));
-        // bound with margin for the float32 partial sums above
-        const double B = cmax * tot * (1.0 + 1e-5);
-        int sh = 0;
-        if (B > 0.0) {
-            sh = (int)floor(log2((2147483647.0 - p.d) / B));
-            sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
-        }
-        const double scale = ldexp(1.0, sh);
-        const int g = 4 / p.bits;
-        const int mask = L - 1;
-        int *T = reinterpret_cast<int *>(lds);
-        // one thread per 16-entry row: the row's coordinates are read once
-        const int rows = p.lut_words >> 4;
-        for (int r = tid; r < rows; r += SCAN_THREADS) {
-            double qv[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) qv[t] = t < g ? (double)q[r * g + t] : 0.0;
-            int4 *row = reinterpret_cast<int4 *>(T + r * 16);
-#pragma unroll
-            for (int c4 = 0; c4 < 4; ++c4) {
-                int e[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int c = c4 * 4 + u;
-                    double v = 0.0;
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        if (t < g) v += (double)p.cents[(c >> (p.bits * t)) & mask] * qv[t];
-                    e[u] = (int)llrint(v * scale);
-                }
-                row[c4] = make_int4(e[0], e[1], e[2], e[3]);
-            }
-        }
-        return sh;
+        return build_nibble_table(lds, red, p.cents, p, qv);
     } else if constexpr (MODE == TRIBIT) {
         for (int e = tid; e < p.lut_words; e += SCAN_THREADS) {
             const int j = e >> 3, c = e & 7;
@@ -221,7 +272,12 @@ struct WaveTopK {
     // workgroup (g_key, global) has proven -- cannot reach the top k and is
     // dropped before the sort.
     __device__ void offer(float sc, int id, int lane, int k, int *wg_key, int *g_key) {
-        const int gk = __hip_atomic_load(g_key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        offer_seen(sc, id, lane, k, wg_key, g_key,
+                   __hip_atomic_load(g_key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    }
+    // As offer(), with gk a value of the global bound read earlier by the
+    // caller (any earlier value is a valid, if weaker, bound).
+    __device__ void offer_seen(float sc, int id, int lane, int k, int *wg_key, int *g_key, int gk) {
         seen_g = gk > seen_g ? gk : seen_g;
         const int bk = *wg_key > seen_g ? *wg_key : seen_g;
         const float bound = unfkey(bk);
@@ -253,11 +309,130 @@ __global__ void fill_keys(int *p, int64_t n, int v) {
         p[i] = v;
 }
 
+// LDS words from the start of dynamic LDS that the table and, after the
+// scan, the merge stage (16 lists of 64*S scores and ids) may occupy; the
+// regions that must survive the merge start here.
+__host__ __device__ inline int aux_words(int lut_words, int S) {
+    const int stage = SCAN_WAVES * 64 * S * 2;
+    return lut_words > stage ? lut_words : stage;
+}
+
+// Workgroup top-k from the 16 wave lists, in three steps.
+//  1. collect_survivors: entries below a proven bound -- the best k-th score
+//     of any wave (LDS key) or of any workgroup (as last seen by the wave) --
+//     cannot reach the top k; each wave appends its other entries to a list
+//     of up to 64 in LDS, counted in *cnt (which starts at zero).
+//  2. If at most 64 survive, write_survivors (one wave) sorts them and
+//     writes the workgroup's k best.
+//  3. Otherwise tree_merge merges the full lists pairwise through LDS.
+template <int S>
+__device__ inline void collect_survivors(const WaveTopK<S> &top, int wg_key, float *surv_s,
+                                         int *surv_i, int *cnt, int lane) {
+    const int bk = wg_key > top.seen_g ? wg_key : top.seen_g;
+    const float bound = unfkey(bk);
+#pragma unroll
+    for (int a = 0; a < S; ++a) {
+        const bool keep = top.li[a] != INT_MAX && !(top.ls[a] < bound);
+        const uint64_t m = __ballot(keep);
+        if (m) {
+            int base = 0;
+            if (lane == 0) base = atomicAdd(cnt, __popcll(m));
+            base = __builtin_amdgcn_readfirstlane(base);
+            const int pos = base + __popcll(m & ((1ull << lane) - 1));
+            if (keep && pos < 64) {
+                surv_s[pos] = top.ls[a];
+                surv_i[pos] = top.li[a];
+            }
+        }
+    }
+}
+
+template <int S>
+__device__ inline void write_survivors(const float *surv_s, const int *surv_i, int total,
+                                       const ScanParams &p, int64_t out, int lane) {
+    float sv = lane < total ? surv_s[lane] : -INFINITY;
+    int iv = lane < total ? surv_i[lane] : INT_MAX;
+    wave_sort64(sv, iv, lane);
+#pragma unroll
+    for (int a = 0; a < S; ++a) {
+        const int r = a * 64 + lane;
+        if (r < p.k) {
+            p.cand_s[out + r] = a == 0 ? sv : -INFINITY;
+            p.cand_i[out + r] = a == 0 ? iv : INT_MAX;
+        }
+    }
+}
+
+// Pairwise merge of the 16 wave lists through LDS (stage_* hold 16 x 64*S
+// entries); wave 0 writes the result.  Starts and ends with a barrier.
+template <int S>
+__device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i, int wave,
+                                  int lane, const ScanParams &p, int64_t out) {
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < S; ++a) {
+        stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
+        stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
+    }
+    __syncthreads();
+    for (int step = 1; step < SCAN_WAVES; step <<= 1) {
+        if ((wave & (2 * step - 1)) == 0) {
+            float os[S];
+            int oi[S];
+            const int w = wave + step;
+#pragma unroll
+            for (int a = 0; a < S; ++a) {
+                os[a] = stage_s[w * 64 * S + a * 64 + lane];
+                oi[a] = stage_i[w * 64 * S + a * 64 + lane];
+            }
+            merge_lists<S>(top.ls, top.li, os, oi, lane);
+#pragma unroll
+            for (int a = 0; a < S; ++a) {
+                stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
+                stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
+            }
+        }
+        __syncthreads();
+    }
+    if (wave == 0) {
+#pragma unroll
+        for (int a = 0; a < S; ++a) {
+            const int r = a * 64 + lane;
+            if (r < p.k) {
+                p.cand_s[out + r] = top.ls[a];
+                p.cand_i[out + r] = top.li[a];
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// The three steps with their barriers, for the block-per-wave scan: the
+// table's LDS holds the survivors and the stage (misc[0]: bound key,
+// misc[2]: survivor count, zero on entry and on return).
+template <int S>
+__device__ inline void workgroup_merge(WaveTopK<S> &top, float *stage_s, int *stage_i, int *misc,
+                                       int wave, int lane, const ScanParams &p, int qi) {
+    __syncthreads();   // every offer is done; the table's LDS is free
+    const int64_t out = ((int64_t)qi * gridDim.x + blockIdx.x) * p.k;
+    collect_survivors<S>(top, misc[0], stage_s, stage_i, misc + 2, lane);
+    __syncthreads();
+    const int total = misc[2];
+    if (total <= 64) {
+        if (wave == 0) write_survivors<S>(stage_s, stage_i, total, p, out, lane);
+    } else {
+        tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);
+    }
+    __syncthreads();   // LDS is rebuilt for the next query
+    if (threadIdx.x == 0) misc[2] = 0;
+}
+
 template <int MODE, int S, int PF>
 __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
-    uint64_t *allow_s = reinterpret_cast<uint64_t *>(lds + p.lut_words);
-    int *misc = reinterpret_cast<int *>(allow_s + p.W);     // [0]: workgroup bound key
+    // [0, aux): the table, later the merge stage; then the fixed regions
+    uint64_t *allow_s = reinterpret_cast<uint64_t *>(lds + aux_words(p.lut_words, S));
+    int *misc = reinterpret_cast<int *>(allow_s + p.W);     // [0] bound key, [2] merge count
     float *red = reinterpret_cast<float *>(misc + 4);        // 16 floats
     float *stage_s = lds;                                     // reused after the scan
     int *stage_i = reinterpret_cast<int *>(lds + SCAN_WAVES * 64 * S);
@@ -277,6 +452,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
     const int64_t b0 = gb0 + (gb1 - gb0) * wave / SCAN_WAVES;
     const int64_t b1 = gb0 + (gb1 - gb0) * (wave + 1) / SCAN_WAVES;
 
+    if (tid == 0) misc[2] = 0;
     for (int qi = 0; qi < p.nq; ++qi) {
         const int sh = build_table<MODE>(lds, red, p, p.qrot + (int64_t)qi * p.d);
         if (filtered)
@@ -358,45 +534,190 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
             }
             blk = r1;
         }
-        __syncthreads();   // table no longer needed: reuse LDS for the wave lists
-        // tree merge of the 16 wave lists
+        workgroup_merge<S>(top, stage_s, stage_i, misc, wave, lane, p, qi);
+    }
+}
+
+// Blocks per accumulation pass of the split scan: 64 blocks x 64 int32 sums
+// = 16 KiB of LDS.
+constexpr int kPassBlocks = 64;
+
+// Unfiltered scan for b in {1, 2, 4} with the work of a workgroup handed
+// out in groups of 8 chunks (8 KiB of one block's codes) rather than whole
+// blocks.
+//  * Every query covers the same blocks of the workgroup, taken in passes of
+//    up to 64 blocks.  The (query, pass, group) work items are numbered in
+//    that order and each wave claims its next item from an LDS counter one
+//    item ahead of the one it is scoring, so the ring of 8 loads always
+//    holds the next group -- also across pass and query boundaries: while
+//    the workgroup merges one query's lists and builds the next table, the
+//    codes of the next query's first groups are already on their way.
+//  * The waves, which the hardware does not run at equal speed, finish a
+//    pass within one group of each other.
+//  * A wave adds its integer sum for a group into the block's LDS slot with
+//    an atomic add (integer: exact and order-free, so the result does not
+//    depend on who scored what), then counts the group done; the wave that
+//    completes a block turns its sums into scores and offers them to its
+//    top-k while the other waves stream on.
+//  * Per query there are three barriers: end of the scan, survivors
+//    collected, next table built (the survivors' sort overlaps the build).
+template <int S>
+__global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) {
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    // [0, aux): the table (and the tree-merge stage); then the fixed regions
+    const int aux = aux_words(p.lut_words, S);
+    int *accb = reinterpret_cast<int *>(lds + aux);   // [kPassBlocks][64] block sums
+    int *done = accb + kPassBlocks * 64;              // [kPassBlocks] finished groups
+    int *misc = done + kPassBlocks;                   // [0] bound key, [1] tickets, [2] survivors
+    float *red = reinterpret_cast<float *>(misc + 4); // 16 wave sums of |q'|
+    float *cents_s = red + 16;                        // 16 levels
+    float *surv_s = cents_s + 16;                     // 64 survivors
+    int *surv_i = reinterpret_cast<int *>(surv_s + 64);
+    float *stage_s = lds;
+    int *stage_i = reinterpret_cast<int *>(lds + SCAN_WAVES * 64 * S);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = gridDim.x;
+    const int g = blockIdx.x;
+    const int CH = p.chunks;          // multiple of 8
+    const int GPB = CH >> 3;          // 8-chunk groups per block
+    const int64_t gb0 = p.nblk * g / G, gb1 = p.nblk * (g + 1) / G;
+    const int nbq = (int)(gb1 - gb0);                       // blocks per query
+    const int NGq = nbq * GPB;                              // groups per query
+    const int npass = (nbq + kPassBlocks - 1) / kPassBlocks;
+    const int PG = kPassBlocks * GPB;                       // groups per full pass
+    const int total = p.nq * NGq;                           // work items (host-bounded)
+    const uint4 *wg_src = p.codes + gb0 * CH * 64;
+    const char *lut = reinterpret_cast<const char *>(lds);
+    // lane 0 takes a ticket; the wave reads it from lane 0 when it needs it
+    auto take = [&](int *ctr) {
+        int v = 0;
+        if (lane == 0) v = atomicAdd(ctr, 1);
+        return v;
+    };
+    // pass number, counted over all queries, of a work item
+    auto stage_of = [&](int t) {
+        const int q = t / NGq;
+        return q * npass + (t - q * NGq) / PG;
+    };
+
+    for (int e = tid; e < kPassBlocks * 65; e += SCAN_THREADS) accb[e] = 0;   // sums and counts
+    if (tid < 16) cents_s[tid] = p.cents[tid];
+    if (tid == 0) {
+        misc[0] = fkey(-INFINITY);
+        misc[1] = 0;
+        misc[2] = 0;
+    }
+    if (p.nq == 0) return;
+    float qv[2][4];
+    load_nibble_query(p, p.qrot, qv);
+    nibble_abs_sum(red, qv);
+    __syncthreads();
+    int sh = build_nibble_table(lds, red, cents_s, p, qv);
+    __syncthreads();
+
+    // this wave's current and next work items, and the ring holding the
+    // current one's 8 chunks
+    int tk = __builtin_amdgcn_readfirstlane(take(misc + 1));
+    int nxt = __builtin_amdgcn_readfirstlane(take(misc + 1));
+    // wave-uniform base of a group; each lane adds its 16-byte slot
+    const uint4 *csrc = wg_src + (int64_t)(tk < total ? tk % NGq : 0) * 8 * 64;
+    uint4 buf[8];
+    if (tk < total) {
 #pragma unroll
-        for (int a = 0; a < S; ++a) {
-            stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
-            stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
+        for (int i = 0; i < 8; ++i) {
+            buf[i] = (csrc + i * 64)[lane];
+            __builtin_amdgcn_sched_barrier(kKeepVmem);
         }
+    }
+    for (int qi = 0; qi < p.nq; ++qi) {
+        WaveTopK<S> top;
+        top.reset();
+        for (int ps = 0; ps < npass; ++ps) {
+            if (ps > 0) __syncthreads();   // the previous pass's slots are free again
+            const int sid = qi * npass + ps;
+            const int64_t p0 = gb0 + (int64_t)ps * kPassBlocks;
+            while (tk < total && stage_of(tk) == sid) {
+                const int gp = tk - qi * NGq - ps * PG;   // group within the pass
+                const int bl = gp / GPB;
+                const int c0 = (gp - bl * GPB) * 8;
+                const int64_t vid = (p0 + bl) * 64 + lane;
+                const bool inside = vid < p.n;
+                // The group that completes a block needs the vectors'
+                // scales and the global bound.  Groups are claimed in order,
+                // so that is almost always the block's last group: it loads
+                // them ahead of its lookups; any other group that turns out
+                // to complete the block loads them when it does.
+                const bool last = c0 == CH - 8;
+                float scl = 0.f;
+                int gk = 0;
+                if (last) {
+                    scl = p.scales[inside ? vid : 0];
+                    gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+                }
+                // past the last item the refills read this group again:
+                // cache hits, no HBM traffic
+                const uint4 *nsrc = nxt < total ? wg_src + (int64_t)(nxt % NGq) * 8 * 64 : csrc;
+                // the ticket after next is taken now and read after the
+                // group's lookups, which hide its LDS round trip
+                const int ticket = take(misc + 1);
+                const char *Lb = lut + c0 * 2048;
+                int acc = 0;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    // consume buf[i], then refill it with the next group
+                    acc += nib_chunk(Lb + i * 2048, buf[i]);
+                    buf[i] = (nsrc + i * 64)[lane];
+                    __builtin_amdgcn_sched_barrier(kKeepVmem);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                const int nxt2 = __builtin_amdgcn_readfirstlane(ticket);
+                atomicAdd(&accb[bl * 64 + lane], acc);
+                // LDS executes each wave's operations in order, so when the
+                // count reaches GPB every group's sum is in the slot
+                const int fin = __builtin_amdgcn_readfirstlane(take(done + bl));
+                if (fin == GPB - 1) {
+                    if (!last) {
+                        scl = p.scales[inside ? vid : 0];
+                        gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    const int sum = accb[bl * 64 + lane];
+                    accb[bl * 64 + lane] = 0;
+                    if (lane == 0) done[bl] = 0;
+                    const float sc = ldexpf((float)sum * scl, -sh);
+                    top.offer_seen(inside ? sc : -INFINITY, inside ? (int)vid : INT_MAX, lane, p.k,
+                                   misc, p.gbound + qi, gk);
+                }
+                tk = nxt;
+                nxt = nxt2;
+                csrc = nsrc;
+            }
+        }
+        // a wave that is done loads the next query's coordinates and |q'|
+        // sum while the others finish (red was last read by this table's build)
+        const bool more = qi + 1 < p.nq;
+        if (more) {
+            load_nibble_query(p, p.qrot + (int64_t)(qi + 1) * p.d, qv);
+            nibble_abs_sum(red, qv);
+        }
+        __syncthreads();   // scan done: every offer made, the bound key final
+        const int64_t out = ((int64_t)qi * G + g) * p.k;
+        collect_survivors<S>(top, misc[0], surv_s, surv_i, misc + 2, lane);
         __syncthreads();
-        for (int step = 1; step < SCAN_WAVES; step <<= 1) {
-            if ((wave & (2 * step - 1)) == 0) {
-                float os[S];
-                int oi[S];
-                const int w = wave + step;
-#pragma unroll
-                for (int a = 0; a < S; ++a) {
-                    os[a] = stage_s[w * 64 * S + a * 64 + lane];
-                    oi[a] = stage_i[w * 64 * S + a * 64 + lane];
-                }
-                merge_lists<S>(top.ls, top.li, os, oi, lane);
-#pragma unroll
-                for (int a = 0; a < S; ++a) {
-                    stage_s[wave * 64 * S + a * 64 + lane] = top.ls[a];
-                    stage_i[wave * 64 * S + a * 64 + lane] = top.li[a];
-                }
-            }
-            __syncthreads();
+        const int ns = misc[2];
+        if (ns <= 64) {
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
+        } else {
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
-        if (wave == 0) {
-            const int64_t base = ((int64_t)qi * G + g) * p.k;
-#pragma unroll
-            for (int a = 0; a < S; ++a) {
-                const int r = a * 64 + lane;
-                if (r < p.k) {
-                    p.cand_s[base + r] = top.ls[a];
-                    p.cand_i[base + r] = top.li[a];
-                }
-            }
-        }
-        __syncthreads();   // LDS is rebuilt for the next query
+        if (more) sh = build_nibble_table(lds, red, cents_s, p, qv);
+        if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
+        __syncthreads();   // table ready; survivor count read by every wave
+        if (tid == 0) misc[2] = 0;
     }
 }
 
@@ -464,16 +785,28 @@ int lut_words_for(const ScanShape &s) {
     return s.chunks * 32 * 16;
 }
 
-size_t lds_bytes_for(const ScanShape &s, int S) {
-    const size_t table = (size_t)lut_words_for(s) * 4 + (size_t)s.W * 8 + 16 + 64;
-    const size_t stage = (size_t)SCAN_WAVES * 64 * S * 8;
-    return table > stage ? table : stage;
+// The split scan serves unfiltered searches over 1-, 2- and 4-bit codes
+// whose chunk count is a multiple of its 8-chunk groups.
+bool use_split(const ScanShape &s, bool filtered) {
+    return !filtered && (s.bits == 1 || s.bits == 2 || s.bits == 4) && s.chunks % 8 == 0;
 }
 
-// Queries per scan launch: as many as fit a 256 MiB candidate buffer.
-int64_t query_chunk(int64_t nq, int k, int grid) {
+size_t lds_bytes_for(const ScanShape &s, int S, bool split) {
+    // split: block sums and counts, misc, |q'| sums, levels, 64 survivors
+    const size_t fixed = split ? (size_t)kPassBlocks * 65 * 4 + 16 + 64 + 64 + 512
+                               : (size_t)s.W * 8 + 16 + 64;
+    return (size_t)aux_words(lut_words_for(s), S) * 4 + fixed;
+}
+
+// Queries per scan launch: as many as fit a 256 MiB candidate buffer, and
+// few enough that the split scan's work items of one workgroup (queries x
+// its 8-chunk groups) stay below 2^30.
+int64_t query_chunk(const ScanShape &s, int64_t nq, int k, int grid) {
     const int64_t per = (int64_t)grid * k * (int64_t)(sizeof(float) + sizeof(int));
     int64_t qc = ((int64_t)256 << 20) / per;
+    const int64_t groups = ((s.nblk + grid - 1) / grid) * (s.chunks / 8 + 1);
+    const int64_t qt = ((int64_t)1 << 30) / (groups + 1);
+    if (qt < qc) qc = qt;
     if (qc < 1) qc = 1;
     return nq < qc ? nq : qc;
 }
@@ -501,7 +834,22 @@ hipError_t launch_scan_pf(const ScanParams &p, int grid, size_t lds, hipStream_t
 }
 
 template <int S>
-hipError_t launch_scan_mode(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
+hipError_t launch_split(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)split_scan_kernel<S>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    hipLaunchKernelGGL(split_scan_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+    return hipGetLastError();
+}
+
+template <int S>
+hipError_t launch_scan_mode(const ScanParams &p, int grid, size_t lds, bool split,
+                            hipStream_t stream) {
+    if (split) return launch_split<S>(p, grid, lds, stream);
     if (p.bits == 8) return launch_scan_pf<BYTE, S>(p, grid, lds, stream);
     if (p.bits == 3) return launch_scan_pf<TRIBIT, S>(p, grid, lds, stream);
     return launch_scan_pf<NIBBLE, S>(p, grid, lds, stream);
@@ -517,7 +865,7 @@ int device_cu_count() {
 }
 
 size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid) {
-    const int64_t qc = query_chunk(nq, k, grid);
+    const int64_t qc = query_chunk(s, nq, k, grid);
     size_t b = (size_t)nq * s.d * sizeof(float);
     b = (b + 255) & ~(size_t)255;
     b += (size_t)qc * grid * k * (sizeof(float) + sizeof(int));
@@ -532,7 +880,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
                       const float *Qrot, int64_t nq, int k, const uint64_t *allow, int grid,
                       void *ws, size_t ws_bytes, int64_t *ids, float *scores,
                       hipStream_t stream) {
-    const int64_t qc = query_chunk(nq, k, grid);
+    const int64_t qc = query_chunk(s, nq, k, grid);
     uint8_t *p8 = static_cast<uint8_t *>(ws);
     p8 += ((size_t)nq * s.d * sizeof(float) + 255) & ~(size_t)255;   // rotated queries live here
     float *cand_s = reinterpret_cast<float *>(p8);
@@ -564,17 +912,18 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.k = k;
         p.nq = (int)m;
         p.lut_words = lut_words_for(s);
-        const size_t lds = lds_bytes_for(s, S);
+        const bool split = use_split(s, allow != nullptr);
+        const size_t lds = lds_bytes_for(s, S, split);
         hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
                            (int)(0x807FFFFFu));   // order key of -inf
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (S == 1)
-            e = launch_scan_mode<1>(p, grid, lds, stream);
+            e = launch_scan_mode<1>(p, grid, lds, split, stream);
         else if (S == 2)
-            e = launch_scan_mode<2>(p, grid, lds, stream);
+            e = launch_scan_mode<2>(p, grid, lds, split, stream);
         else
-            e = launch_scan_mode<4>(p, grid, lds, stream);
+            e = launch_scan_mode<4>(p, grid, lds, split, stream);
         if (e != hipSuccess) return e;
         if (S == 1)
             hipLaunchKernelGGL(merge_kernel<1>, dim3(m), dim3(256), 0, stream, cand_s, cand_i,
