@@ -179,11 +179,25 @@ tq_status tq_search(const tq_index *idx, const float *Q_dev, int64_t nq,
                     int32_t k, const uint64_t *allow_dev, int64_t *ids_dev,
                     float *scores_dev, void *stream);
 
-/* Scan path selection for tq_search_ex. */
+/* Scan path selection for tq_search_ex (section II-B step 5; the batched
+ * path is this library's, not the paper's).
+ *  TQ_PATH_AUTO  the single-query scan.
+ *  TQ_PATH_LUT   one pass over the code store per query, with the query's
+ *                lookup table in LDS.
+ *  TQ_PATH_MFMA  one pass per tile of 32 queries: approximate float16 scores
+ *                on the matrix cores select 64 candidates per query, which
+ *                are rescored exactly (the same scores as TQ_PATH_LUT).  A
+ *                per-query certificate -- a rigorous bound on the
+ *                approximation error -- proves that the exact top k lies
+ *                among the candidates; queries without one are re-run on the
+ *                LUT path (see tq_last_search_fallbacks).  Needs 4-bit codes,
+ *                d % 256 == 0, k <= 64 and n_tenants <= 4096, else
+ *                TQ_EUNSUPPORTED.  Synchronises `stream` once per call, to
+ *                read the certificates on the host. */
 typedef enum {
-    TQ_PATH_AUTO = 0,     /* library choice */
-    TQ_PATH_LUT = 1,      /* one pass per query: LDS lookup tables */
-    TQ_PATH_MFMA = 2      /* query tiles on the matrix cores + exact rescoring */
+    TQ_PATH_AUTO = 0,
+    TQ_PATH_LUT = 1,
+    TQ_PATH_MFMA = 2
 } tq_path;
 
 /* Flag ORed into `path`: Q_dev already holds rotated queries R q (for
@@ -195,12 +209,17 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k,
                                    int32_t path, size_t *bytes_out);
 
 /* tq_search with an explicit path and a caller-provided device workspace of
- * at least tq_search_workspace_size() bytes (256-byte aligned).  Allocates
- * nothing.  Calls sharing one workspace must not overlap in time. */
+ * at least tq_search_workspace_size() bytes (256-byte aligned).  Allocates no
+ * device memory.  Calls sharing one workspace must not overlap in time. */
 tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq,
                        int32_t k, const uint64_t *allow_dev, int32_t path,
                        void *workspace_dev, size_t workspace_bytes,
                        int64_t *ids_dev, float *scores_dev, void *stream);
+
+/* Number of queries of the calling thread's last tq_search_ex call that the
+ * TQ_PATH_MFMA path re-ran on the LUT path because their certificate failed
+ * (0 after any other path). */
+int32_t tq_last_search_fallbacks(void);
 
 #ifdef __cplusplus
 }

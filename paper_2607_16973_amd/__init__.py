@@ -18,11 +18,17 @@ import numpy as np
 from ._lib import FLAG_PREROTATED, PATHS, TQError, check, lib
 
 __all__ = ["Codebook", "Rotation", "Index", "TQError", "rotate_quantize",
-           "rotate_queries", "version"]
+           "rotate_queries", "version", "last_search_fallbacks"]
 
 
 def version() -> str:
     return lib.tq_version().decode()
+
+
+def last_search_fallbacks() -> int:
+    """Queries of this thread's last search that the matrix-core path re-ran
+    on the single-query scan (their top-k certificate failed)."""
+    return int(lib.tq_last_search_fallbacks())
 
 
 def _torch():

@@ -28,7 +28,7 @@ class TQError(RuntimeError):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libtq.so is not built (run `python -m paper_2607_16973_amd.build`); "
+        raise ImportError("libtq.so is not built (run `python paper_2607_16973_amd/build.py`); "
                           "there is no fallback implementation")
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64, U64, SZ = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
@@ -56,6 +56,7 @@ def _load():
         "tq_search": ([P, P, I64, I32, P, P, P, P], ctypes.c_int),
         "tq_search_workspace_size": ([P, I64, I32, I32, P], ctypes.c_int),
         "tq_search_ex": ([P, P, I64, I32, P, I32, P, SZ, P, P, P], ctypes.c_int),
+        "tq_last_search_fallbacks": ([], ctypes.c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -70,7 +71,7 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_rotation_free", "tq_rotate_quantize", "tq_rotate_queries", "tq_index_create",
             "tq_index_reserve", "tq_index_add", "tq_index_add_codes", "tq_index_size",
             "tq_index_export", "tq_index_free", "tq_search", "tq_search_workspace_size",
-            "tq_search_ex")
+            "tq_search_ex", "tq_last_search_fallbacks")
 
 
 def check(status: int) -> None:

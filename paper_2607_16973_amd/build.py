@@ -1,6 +1,6 @@
 """Build libtq.so (HIP for gfx950) in-tree.
 
-    python -m paper_2607_16973_amd.build
+    python paper_2607_16973_amd/build.py
 
 Device code is compiled for gfx950 only, with packed-float32 instruction
 selection disabled.  The two host-only solvers (codebook, rotation) are
@@ -21,14 +21,16 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtq.so")
 
-HIP_SOURCES = ["encode.hip", "scan.hip", "layout.hip", "api.cpp"]
+HIP_SOURCES = ["encode.hip", "scan.hip", "batch.hip", "layout.hip", "api.cpp"]
 # Per-source extra flags.  The scan's prefetch ring must stay where it is
 # written: machine sinking would move every refill into the loop latch and
 # serialise the loads with the table lookups.  The atomic optimizer would
 # turn the one-lane work-claim atomics into wave-wide ones whose result is
 # read at once, stalling on the LDS round trip the scan hides.
 EXTRA_FLAGS = {"scan.hip": ["-mllvm", "-disable-machine-sink",
-                            "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+                            "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+               "batch.hip": ["-mllvm", "-disable-machine-sink",
+                             "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
 HOST_SOURCES = ["codebook.cpp", "rotation.cpp"]
 
 

@@ -15,6 +15,9 @@ namespace tq {
 
 namespace {
 thread_local std::string g_err;
+// queries of the calling thread's last search that the matrix-core path
+// handed to the single-query scan
+thread_local int g_last_fallbacks = 0;
 
 bool valid_bits(int b) { return b == 1 || b == 2 || b == 3 || b == 4 || b == 8; }
 
@@ -134,6 +137,10 @@ namespace {
 
 size_t block_bytes(const tq_index *x) { return (size_t)x->chunks * 1024; }
 
+// The device status buffer (256 bytes) holds the status word at byte 0 and
+// the largest scale in the store, a float, at byte 64.
+float *scale_max_dev(const tq_index *x) { return reinterpret_cast<float *>(x->status) + 16; }
+
 void index_release(tq_index *x) {
     if (x->codes) (void)hipFree(x->codes);
     if (x->scales) (void)hipFree(x->scales);
@@ -238,6 +245,8 @@ extern "C" {
 const char *tq_last_error(void) { return g_err.c_str(); }
 
 const char *tq_version(void) { return "tq 0.1.0 gfx950"; }
+
+int32_t tq_last_search_fallbacks(void) { return g_last_fallbacks; }
 
 tq_status tq_build_codebook(int32_t d, int32_t bits, tq_codebook **out) {
     if (!out) return fail(TQ_EINVAL, "out is NULL");
@@ -384,6 +393,8 @@ static tq_status finish_add(tq_index *x, const uint16_t *tenants_dev, int64_t n,
     if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
     e = add_tenants(tenants_dev, n, x->n, x->T, x->W, x->tenants, x->summ, x->status, s);
     if (e != hipSuccess) return hip_fail(e, "add_tenants");
+    e = update_scale_max(x->scales + x->n, n, scale_max_dev(x), s);
+    if (e != hipSuccess) return hip_fail(e, "scale maximum");
     int h = 0;
     tq_status st = read_status(x->status, s, &h);
     if (st != TQ_OK) return st;
@@ -489,6 +500,21 @@ static int scan_grid() {
     return cus > 0 ? cus : 256;
 }
 
+static bool use_mfma(const ScanShape &sh, int k, int base) {
+    return base == TQ_PATH_MFMA && mfma_search_supported(sh, k);
+}
+
+static size_t search_bytes(const ScanShape &sh, int64_t nq, int k, int base) {
+    return use_mfma(sh, k, base) ? mfma_search_workspace_bytes(sh, nq, k, scan_grid())
+                                 : lut_search_workspace_bytes(sh, nq, k, scan_grid());
+}
+
+static float centroid_max(const tq_index *x) {
+    float m = 0.f;
+    for (int i = 0; i < (1 << x->bits); ++i) m = std::max(m, std::fabs(x->cbdev.cents32[i]));
+    return m;
+}
+
 tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, int32_t path,
                                    size_t *bytes_out) {
     if (!idx || !bytes_out) return fail(TQ_EINVAL, "NULL argument");
@@ -497,9 +523,12 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
     const int base = path & ~TQ_FLAG_PREROTATED;
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
+    if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, k <= 64 "
+                                     "and at most 4096 tenants");
     tq_status st = device_ready();
     if (st != TQ_OK) return st;
-    *bytes_out = lut_search_workspace_bytes(shape_of(idx), nq, k, scan_grid());
+    *bytes_out = search_bytes(shape_of(idx), nq, k, base);
     return TQ_OK;
 }
 
@@ -521,8 +550,11 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     tq_status st = device_ready();
     if (st != TQ_OK) return st;
     const ScanShape sh = shape_of(idx);
+    if (base == TQ_PATH_MFMA && !mfma_search_supported(sh, k))
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, k <= 64 "
+                                     "and at most 4096 tenants");
     const int grid = scan_grid();
-    const size_t need = lut_search_workspace_bytes(sh, nq, k, grid);
+    const size_t need = search_bytes(sh, nq, k, base);
     if (workspace_bytes < need)
         return fail(TQ_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -547,9 +579,20 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
         if (e != hipSuccess) return hip_fail(e, "query rotation");
         Qrot = qr;
     }
+    if (use_mfma(sh, k, base)) {
+        int n_fallback = 0;
+        hipError_t e = mfma_search(sh, idx->codes, idx->scales, scale_max_dev(idx), idx->tenants,
+                                   idx->summ, idx->cents_dev, centroid_max(idx), Qrot, nq, k,
+                                   allow_dev, grid, workspace_dev, ids_dev, scores_dev,
+                                   &n_fallback, s);
+        if (e != hipSuccess) return hip_fail(e, "matrix-core search");
+        g_last_fallbacks = n_fallback;
+        return TQ_OK;
+    }
     hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev, Qrot, nq, k,
                    allow_dev, grid, workspace_dev, workspace_bytes, ids_dev, scores_dev, s);
     if (e != hipSuccess) return hip_fail(e, "scan");
+    g_last_fallbacks = 0;
     return TQ_OK;
 }
 

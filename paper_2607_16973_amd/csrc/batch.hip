@@ -1,0 +1,679 @@
+// Batched search on the matrix cores (section II-B step 5 for a tile of
+// queries at once, with the filter of section III-B).
+//
+// Per tile of up to 32 queries:
+//  1. prep_kernel: q' scaled by a power of two and rounded to float16, with
+//     the per-query constants below.
+//  2. mfma_scores_kernel: one pass over the code store.  Each 16-byte chunk
+//     of 64 vectors (32 coordinates each) is turned into float16 centroid
+//     values and multiplied with the query tile on v_mfma_f32_16x16x32_f16;
+//     after a block's last chunk the approximate scores s_v <c_hat, q'> are
+//     written, scaled to a float16 range, as a [query][vector] matrix.
+//  3. select_kernel + select_merge_kernel: the 64 best approximate scores of
+//     every query (allowed vectors only).
+//  4. rescore_kernel: the exact score of each of the 64 candidates with the
+//     single-query scan's integer table (bit-identical scores), the top k of
+//     them, and a certificate: with E a rigorous bound on |approximate -
+//     exact| for every vector, a vector outside the 64 scores at most
+//     (64th approximate) + E; if that is below the k-th exact score the top
+//     k is proven, otherwise the query is flagged and the caller re-runs it
+//     on the single-query scan.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+#include <vector>
+
+#include "kernels.h"
+#include "lut.h"
+#include "topk.h"
+
+namespace tq {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
+constexpr int kCand = 64;          // candidates per query kept for exact rescoring
+constexpr int MF_THREADS = 512;    // 8 waves: two per SIMD, 256 registers each
+constexpr int MF_WAVES = MF_THREADS / 64;
+constexpr int SEL_THREADS = 256;
+constexpr int SEL_GROUPS = 32;     // select workgroups per query
+constexpr int kKeepVmemB = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
+
+// Per-query constants written by prep_kernel.
+struct QInfo {
+    float f;      // stored approximate score = s_v * acc * f (acc: MFMA sum of the scaled query)
+    float norm;   // approximate score = stored * norm  (s_max ||q'||_2)
+    float err;    // E: bound on |approximate - exact| for every vector
+    float pad;
+};
+
+// ------------------------------------------------------------------- prep
+// The query is scaled by alpha = 2^e with max|alpha q'_j| in [2^14, 2^15),
+// then rounded to float16 (relative error 2^-11, or 2^-25 absolute below
+// the normal range).  Error bound of the approximate score of vector v
+// against the exact one (both times s_v <= s_max), with u = 2^-11,
+// cmax = max|c|, q1 = ||q'||_1, and float32 accumulation of the d products
+// in any order (gamma_d = d 2^-24 / (1 - d 2^-24)):
+//   float16 centroids and query, products exact in float32:
+//       cmax q1 (2u + u^2) + cmax d 2^-25 (1 + u) / alpha
+//   accumulation:  gamma_d (1 + u)^2 cmax q1 + gamma_d cmax d 2^-25 / alpha
+//   scaling by s_v and f (two float32 roundings): 2^-22 cmax q1
+//   float16 storage of approx / norm: u |approx| + 2^-25 norm
+//   the exact score itself (integer table, float conversion): 7e-7 cmax q1
+// Their sum, times s_max, times 1.25 for margin, is E.
+__global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const float *smax_p,
+                            float cmax, _Float16 *__restrict__ q16, QInfo *__restrict__ info) {
+    __shared__ float red_m[SEL_THREADS / 64];
+    __shared__ double red_1[SEL_THREADS / 64], red_2[SEL_THREADS / 64];
+    const int q = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float *row = Q + (int64_t)q * d;
+    float m = 0.f;
+    double s1 = 0.0, s2 = 0.0;
+    for (int j = tid; j < d; j += SEL_THREADS) {
+        const float v = row[j];
+        m = fmaxf(m, fabsf(v));
+        s1 += fabs((double)v);
+        s2 += (double)v * v;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        m = fmaxf(m, __shfl_xor(m, o, 64));
+        s1 += __shfl_xor(s1, o, 64);
+        s2 += __shfl_xor(s2, o, 64);
+    }
+    if (lane == 0) {
+        red_m[wave] = m;
+        red_1[wave] = s1;
+        red_2[wave] = s2;
+    }
+    __syncthreads();
+    m = 0.f;
+    s1 = 0.0;
+    s2 = 0.0;
+    for (int w = 0; w < SEL_THREADS / 64; ++w) {
+        m = fmaxf(m, red_m[w]);
+        s1 += red_1[w];
+        s2 += red_2[w];
+    }
+    const int e = m > 0.f ? 14 - ilogbf(m) : 0;
+    const float alpha = ldexpf(1.0f, e);
+    for (int j = tid; j < d; j += SEL_THREADS) q16[(int64_t)q * d + j] = (_Float16)(row[j] * alpha);
+    if (tid == 0) {
+        const double smax = (double)*smax_p;
+        double norm = smax * sqrt(s2);
+        if (!(norm > 0.0)) norm = 1.0;
+        const double u = ldexp(1.0, -11);
+        const double t = ldexp(1.0, -25);
+        const double gd = d * ldexp(1.0, -24) / (1.0 - d * ldexp(1.0, -24));
+        const double cq = (double)cmax * s1;
+        const double sub = (double)cmax * d * t / alpha;
+        double E = cq * (2 * u + u * u) + sub * (1 + u) + gd * (1 + u) * (1 + u) * cq + gd * sub +
+                   ldexp(1.0, -22) * cq + u * cq * (1 + 4 * u) + 7e-7 * cq;
+        E = smax * E + t * norm;
+        QInfo qi;
+        qi.f = (float)(1.0 / ((double)alpha * norm));
+        qi.norm = (float)norm;
+        qi.err = (float)(1.25 * E);
+        qi.pad = 0.f;
+        info[q] = qi;
+    }
+}
+
+// ------------------------------------------------------------ MFMA scores
+struct ScoreParams {
+    const uint4 *codes;        // blocked store (b = 4)
+    const float *scales;
+    const _Float16 *q16;       // [nqt][d]
+    const QInfo *info;         // [nqt]
+    const float *cents;        // 16 levels
+    _Float16 *out;             // [kTile][npad] approximate scores / norm
+    int64_t n, nblk, npad;
+    int d, chunks, nqt;
+};
+
+// Float16 centroid of every 4-bit field of a stored word w (the canonical
+// word rotated left by 2): element t is coordinate t of the word.  T holds
+// the 16 centroids at a 4-byte stride.
+__device__ inline half8 dequant8(const char *__restrict__ T, uint32_t w) {
+    uint32_t lo = w & 0x3C3C3C3Cu;                                  // byte b: field 2b   times 4
+    uint32_t hi = __builtin_amdgcn_alignbit(w, w, 4) & 0x3C3C3C3Cu; // byte b: field 2b+1 times 4
+    asm volatile("" : "+v"(lo), "+v"(hi));
+    half8 r;
+    r[0] = *reinterpret_cast<const _Float16 *>(T + (lo & 0xFFu));
+    r[1] = *reinterpret_cast<const _Float16 *>(T + (hi & 0xFFu));
+    r[2] = *reinterpret_cast<const _Float16 *>(T + ((lo >> 8) & 0xFFu));
+    r[3] = *reinterpret_cast<const _Float16 *>(T + ((hi >> 8) & 0xFFu));
+    r[4] = *reinterpret_cast<const _Float16 *>(T + ((lo >> 16) & 0xFFu));
+    r[5] = *reinterpret_cast<const _Float16 *>(T + ((hi >> 16) & 0xFFu));
+    r[6] = *reinterpret_cast<const _Float16 *>(T + (lo >> 24));
+    r[7] = *reinterpret_cast<const _Float16 *>(T + (hi >> 24));
+    return r;
+}
+
+// One workgroup of 8 waves per compute unit.  The query tile (32 rows of d
+// float16, rows padded by 16 bytes so the 16 rows read by one instruction
+// fall in distinct banks) stays in LDS.  Waves claim the workgroup's
+// 64-vector blocks one at a time from an LDS counter (one ahead, so the ring
+// of 8 chunk loads runs on into the next block).  For a chunk, lane 16q+i
+// has loaded the 4 words of vector 16q+i; two rounds of lane-quarter swaps
+// give it word q of vectors i, 16+i, 32+i, 48+i -- the B operand (k = 8q..8q+7,
+// column i) of the four 16-vector MFMAs.
+__global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int ld = p.d + 8;                                   // row stride in halves
+    _Float16 *Qs = reinterpret_cast<_Float16 *>(smem);       // [kTile][ld]
+    char *T = smem + (size_t)kTile * ld * 2;                 // 16 x 4 bytes
+    int *ctr = reinterpret_cast<int *>(T + 64);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int G = gridDim.x, g = blockIdx.x;
+    const int CH = p.chunks;   // multiple of 8
+    const int64_t gb0 = p.nblk * g / G, gb1 = p.nblk * (g + 1) / G;
+    const int nbw = (int)(gb1 - gb0);
+
+    // query tile, zero rows past nqt
+    for (int e = tid; e < kTile * (p.d / 8); e += MF_THREADS) {
+        const int r = e / (p.d / 8), c8 = e - r * (p.d / 8);
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (r < p.nqt) v = reinterpret_cast<const uint4 *>(p.q16 + (int64_t)r * p.d)[c8];
+        *reinterpret_cast<uint4 *>(Qs + r * ld + c8 * 8) = v;
+    }
+    if (tid < 16) {
+        const _Float16 c = (_Float16)p.cents[tid];
+        uint32_t bits = (uint32_t)__builtin_bit_cast(uint16_t, c);
+        reinterpret_cast<uint32_t *>(T)[tid] = bits;
+    }
+    if (tid == 0) *ctr = 0;
+    // per-lane query factors: tile t, rows 4*(lane/16) + r
+    float qf[2][4];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int q = 16 * t + 4 * (lane >> 4) + r;
+            qf[t][r] = q < p.nqt ? p.info[q].f : 0.f;
+        }
+    __syncthreads();
+
+    auto take = [&]() {
+        int v = 0;
+        if (lane == 0) v = atomicAdd(ctr, 1);
+        return v;
+    };
+    int cur = __builtin_amdgcn_readfirstlane(take());
+    if (cur >= nbw) return;
+    int nxt = __builtin_amdgcn_readfirstlane(take());
+    const uint4 *bsrc = p.codes + (gb0 + cur) * CH * 64;
+    uint4 buf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        buf[i] = (bsrc + i * 64)[lane];
+        __builtin_amdgcn_sched_barrier(kKeepVmemB);
+    }
+    const int qrow = lane & 15, kq = lane >> 4;
+    const _Float16 *qa0 = Qs + qrow * ld + kq * 8;
+    const _Float16 *qa1 = Qs + (16 + qrow) * ld + kq * 8;
+    while (true) {
+        const int64_t blk = gb0 + cur;
+        // the block after this one (or this one again past the end: cache hits)
+        const uint4 *nsrc = nxt < nbw ? p.codes + (gb0 + nxt) * CH * 64 : bsrc;
+        const int ticket = take();
+        float scl[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int64_t v = blk * 64 + 16 * m + qrow;
+            scl[m] = v < p.n ? p.scales[v] : 0.f;
+        }
+        float4v acc[2][4];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int m = 0; m < 4; ++m) acc[t][m] = float4v{0.f, 0.f, 0.f, 0.f};
+        for (int c0 = 0; c0 < CH; c0 += 8) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int c = c0 + i;
+                uint32_t r[4] = {buf[i].x, buf[i].y, buf[i].z, buf[i].w};
+                // refill 8 chunks ahead: this block, then the next one
+                const int nc = c + 8;
+                buf[i] = (nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64)[lane];
+                __builtin_amdgcn_sched_barrier(kKeepVmemB);
+                const auto s02 = __builtin_amdgcn_permlane32_swap(r[0], r[2], false, false);
+                const auto s13 = __builtin_amdgcn_permlane32_swap(r[1], r[3], false, false);
+                r[0] = s02[0];
+                r[2] = s02[1];
+                r[1] = s13[0];
+                r[3] = s13[1];
+                const auto s01 = __builtin_amdgcn_permlane16_swap(r[0], r[1], false, false);
+                const auto s23 = __builtin_amdgcn_permlane16_swap(r[2], r[3], false, false);
+                r[0] = s01[0];
+                r[1] = s01[1];
+                r[2] = s23[0];
+                r[3] = s23[1];
+                const half8 a0 = *reinterpret_cast<const half8 *>(qa0 + c * 32);
+                const half8 a1 = *reinterpret_cast<const half8 *>(qa1 + c * 32);
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const half8 b = dequant8(T, r[m]);
+                    acc[0][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, b, acc[0][m], 0, 0, 0);
+                    acc[1][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, b, acc[1][m], 0, 0, 0);
+                }
+            }
+        }
+        // lane holds vectors 16m + qrow, queries 16t + 4*kq + r
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int64_t v = blk * 64 + 16 * m + qrow;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int q = 16 * t + 4 * kq + r;
+                    if (q < p.nqt)
+                        p.out[(int64_t)q * p.npad + v] = (_Float16)(acc[t][m][r] * scl[m] * qf[t][r]);
+                }
+        }
+        if (nxt >= nbw) break;
+        cur = nxt;
+        nxt = __builtin_amdgcn_readfirstlane(ticket);
+        bsrc = nsrc;
+    }
+}
+
+// -------------------------------------------------------------- selection
+struct SelectParams {
+    const _Float16 *approx;    // [nqt][npad]
+    const uint16_t *tenants;
+    const uint64_t *allow;     // [nqt][W] or null
+    float *cand_s;             // [nqt][SEL_GROUPS][kCand]
+    int *cand_i;
+    int *gbound;               // [nqt] order keys
+    int64_t n, npad;
+    int W;
+};
+
+// The kCand best allowed approximate scores of one query over 1/SEL_GROUPS
+// of the vectors; each lane reads 8 consecutive scores per load.
+__global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
+    __shared__ float st_s[4 * 64];
+    __shared__ int st_i[4 * 64];
+    __shared__ int wg_key;
+    __shared__ uint64_t allow_s[64];
+    const int g = blockIdx.x, q = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool filtered = p.allow != nullptr;
+    if (tid == 0) wg_key = fkey(-INFINITY);
+    if (filtered)
+        for (int w = tid; w < p.W && w < 64; w += SEL_THREADS) allow_s[w] = p.allow[(int64_t)q * p.W + w];
+    __syncthreads();
+    // ranges of 512 vectors (one load per lane per wave)
+    const int64_t units = p.npad / 512;
+    const int64_t u0 = units * g / SEL_GROUPS, u1 = units * (g + 1) / SEL_GROUPS;
+    WaveTopK<1> top;
+    top.reset();
+    const uint4 *row = reinterpret_cast<const uint4 *>(p.approx + (int64_t)q * p.npad);
+    for (int64_t u = u0 + wave; u < u1; u += 4) {
+        const uint4 w = row[u * 64 + lane];
+        const int gk = __hip_atomic_load(p.gbound + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const _Float16 *h = reinterpret_cast<const _Float16 *>(&w);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int64_t v = u * 512 + lane * 8 + e;
+            bool ok = v < p.n;
+            if (ok && filtered) {
+                const int t = p.tenants[v];
+                ok = (t >> 6) < p.W && ((allow_s[t >> 6] >> (t & 63)) & 1ull);
+            }
+            top.offer_seen(ok ? (float)h[e] : -INFINITY, ok ? (int)v : INT_MAX, lane, kCand,
+                           &wg_key, p.gbound + q, gk);
+        }
+    }
+    // merge the 4 wave lists
+    st_s[wave * 64 + lane] = top.ls[0];
+    st_i[wave * 64 + lane] = top.li[0];
+    __syncthreads();
+    if (wave == 0) {
+        for (int w = 1; w < 4; ++w) {
+            float os[1] = {st_s[w * 64 + lane]};
+            int oi[1] = {st_i[w * 64 + lane]};
+            merge_lists<1>(top.ls, top.li, os, oi, lane);
+        }
+        const int64_t base = ((int64_t)q * SEL_GROUPS + g) * kCand;
+        p.cand_s[base + lane] = top.ls[0];
+        p.cand_i[base + lane] = top.li[0];
+    }
+}
+
+// The kCand best of the SEL_GROUPS lists of each query, sorted.
+__global__ __launch_bounds__(256) void select_merge_kernel(const float *__restrict__ cs,
+                                                           const int *__restrict__ ci,
+                                                           float *__restrict__ top_s,
+                                                           int *__restrict__ top_i) {
+    __shared__ float st_s[4 * 64];
+    __shared__ int st_i[4 * 64];
+    const int q = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    float ls[1] = {-INFINITY};
+    int li[1] = {INT_MAX};
+    for (int g = wave; g < SEL_GROUPS; g += 4) {
+        const int64_t base = ((int64_t)q * SEL_GROUPS + g) * kCand;
+        float os[1] = {cs[base + lane]};
+        int oi[1] = {ci[base + lane]};
+        merge_lists<1>(ls, li, os, oi, lane);
+    }
+    st_s[wave * 64 + lane] = ls[0];
+    st_i[wave * 64 + lane] = li[0];
+    __syncthreads();
+    if (wave == 0) {
+        for (int w = 1; w < 4; ++w) {
+            float os[1] = {st_s[w * 64 + lane]};
+            int oi[1] = {st_i[w * 64 + lane]};
+            merge_lists<1>(ls, li, os, oi, lane);
+        }
+        top_s[(int64_t)q * kCand + lane] = ls[0];
+        top_i[(int64_t)q * kCand + lane] = li[0];
+    }
+}
+
+// ------------------------------------------------------- exact rescoring
+struct RescoreParams {
+    const uint4 *codes;
+    const float *scales;
+    const float *qrot;         // [nqt][d] float32 rotated queries
+    const float *cents;
+    const QInfo *info;
+    const float *top_s;        // [nqt][kCand] approximate, sorted
+    const int *top_i;
+    int64_t *ids;              // [nqt][k]
+    float *scores;
+    int *flags;                // [nqt]: 1 = not certified
+    int d, bits, chunks, lut_words, k;
+};
+
+__global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p) {
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    float *red = lds + p.lut_words;         // 16
+    float *ex_s = red + 16;                 // kCand exact scores
+    int *ex_i = reinterpret_cast<int *>(ex_s + kCand);
+    const int q = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const TableShape ts{p.d, p.bits, p.lut_words};
+    float qv[2][4];
+    load_nibble_query(ts, p.qrot + (int64_t)q * p.d, qv);
+    nibble_abs_sum(red, qv);
+    __syncthreads();
+    const int sh = build_nibble_table(lds, red, p.cents, ts, qv);
+    __syncthreads();
+    const char *lut = reinterpret_cast<const char *>(lds);
+    for (int j = wave; j < kCand; j += kTableWaves) {
+        const int v = p.top_i[(int64_t)q * kCand + j];
+        int part = 0;
+        const bool valid = v != INT_MAX;
+        if (valid && lane < p.chunks) {
+            const uint4 w = p.codes[((int64_t)(v >> 6) * p.chunks + lane) * 64 + (v & 63)];
+            part = nib_chunk(lut + lane * 2048, w);
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+        if (lane == 0) {
+            ex_s[j] = valid ? ldexpf((float)part * p.scales[v], -sh) : -INFINITY;
+            ex_i[j] = valid ? v : INT_MAX;
+        }
+    }
+    __syncthreads();
+    if (wave == 0) {
+        float s = ex_s[lane];
+        int i = ex_i[lane];
+        wave_sort64(s, i, lane);
+        if (lane < p.k) {
+            const bool empty = !(s > -INFINITY);
+            p.ids[(int64_t)q * p.k + lane] = empty ? -1 : (int64_t)i;
+            p.scores[(int64_t)q * p.k + lane] = empty ? -INFINITY : s;
+        }
+        // certificate
+        const int nvalid = __popcll(__ballot(p.top_i[(int64_t)q * kCand + lane] != INT_MAX));
+        const float ek = __shfl(s, p.k - 1, 64);
+        const float amin = p.top_s[(int64_t)q * kCand + kCand - 1];
+        const QInfo qi = p.info[q];
+        const bool cert = nvalid < kCand || (double)amin * qi.norm + (double)qi.err < (double)ek;
+        if (lane == 0) p.flags[q] = cert ? 0 : 1;
+    }
+}
+
+// ------------------------------------------------------ fallback helpers
+__global__ void fill_order_keys(int *p, int n) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = fkey(-INFINITY);
+}
+
+__global__ void gather_allow(const uint64_t *__restrict__ src, const int *__restrict__ rows, int nr,
+                             int W, uint64_t *__restrict__ dst) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < (int64_t)nr * W;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(e / W);
+        dst[e] = src[(int64_t)rows[r] * W + (e - (int64_t)r * W)];
+    }
+}
+
+__global__ void gather_rows(const float *__restrict__ src, const int *__restrict__ rows, int nr,
+                            int d, float *__restrict__ dst) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < (int64_t)nr * d;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(e / d);
+        dst[e] = src[(int64_t)rows[r] * d + (e - (int64_t)r * d)];
+    }
+}
+
+__global__ void scatter_results(const int64_t *__restrict__ ci, const float *__restrict__ cs,
+                                const int *__restrict__ rows, int nr, int k,
+                                int64_t *__restrict__ ids, float *__restrict__ scores) {
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < (int64_t)nr * k;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(e / k);
+        const int64_t dst = (int64_t)rows[r] * k + (e - (int64_t)r * k);
+        ids[dst] = ci[e];
+        scores[dst] = cs[e];
+    }
+}
+
+__global__ void scale_max_kernel(const float *__restrict__ s, int64_t n, int *smax_bits) {
+    int m = 0;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int b = __float_as_int(s[i]);   // scales are >= 0: bit order is value order
+        m = b > m ? b : m;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const int x = __shfl_xor(m, o, 64);
+        m = x > m ? x : m;
+    }
+    if ((threadIdx.x & 63) == 0) atomicMax(smax_bits, m);
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+struct BatchLayout {
+    size_t q16, info, approx, cand_s, cand_i, top_s, top_i, gbound, flags, rows, qc, allow_c, ids_c,
+        scores_c, lut, total;
+};
+
+// Row length of the approximate-score matrix: whole 512-vector select units.
+int64_t approx_row(const ScanShape &s) { return (s.nblk * 64 + 511) / 512 * 512; }
+
+BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
+    BatchLayout L{};
+    size_t o = align256((size_t)nq * s.d * sizeof(float));   // rotated queries
+    const int64_t npad = approx_row(s);
+    L.q16 = o;
+    o += align256((size_t)kTile * s.d * 2);
+    L.info = o;
+    o += align256(kTile * sizeof(QInfo));
+    L.approx = o;
+    o += align256((size_t)kTile * npad * 2);
+    L.cand_s = o;
+    o += align256((size_t)kTile * SEL_GROUPS * kCand * 4);
+    L.cand_i = o;
+    o += align256((size_t)kTile * SEL_GROUPS * kCand * 4);
+    L.top_s = o;
+    o += align256((size_t)kTile * kCand * 4);
+    L.top_i = o;
+    o += align256((size_t)kTile * kCand * 4);
+    L.gbound = o;
+    o += align256(kTile * 4);
+    L.flags = o;
+    o += align256((size_t)nq * 4);
+    L.rows = o;
+    o += align256((size_t)nq * 4);
+    L.qc = o;
+    o += align256((size_t)nq * s.d * sizeof(float));
+    L.allow_c = o;
+    o += align256((size_t)nq * s.W * sizeof(uint64_t));
+    L.ids_c = o;
+    o += align256((size_t)nq * k * 8);
+    L.scores_c = o;
+    o += align256((size_t)nq * k * 4);
+    L.lut = o;
+    o += lut_search_workspace_bytes(s, nq, k, grid);
+    L.total = o + 256;
+    return L;
+}
+
+}  // namespace
+
+bool mfma_search_supported(const ScanShape &s, int k) {
+    return s.bits == 4 && s.chunks % 8 == 0 && k <= kCand && s.W <= 64;
+}
+
+size_t mfma_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid) {
+    return batch_layout(s, nq, k, grid).total;
+}
+
+hipError_t update_scale_max(const float *scales, int64_t n, float *smax, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    int64_t g = (n + 255) / 256;
+    if (g > 2048) g = 2048;
+    hipLaunchKernelGGL(scale_max_kernel, dim3((int)g), dim3(256), 0, stream, scales, n,
+                       reinterpret_cast<int *>(smax));
+    return hipGetLastError();
+}
+
+hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
+                       const float *smax, const uint16_t *tenants, const uint64_t *summaries,
+                       const float *cents32, float cmax, const float *Qrot, int64_t nq, int k,
+                       const uint64_t *allow, int grid, void *ws, int64_t *ids, float *scores,
+                       int *n_fallback, hipStream_t stream) {
+    const BatchLayout L = batch_layout(s, nq, k, grid);
+    uint8_t *w8 = static_cast<uint8_t *>(ws);
+    _Float16 *q16 = reinterpret_cast<_Float16 *>(w8 + L.q16);
+    QInfo *info = reinterpret_cast<QInfo *>(w8 + L.info);
+    _Float16 *approx = reinterpret_cast<_Float16 *>(w8 + L.approx);
+    float *cand_s = reinterpret_cast<float *>(w8 + L.cand_s);
+    int *cand_i = reinterpret_cast<int *>(w8 + L.cand_i);
+    float *top_s = reinterpret_cast<float *>(w8 + L.top_s);
+    int *top_i = reinterpret_cast<int *>(w8 + L.top_i);
+    int *gbound = reinterpret_cast<int *>(w8 + L.gbound);
+    int *flags = reinterpret_cast<int *>(w8 + L.flags);
+    const int64_t npad = approx_row(s);
+    const size_t lds_scores = (size_t)kTile * (s.d + 8) * 2 + 64 + 16;
+    const size_t lds_rescore = (size_t)s.chunks * 2048 + (16 + 2 * kCand) * 4;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)mfma_scores_kernel,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)rescore_kernel,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    for (int64_t q0 = 0; q0 < nq; q0 += kTile) {
+        const int nqt = (int)((nq - q0) < kTile ? (nq - q0) : kTile);
+        hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream, Qrot + q0 * s.d,
+                           nqt, s.d, smax, cmax, q16, info);
+        ScoreParams sp{};
+        sp.codes = reinterpret_cast<const uint4 *>(blocked);
+        sp.scales = scales;
+        sp.q16 = q16;
+        sp.info = info;
+        sp.cents = cents32;
+        sp.out = approx;
+        sp.n = s.n;
+        sp.nblk = s.nblk;
+        sp.npad = npad;
+        sp.d = s.d;
+        sp.chunks = s.chunks;
+        sp.nqt = nqt;
+        hipLaunchKernelGGL(mfma_scores_kernel, dim3(grid), dim3(MF_THREADS), lds_scores, stream, sp);
+        hipLaunchKernelGGL(fill_order_keys, dim3(1), dim3(64), 0, stream, gbound, nqt);
+        SelectParams sl{};
+        sl.approx = approx;
+        sl.tenants = tenants;
+        sl.allow = allow ? allow + q0 * s.W : nullptr;
+        sl.cand_s = cand_s;
+        sl.cand_i = cand_i;
+        sl.gbound = gbound;
+        sl.n = s.n;
+        sl.npad = npad;
+        sl.W = s.W;
+        hipLaunchKernelGGL(select_kernel, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0, stream, sl);
+        hipLaunchKernelGGL(select_merge_kernel, dim3(nqt), dim3(256), 0, stream, cand_s, cand_i,
+                           top_s, top_i);
+        RescoreParams rp{};
+        rp.codes = reinterpret_cast<const uint4 *>(blocked);
+        rp.scales = scales;
+        rp.qrot = Qrot + q0 * s.d;
+        rp.cents = cents32;
+        rp.info = info;
+        rp.top_s = top_s;
+        rp.top_i = top_i;
+        rp.ids = ids + q0 * k;
+        rp.scores = scores + q0 * k;
+        rp.flags = flags + q0;
+        rp.d = s.d;
+        rp.bits = s.bits;
+        rp.chunks = s.chunks;
+        rp.lut_words = s.chunks * 512;
+        rp.k = k;
+        hipLaunchKernelGGL(rescore_kernel, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    // queries whose top k is not proven run on the single-query scan
+    std::vector<int> hf((size_t)nq);
+    hipError_t e = hipMemcpyAsync(hf.data(), flags, nq * sizeof(int), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return e;
+    std::vector<int> rows;
+    for (int64_t i = 0; i < nq; ++i)
+        if (hf[i]) rows.push_back((int)i);
+    *n_fallback = (int)rows.size();
+    if (rows.empty()) return hipSuccess;
+    const int nr = (int)rows.size();
+    int *rows_d = reinterpret_cast<int *>(w8 + L.rows);
+    float *qc = reinterpret_cast<float *>(w8 + L.qc);
+    int64_t *ids_c = reinterpret_cast<int64_t *>(w8 + L.ids_c);
+    float *scores_c = reinterpret_cast<float *>(w8 + L.scores_c);
+    e = hipMemcpyAsync(rows_d, rows.data(), nr * sizeof(int), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(gather_rows, dim3(256), dim3(256), 0, stream, Qrot, rows_d, nr, s.d, qc);
+    uint64_t *allow_c = nullptr;
+    if (allow) {
+        allow_c = reinterpret_cast<uint64_t *>(w8 + L.allow_c);
+        hipLaunchKernelGGL(gather_allow, dim3(64), dim3(256), 0, stream, allow, rows_d, nr, s.W,
+                           allow_c);
+    }
+    e = lut_search(s, blocked, scales, tenants, summaries, cents32, qc, nr, k, allow_c, grid,
+                   w8 + L.lut, lut_search_workspace_bytes(s, nq, k, grid), ids_c, scores_c, stream);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(scatter_results, dim3(256), dim3(256), 0, stream, ids_c, scores_c, rows_d, nr,
+                       k, ids, scores);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);   // host vectors above go out of scope
+    return e;
+}
+
+}  // namespace tq

@@ -85,6 +85,22 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
                       const uint64_t *allow, int grid, void *ws, size_t ws_bytes,
                       int64_t *ids, float *scores, hipStream_t stream);
 
+// Batched search of a tile of queries on the matrix cores with exact
+// rescoring (b = 4, chunks % 8 == 0, k <= 64, at most 4096 tenants).
+// Queries whose top k the certificate does not prove are re-run on the
+// single-query scan; their count goes to *n_fallback.  Synchronises
+// `stream` once to read the certificates.  `smax` is a device float: the
+// largest scale in the store.
+bool mfma_search_supported(const ScanShape &s, int k);
+size_t mfma_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid);
+hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
+                       const float *smax, const uint16_t *tenants, const uint64_t *summaries,
+                       const float *cents32, float cmax, const float *Qrot, int64_t nq, int k,
+                       const uint64_t *allow, int grid, void *ws, int64_t *ids, float *scores,
+                       int *n_fallback, hipStream_t stream);
+// *smax = max(*smax, max of scales[0..n)); scales are >= 0.
+hipError_t update_scale_max(const float *scales, int64_t n, float *smax, hipStream_t stream);
+
 int device_cu_count();
 
 }  // namespace tq

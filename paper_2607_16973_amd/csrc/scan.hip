@@ -25,12 +25,13 @@
 #include <cstdint>
 
 #include "kernels.h"
+#include "lut.h"
 #include "topk.h"
 
 namespace tq {
 namespace {
 
-constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_THREADS = kTableThreads;
 constexpr int SCAN_WAVES = SCAN_THREADS / 64;
 // Scheduling-barrier mask: ALU, SALU, MFMA, LDS and transcendental
 // instructions may move across, memory loads and stores to HBM may not.
@@ -54,36 +55,14 @@ struct ScanParams {
     int lut_words;              // 32-bit words of LDS used by the table
 };
 
+__device__ inline TableShape table_shape(const ScanParams &p) {
+    return TableShape{p.d, p.bits, p.lut_words};
+}
+
 // ---------------------------------------------------------------- tables
-// b in {1,2,4}: one row of 16 int32 entries per 4-bit field of the code
-// stream (row r covers coordinates r*g .. r*g+g-1, g = 4/b), holding
-// round(2^sh * sum_t c[code_t] q'_j) -- fixed point with a per-query power of
-// two 2^sh chosen so that every possible sum of one entry per row fits in
-// int32: sum_r max_c |entry| <= 2^sh max|c| sum_j |q'_j| + rows/2 < 2^31.
-// The integer sums are then exact; the only error is the rounding of each
-// entry, at most rows * 2^-(sh+1) in total.
+// b in {1,2,4}: int32 fixed-point rows of 16 entries (lut.h).
 // b = 3: float32 rows of 8 entries c[code] q'_j per coordinate.
 // b = 8: the 256 float32 centroids followed by q' (multiplied on the fly).
-
-// Sum of 8 int32 table hits addressed by the 8 4-bit fields of a stored
-// word w (the canonical word rotated left by 2 bits); row t of the 8 rows
-// starting at Lb (64 bytes per row) is indexed by field t.
-__device__ inline int nib8(const char *__restrict__ Lb, uint32_t w) {
-    uint32_t lo = w & 0x3C3C3C3Cu;                                  // byte b: field 2b   times 4
-    uint32_t hi = __builtin_amdgcn_alignbit(w, w, 4) & 0x3C3C3C3Cu; // byte b: field 2b+1 times 4
-    // keep the byte-aligned form: each address is then one add with a byte
-    // select (SDWA) instead of a shift, a mask and an add per field
-    asm volatile("" : "+v"(lo), "+v"(hi));
-    const int a0 = *reinterpret_cast<const int *>(Lb + 0 * 64 + (lo & 0xFFu));
-    const int a1 = *reinterpret_cast<const int *>(Lb + 1 * 64 + (hi & 0xFFu));
-    const int a2 = *reinterpret_cast<const int *>(Lb + 2 * 64 + ((lo >> 8) & 0xFFu));
-    const int a3 = *reinterpret_cast<const int *>(Lb + 3 * 64 + ((hi >> 8) & 0xFFu));
-    const int a4 = *reinterpret_cast<const int *>(Lb + 4 * 64 + ((lo >> 16) & 0xFFu));
-    const int a5 = *reinterpret_cast<const int *>(Lb + 5 * 64 + ((hi >> 16) & 0xFFu));
-    const int a6 = *reinterpret_cast<const int *>(Lb + 6 * 64 + (lo >> 24));
-    const int a7 = *reinterpret_cast<const int *>(Lb + 7 * 64 + (hi >> 24));
-    return (a0 + a1 + a2) + (a3 + a4 + a5) + (a6 + a7);
-}
 
 __device__ inline float tri10(const float *__restrict__ L, uint32_t w) {
     float a = 0.f, b = 0.f;
@@ -107,12 +86,6 @@ __device__ inline float byte4(const float *__restrict__ cents, const float *__re
 template <int MODE> struct AccOf { typedef float type; };
 template <> struct AccOf<NIBBLE> { typedef int type; };
 
-// Sum of the 32 table hits of one 16-byte chunk; Lb is the chunk's 2 KiB of
-// table rows.
-__device__ inline int nib_chunk(const char *__restrict__ Lb, uint4 v) {
-    return (nib8(Lb, v.x) + nib8(Lb + 512, v.y)) + (nib8(Lb + 1024, v.z) + nib8(Lb + 1536, v.w));
-}
-
 template <int MODE>
 __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__ lds, int c, uint4 v) {
     if constexpr (MODE == NIBBLE) {
@@ -128,97 +101,6 @@ __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__
     }
 }
 
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m > 0; m >>= 1) v += __shfl_xor(v, m, 64);
-    return v;
-}
-
-// 4-bit-field tables (b in {1, 2, 4}): row r of 16 entries covers
-// coordinates r*g .. r*g+g-1 (g = 4/b) and rows = d*b/4 <= 2048, so thread t
-// owns rows t and t + 1024.  Loads the thread's coordinates of q'.
-__device__ inline void load_nibble_query(const ScanParams &p, const float *__restrict__ q,
-                                         float (&qv)[2][4]) {
-    const int g = 4 / p.bits;
-    const int rows = p.lut_words >> 4;
-#pragma unroll
-    for (int m = 0; m < 2; ++m) {
-        const int r = threadIdx.x + m * SCAN_THREADS;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) qv[m][t] = (r < rows && t < g) ? q[r * g + t] : 0.f;
-    }
-}
-
-// Writes this wave's share of sum_j |q'_j| to red[wave] (16 floats of LDS).
-__device__ inline void nibble_abs_sum(float *red, const float (&qv)[2][4]) {
-    float part = 0.f;
-#pragma unroll
-    for (int m = 0; m < 2; ++m)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) part += fabsf(qv[m][t]);
-    part = wave_sum(part);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
-}
-
-// Writes the int32 table from the coordinates loaded by load_nibble_query,
-// once red[] holds the 16 wave sums of |q'| (nibble_abs_sum, then a
-// barrier); returns the table's exponent sh.  The caller synchronises
-// before the table is read.
-//
-// Entries are rounded from float32 products: each is within 1/2 unit of
-// 2^sh c q' plus 2^-23 of its magnitude, so the summed error stays below
-// 2^-23 B + rows/2 units, B = max|c| sum_j |q'_j| -- far inside the score
-// tolerance.
-__device__ inline int build_nibble_table(float *lds, const float *red, const float *cents,
-                                         const ScanParams &p, const float (&qv)[2][4]) {
-    const int tid = threadIdx.x;
-    const int rows = p.lut_words >> 4;
-    const int L = 1 << p.bits;
-    // the levels: at most 16 (`cents` holds 16 values, unused ones finite)
-    float cl[16];
-#pragma unroll
-    for (int c = 0; c < 16; ++c) cl[c] = cents[c];
-    double tot = 0.0;
-#pragma unroll
-    for (int w = 0; w < SCAN_WAVES; ++w) tot += (double)red[w];
-    const double cmax = fmax(fabs((double)cl[0]), fabs((double)cl[L - 1]));
-    // bound with margin for the float32 partial sums and products
-    const double B = cmax * tot * (1.0 + 1e-5);
-    int sh = 0;
-    if (B > 0.0) {
-        sh = (int)floor(log2((2147483647.0 - 2.0 * p.d) / B));
-        sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
-    }
-    const float scale = ldexpf(1.0f, sh);
-    int *T = reinterpret_cast<int *>(lds);
-#pragma unroll
-    for (int m = 0; m < 2; ++m) {
-        const int r = tid + m * SCAN_THREADS;
-        if (r < rows) {
-            const float q0 = qv[m][0] * scale, q1 = qv[m][1] * scale;
-            const float q2 = qv[m][2] * scale, q3 = qv[m][3] * scale;
-            int e[16];
-            if (p.bits == 4) {
-#pragma unroll
-                for (int c = 0; c < 16; ++c) e[c] = (int)rintf(cl[c] * q0);
-            } else if (p.bits == 2) {
-#pragma unroll
-                for (int c = 0; c < 16; ++c) e[c] = (int)rintf(fmaf(cl[c & 3], q0, cl[c >> 2] * q1));
-            } else {
-#pragma unroll
-                for (int c = 0; c < 16; ++c)
-                    e[c] = (int)rintf(fmaf(cl[c & 1], q0, cl[(c >> 1) & 1] * q1) +
-                                      fmaf(cl[(c >> 2) & 1], q2, cl[c >> 3] * q3));
-            }
-            int4 *row = reinterpret_cast<int4 *>(T + r * 16);
-#pragma unroll
-            for (int c4 = 0; c4 < 4; ++c4)
-                row[c4] = make_int4(e[4 * c4], e[4 * c4 + 1], e[4 * c4 + 2], e[4 * c4 + 3]);
-        }
-    }
-    return sh;
-}
-
 // Builds the table for one query; returns the fixed-point exponent sh
 // (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.
 template <int MODE>
@@ -226,10 +108,10 @@ __device__ int build_table(float *lds, float *red, const ScanParams &p, const fl
     const int tid = threadIdx.x;
     if constexpr (MODE == NIBBLE) {
         float qv[2][4];
-        load_nibble_query(p, q, qv);
+        load_nibble_query(table_shape(p), q, qv);
         nibble_abs_sum(red, qv);
         __syncthreads();
-        return build_nibble_table(lds, red, p.cents, p, qv);
+        return build_nibble_table(lds, red, p.cents, table_shape(p), qv);
     } else if constexpr (MODE == TRIBIT) {
         for (int e = tid; e < p.lut_words; e += SCAN_THREADS) {
             const int j = e >> 3, c = e & 7;
@@ -242,66 +124,6 @@ __device__ int build_table(float *lds, float *red, const ScanParams &p, const fl
         return 0;
     }
 }
-
-// Order-preserving map of float32 onto int32 (for atomicMax thresholds).
-__device__ inline int fkey(float f) {
-    const int b = __float_as_int(f);
-    return b >= 0 ? b : (b ^ 0x7FFFFFFF);
-}
-__device__ inline float unfkey(int k) { return __int_as_float(k >= 0 ? k : (k ^ 0x7FFFFFFF)); }
-
-template <int S>
-struct WaveTopK {
-    float ls[S];
-    int li[S];
-    float th_s;      // this wave's k-th best (or -inf while fewer than k)
-    int th_i;
-    int seen_g;      // last global bound read (order key)
-    __device__ void reset() {
-#pragma unroll
-        for (int a = 0; a < S; ++a) {
-            ls[a] = -INFINITY;
-            li[a] = INT_MAX;
-        }
-        th_s = -INFINITY;
-        th_i = INT_MAX;
-        seen_g = fkey(-INFINITY);
-    }
-    // Offer one (score, id) per lane.  A score strictly below the bound --
-    // the best k-th score any wave of this workgroup (wg_key, LDS) or of any
-    // workgroup (g_key, global) has proven -- cannot reach the top k and is
-    // dropped before the sort.
-    __device__ void offer(float sc, int id, int lane, int k, int *wg_key, int *g_key) {
-        offer_seen(sc, id, lane, k, wg_key, g_key,
-                   __hip_atomic_load(g_key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-    }
-    // As offer(), with gk a value of the global bound read earlier by the
-    // caller (any earlier value is a valid, if weaker, bound).
-    __device__ void offer_seen(float sc, int id, int lane, int k, int *wg_key, int *g_key, int gk) {
-        seen_g = gk > seen_g ? gk : seen_g;
-        const int bk = *wg_key > seen_g ? *wg_key : seen_g;
-        const float bound = unfkey(bk);
-        const bool cand = better(sc, id, th_s, th_i) && !(sc < bound);
-        if (__any(cand)) {
-            if (!cand) {
-                sc = -INFINITY;
-                id = INT_MAX;
-            }
-            wave_sort64(sc, id, lane);
-            merge_sorted64<S>(ls, li, sc, id, lane);
-            rank_entry<S>(ls, li, k - 1, th_s, th_i);
-            if (th_s > -INFINITY) {
-                const int key = fkey(th_s);
-                if (lane == 0) atomicMax(wg_key, key);
-                if (key > seen_g) {
-                    if (lane == 0)
-                        __hip_atomic_fetch_max(g_key, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    seen_g = key;
-                }
-            }
-        }
-    }
-};
 
 __global__ void fill_keys(int *p, int64_t n, int v) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
@@ -612,10 +434,10 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
     }
     if (p.nq == 0) return;
     float qv[2][4];
-    load_nibble_query(p, p.qrot, qv);
+    load_nibble_query(table_shape(p), p.qrot, qv);
     nibble_abs_sum(red, qv);
     __syncthreads();
-    int sh = build_nibble_table(lds, red, cents_s, p, qv);
+    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
     __syncthreads();
 
     // this wave's current and next work items, and the ring holding the
@@ -701,7 +523,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         // sum while the others finish (red was last read by this table's build)
         const bool more = qi + 1 < p.nq;
         if (more) {
-            load_nibble_query(p, p.qrot + (int64_t)(qi + 1) * p.d, qv);
+            load_nibble_query(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
             nibble_abs_sum(red, qv);
         }
         __syncthreads();   // scan done: every offer made, the bound key final
@@ -714,7 +536,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         } else {
             tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
-        if (more) sh = build_nibble_table(lds, red, cents_s, p, qv);
+        if (more) sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
         if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
         __syncthreads();   // table ready; survivor count read by every wave
         if (tid == 0) misc[2] = 0;

@@ -175,4 +175,66 @@ __device__ inline void rank_entry(const float (&ls)[S], const int (&li)[S], int 
     i = __builtin_amdgcn_readlane(vi, ln);
 }
 
+// Order-preserving map of float32 onto int32 (for atomicMax thresholds).
+__device__ inline int fkey(float f) {
+    const int b = __float_as_int(f);
+    return b >= 0 ? b : (b ^ 0x7FFFFFFF);
+}
+__device__ inline float unfkey(int k) { return __int_as_float(k >= 0 ? k : (k ^ 0x7FFFFFFF)); }
+
+// A wave's best 64*S (score, id) entries, kept sorted in registers, with
+// the k-th best as threshold.
+template <int S>
+struct WaveTopK {
+    float ls[S];
+    int li[S];
+    float th_s;      // this wave's k-th best (or -inf while fewer than k)
+    int th_i;
+    int seen_g;      // last global bound read (order key)
+    __device__ void reset() {
+#pragma unroll
+        for (int a = 0; a < S; ++a) {
+            ls[a] = -INFINITY;
+            li[a] = INT_MAX;
+        }
+        th_s = -INFINITY;
+        th_i = INT_MAX;
+        seen_g = fkey(-INFINITY);
+    }
+    // Offer one (score, id) per lane.  A score strictly below the bound --
+    // the best k-th score any wave of this workgroup (wg_key, LDS) or of any
+    // workgroup (g_key, global) has proven -- cannot reach the top k and is
+    // dropped before the sort.
+    __device__ void offer(float sc, int id, int lane, int k, int *wg_key, int *g_key) {
+        offer_seen(sc, id, lane, k, wg_key, g_key,
+                   __hip_atomic_load(g_key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    }
+    // As offer(), with gk a value of the global bound read earlier by the
+    // caller (any earlier value is a valid, if weaker, bound).
+    __device__ void offer_seen(float sc, int id, int lane, int k, int *wg_key, int *g_key, int gk) {
+        seen_g = gk > seen_g ? gk : seen_g;
+        const int bk = *wg_key > seen_g ? *wg_key : seen_g;
+        const float bound = unfkey(bk);
+        const bool cand = better(sc, id, th_s, th_i) && !(sc < bound);
+        if (__any(cand)) {
+            if (!cand) {
+                sc = -INFINITY;
+                id = INT_MAX;
+            }
+            wave_sort64(sc, id, lane);
+            merge_sorted64<S>(ls, li, sc, id, lane);
+            rank_entry<S>(ls, li, k - 1, th_s, th_i);
+            if (th_s > -INFINITY) {
+                const int key = fkey(th_s);
+                if (lane == 0) atomicMax(wg_key, key);
+                if (key > seen_g) {
+                    if (lane == 0)
+                        __hip_atomic_fetch_max(g_key, key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    seen_g = key;
+                }
+            }
+        }
+    }
+};
+
 }  // namespace tq

@@ -1,0 +1,112 @@
+"""GPU parity of the batched matrix-core search path (TQ_PATH_MFMA) against
+the oracle and against the single-query path on the small workload.
+
+The batched path selects 64 candidates per query from float16 matrix-core
+scores and rescores them with the single-query path's integer tables, so a
+returned (id, score) pair carries exactly the score the single-query path
+gives that id; a certificate proves the exact top k is among the candidates,
+and queries without one are re-run on the single-query path."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.conftest import gpu_available
+from tests.parity import check_topk
+
+pytestmark = pytest.mark.gpu
+if not gpu_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import torch  # noqa: E402
+
+import paper_2607_16973_amd as tq  # noqa: E402
+
+D = 1536
+
+
+@pytest.fixture(scope="module")
+def env(small_env):
+    return small_env
+
+
+def same_as_lut(idx, Q, k, mi, ms, allow=None):
+    """Every id the batched path returns carries the single-query path's
+    score for it, and both lists agree up to swaps of equal scores."""
+    li, ls = idx.search(Q, k, allow=allow, path="lut")
+    li, ls, mi, ms = (t.cpu().numpy() for t in (li, ls, mi, ms))
+    for b in range(Q.shape[0]):
+        assert np.array_equal(np.sort(ls[b]), np.sort(ms[b])), b
+        tied = np.isin(ms[b], ms[b][np.isin(mi[b], li[b], invert=True)])
+        assert np.all(np.isin(mi[b], li[b]) | tied), b
+
+
+@pytest.mark.parametrize("k", [10, 1, 64])
+def test_batched_matches_oracle_and_lut(env, k):
+    print("mfma k=%d" % k, flush=True)
+    ids, sc = env.idx.search(env.Qd, k, path="mfma")
+    fb = tq.last_search_fallbacks()
+    ref_i, ref_s = oracle.search(env.codes, env.scales, env.ocb.cents, env.R32, env.Q, k)
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents,
+               env.qrot, env.qn, k, ref_i, ref_s)
+    same_as_lut(env.idx, env.Qd, k, ids, sc)
+    print("fallbacks %d of %d" % (fb, env.Q.shape[0]), flush=True)
+    if k == 10:
+        # the certificate should hold for nearly every query of this workload
+        assert fb <= env.Q.shape[0] // 4
+
+
+@pytest.mark.parametrize("nq", [1, 15, 45])
+def test_ragged_query_counts(env, nq):
+    Q = env.Qd[:nq].contiguous()
+    ids, sc = env.idx.search(Q, 10, path="mfma")
+    ref_i, ref_s = oracle.search(env.codes, env.scales, env.ocb.cents, env.R32, env.Q[:nq], 10)
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents,
+               env.qrot[:nq], env.qn[:nq], 10, ref_i, ref_s)
+
+
+def test_ragged_index_and_filter(env):
+    """n not a multiple of 64 (or of 512), with a selective tenant filter."""
+    n = 5000 + 37
+    T = 100
+    tenants = synth.zipf_tenants(n, T, seed=44)
+    allowed = synth.allowlists(env.Q.shape[0], T, "broad", seed=45)
+    bm = synth.allowlist_bitmap(allowed, T)
+    idx = tq.Index(env.cb, env.rot, n_tenants=T)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(env.codes[:n], 4)).cuda(),
+                  torch.from_numpy(env.scales[:n]).cuda(),
+                  torch.from_numpy(tenants.view(np.int16)).cuda())
+    allow_d = torch.from_numpy(bm.view(np.int64)).cuda()
+    ids, sc = idx.search(env.Qd, 10, allow=allow_d, path="mfma")
+    ref_i, ref_s = oracle.search(env.codes[:n], env.scales[:n], env.ocb.cents, env.R32, env.Q, 10,
+                                 tenants, bm)
+    masks = [oracle.allowed_mask(tenants, bm[b]) for b in range(env.Q.shape[0])]
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes[:n], env.scales[:n],
+               env.ocb.cents, env.qrot, env.qn, 10, ref_i, ref_s, allowed=masks, n=n)
+    same_as_lut(idx, env.Qd, 10, ids, sc, allow=allow_d)
+
+
+def test_certificate_failure_falls_back(env):
+    """200 copies of one vector tie every candidate score: no certificate can
+    hold, so every query is re-run on the single-query path."""
+    n = 200
+    pk = torch.from_numpy(oracle.pack_codes(np.repeat(env.codes[:1], n, axis=0), 4)).cuda()
+    sc0 = torch.from_numpy(np.repeat(env.scales[:1], n)).cuda()
+    idx = tq.Index(env.cb, env.rot, n_tenants=1)
+    idx.add_codes(pk, sc0)
+    Q = env.Qd[:8].contiguous()
+    ids, sc = idx.search(Q, 10, path="mfma")
+    assert tq.last_search_fallbacks() == 8
+    li, ls = idx.search(Q, 10, path="lut")
+    assert torch.equal(ids, li) and torch.equal(sc, ls)
+    assert np.array_equal(ids.cpu().numpy()[0], np.arange(10))   # ties: lowest ids
+
+
+def test_unsupported_shapes_rejected(env):
+    with pytest.raises(tq.TQError, match="TQ_EUNSUPPORTED"):
+        env.idx.search(env.Qd, 100, path="mfma")
+    cb2 = tq.Codebook(D, 2)
+    idx = tq.Index(cb2, env.rot, n_tenants=1)
+    idx.add(env.Xd[:100].contiguous())
+    with pytest.raises(tq.TQError, match="TQ_EUNSUPPORTED"):
+        idx.search(env.Qd, 10, path="mfma")

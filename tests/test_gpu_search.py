@@ -27,28 +27,9 @@ import paper_2607_16973_amd as tq  # noqa: E402
 D = 1536
 
 
-class Setup:
-    pass
-
-
 @pytest.fixture(scope="module")
-def env():
-    s = Setup()
-    s.X, s.Q = synth.workload("small")
-    s.R32 = oracle.haar_rotation(D, 42)[1]
-    s.ocb = oracle.lloyd_max(D, 4)
-    s.codes, s.norms, s.scales = oracle.encode(s.X, s.R32, s.ocb)
-    s.qrot = oracle.rotate_queries(s.R32, s.Q)
-    s.qn = np.linalg.norm(s.Q.astype(np.float64), axis=1)
-    s.cb = tq.Codebook(D, 4)
-    s.rot = tq.Rotation(D, 42)
-    s.Xd = torch.from_numpy(s.X).cuda()
-    s.Qd = torch.from_numpy(s.Q).cuda()
-    s.idx = tq.Index(s.cb, s.rot, n_tenants=1)
-    print("index add n=%d" % s.X.shape[0], flush=True)
-    s.idx.add(s.Xd)
-    torch.cuda.synchronize()
-    return s
+def env(small_env):
+    return small_env
 
 
 def oracle_topk(s, k, tenants=None, allow=None, n=None):
