@@ -73,10 +73,12 @@ class Codebook:
         check(lib.tq_codebook_mse(h, ctypes.byref(m)))
         self.mse = m.value
 
-    def __del__(self):
+    # the free function is bound when the class is defined: module globals may
+    # already be gone when an object is collected at interpreter exit
+    def __del__(self, _free=lib.tq_codebook_free):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            lib.tq_codebook_free(h)
+            _free(h)
             self._h = None
 
 
@@ -94,10 +96,12 @@ class Rotation:
         check(lib.tq_rotation_matrix(self._h, R.ctypes.data_as(ctypes.c_void_p)))
         return R
 
-    def __del__(self):
+    # the free function is bound when the class is defined: module globals may
+    # already be gone when an object is collected at interpreter exit
+    def __del__(self, _free=lib.tq_rotation_free):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            lib.tq_rotation_free(h)
+            _free(h)
             self._h = None
 
 
@@ -213,8 +217,10 @@ class Index:
                             _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
         return ids, scores
 
-    def __del__(self):
+    # the free function is bound when the class is defined: module globals may
+    # already be gone when an object is collected at interpreter exit
+    def __del__(self, _free=lib.tq_index_free):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            lib.tq_index_free(h)
+            _free(h)
             self._h = None

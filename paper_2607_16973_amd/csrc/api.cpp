@@ -509,10 +509,17 @@ static size_t search_bytes(const ScanShape &sh, int64_t nq, int k, int base) {
                                  : lut_search_workspace_bytes(sh, nq, k, scan_grid());
 }
 
-static float centroid_max(const tq_index *x) {
-    float m = 0.f;
-    for (int i = 0; i < (1 << x->bits); ++i) m = std::max(m, std::fabs(x->cbdev.cents32[i]));
-    return m;
+// max |float16(c)| and max |float16(c) - c| over the float32 centroids
+static void centroid_half_bounds(const tq_index *x, float *cmax16, float *dmax) {
+    float m = 0.f, dm = 0.f;
+    for (int i = 0; i < (1 << x->bits); ++i) {
+        const float c = x->cbdev.cents32[i];
+        const float h = (float)(_Float16)c;
+        m = std::max(m, std::fabs(h));
+        dm = std::max(dm, std::fabs(h - c));
+    }
+    *cmax16 = m;
+    *dmax = dm;
 }
 
 tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, int32_t path,
@@ -581,8 +588,10 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     }
     if (use_mfma(sh, k, base)) {
         int n_fallback = 0;
+        float cmax16 = 0.f, dmax = 0.f;
+        centroid_half_bounds(idx, &cmax16, &dmax);
         hipError_t e = mfma_search(sh, idx->codes, idx->scales, scale_max_dev(idx), idx->tenants,
-                                   idx->summ, idx->cents_dev, centroid_max(idx), Qrot, nq, k,
+                                   idx->summ, idx->cents_dev, cmax16, dmax, Qrot, nq, k,
                                    allow_dev, grid, workspace_dev, ids_dev, scores_dev,
                                    &n_fallback, s);
         if (e != hipSuccess) return hip_fail(e, "matrix-core search");

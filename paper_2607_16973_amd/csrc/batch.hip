@@ -36,7 +36,8 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
-constexpr int kCand = 64;          // candidates per query kept for exact rescoring
+constexpr int kCand = 256;         // candidates per query kept for exact rescoring
+constexpr int kCandS = kCand / 64;  // 64-entry slots of a candidate list
 constexpr int MF_THREADS = 512;    // 8 waves: two per SIMD, 256 registers each
 constexpr int MF_WAVES = MF_THREADS / 64;
 constexpr int SEL_THREADS = 256;
@@ -47,26 +48,27 @@ constexpr int kKeepVmemB = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
 struct QInfo {
     float f;      // stored approximate score = s_v * acc * f (acc: MFMA sum of the scaled query)
     float norm;   // approximate score = stored * norm  (s_max ||q'||_2)
-    float err;    // E: bound on |approximate - exact| for every vector
+    float err;    // bound on |approximate - exact| before the float16 storage
     float pad;
 };
 
 // ------------------------------------------------------------------- prep
-// The query is scaled by alpha = 2^e with max|alpha q'_j| in [2^14, 2^15),
-// then rounded to float16 (relative error 2^-11, or 2^-25 absolute below
-// the normal range).  Error bound of the approximate score of vector v
-// against the exact one (both times s_v <= s_max), with u = 2^-11,
-// cmax = max|c|, q1 = ||q'||_1, and float32 accumulation of the d products
-// in any order (gamma_d = d 2^-24 / (1 - d 2^-24)):
-//   float16 centroids and query, products exact in float32:
-//       cmax q1 (2u + u^2) + cmax d 2^-25 (1 + u) / alpha
-//   accumulation:  gamma_d (1 + u)^2 cmax q1 + gamma_d cmax d 2^-25 / alpha
-//   scaling by s_v and f (two float32 roundings): 2^-22 cmax q1
-//   float16 storage of approx / norm: u |approx| + 2^-25 norm
-//   the exact score itself (integer table, float conversion): 7e-7 cmax q1
-// Their sum, times s_max, times 1.25 for margin, is E.
+// The query is scaled by alpha = 2^e with max|alpha q'_j| in [2^14, 2^15)
+// and rounded to float16: alpha q'_j + eps_j.  With the float16 centroids
+// c_l + delta_l (|delta_l| <= dmax, |c_l + delta_l| <= cmax16), the MFMA sum
+// is alpha sum_j c q'_j + sum_j (alpha delta q'_j + (c + delta) eps_j), so
+//   |acc / alpha - <c, q'>| <= dmax ||q'||_1 + cmax16 ||eps||_1 / alpha
+// plus the float32 accumulation of d products in any order,
+//   gamma_d cmax16 (||q'||_1 + ||eps||_1 / alpha),  gamma_d = d u / (1 - d u),
+// u = 2^-24, and two float32 roundings when scaling (2^-23 of the same
+// magnitude).  The exact score (integer table, float conversion) is within
+// 7e-7 cmax ||q'||_1 of s_v <c, q'>.  The sum, times s_max and 1.1, is the
+// error before storage; the float16 storage of the approximate score adds
+// at most 2^-11 of its magnitude plus 2^-25 norm, accounted for where the
+// certificate is checked.
 __global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const float *smax_p,
-                            float cmax, _Float16 *__restrict__ q16, QInfo *__restrict__ info) {
+                            float cmax16, float dmax, _Float16 *__restrict__ q16,
+                            QInfo *__restrict__ info) {
     __shared__ float red_m[SEL_THREADS / 64];
     __shared__ double red_1[SEL_THREADS / 64], red_2[SEL_THREADS / 64];
     const int q = blockIdx.x;
@@ -99,25 +101,34 @@ __global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const fl
         s1 += red_1[w];
         s2 += red_2[w];
     }
+    __syncthreads();   // red_1 is reused below
     const int e = m > 0.f ? 14 - ilogbf(m) : 0;
     const float alpha = ldexpf(1.0f, e);
-    for (int j = tid; j < d; j += SEL_THREADS) q16[(int64_t)q * d + j] = (_Float16)(row[j] * alpha);
+    double se = 0.0;   // ||eps||_1
+    for (int j = tid; j < d; j += SEL_THREADS) {
+        const float a = row[j] * alpha;   // exact: alpha is a power of two
+        const _Float16 h = (_Float16)a;
+        q16[(int64_t)q * d + j] = h;
+        se += fabs((double)(float)h - (double)a);
+    }
+    for (int o = 32; o > 0; o >>= 1) se += __shfl_xor(se, o, 64);
+    if (lane == 0) red_1[wave] = se;
+    __syncthreads();
     if (tid == 0) {
+        se = 0.0;
+        for (int w = 0; w < SEL_THREADS / 64; ++w) se += red_1[w];
         const double smax = (double)*smax_p;
         double norm = smax * sqrt(s2);
         if (!(norm > 0.0)) norm = 1.0;
-        const double u = ldexp(1.0, -11);
-        const double t = ldexp(1.0, -25);
-        const double gd = d * ldexp(1.0, -24) / (1.0 - d * ldexp(1.0, -24));
-        const double cq = (double)cmax * s1;
-        const double sub = (double)cmax * d * t / alpha;
-        double E = cq * (2 * u + u * u) + sub * (1 + u) + gd * (1 + u) * (1 + u) * cq + gd * sub +
-                   ldexp(1.0, -22) * cq + u * cq * (1 + 4 * u) + 7e-7 * cq;
-        E = smax * E + t * norm;
+        const double u = ldexp(1.0, -24);
+        const double gd = d * u / (1.0 - d * u);
+        const double mag = (double)cmax16 * (s1 + se / alpha);
+        const double E = (double)dmax * s1 + (double)cmax16 * se / alpha + gd * mag +
+                         2 * ldexp(1.0, -23) * mag + 7e-7 * (double)cmax16 * s1;
         QInfo qi;
         qi.f = (float)(1.0 / ((double)alpha * norm));
         qi.norm = (float)norm;
-        qi.err = (float)(1.25 * E);
+        qi.err = (float)(1.1 * smax * E);
         qi.pad = 0.f;
         info[q] = qi;
     }
@@ -298,10 +309,17 @@ struct SelectParams {
 };
 
 // The kCand best allowed approximate scores of one query over 1/SEL_GROUPS
-// of the vectors; each lane reads 8 consecutive scores per load.
+// of the vectors; each lane reads 8 consecutive scores per load.  A wave
+// keeps its best kCand in registers; scores that pass its current bound are
+// first appended to a per-wave LDS buffer, and the buffer is sorted into
+// the list only when 64 have gathered -- a sort per 64 real candidates
+// rather than per 64 scores read.
 __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
-    __shared__ float st_s[4 * 64];
-    __shared__ int st_i[4 * 64];
+    constexpr int NW = SEL_THREADS / 64;
+    __shared__ float st_s[NW * kCand];
+    __shared__ int st_i[NW * kCand];
+    __shared__ float buf_s[NW * 128];
+    __shared__ int buf_i[NW * 128];
     __shared__ int wg_key;
     __shared__ uint64_t allow_s[64];
     const int g = blockIdx.x, q = blockIdx.y;
@@ -311,15 +329,40 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     if (filtered)
         for (int w = tid; w < p.W && w < 64; w += SEL_THREADS) allow_s[w] = p.allow[(int64_t)q * p.W + w];
     __syncthreads();
+    float *bs = buf_s + wave * 128;
+    int *bi = buf_i + wave * 128;
+    int cnt = 0;   // wave-uniform
+    const uint64_t below = (1ull << lane) - 1;
     // ranges of 512 vectors (one load per lane per wave)
     const int64_t units = p.npad / 512;
     const int64_t u0 = units * g / SEL_GROUPS, u1 = units * (g + 1) / SEL_GROUPS;
-    WaveTopK<1> top;
+    WaveTopK<kCandS> top;
     top.reset();
     const uint4 *row = reinterpret_cast<const uint4 *>(p.approx + (int64_t)q * p.npad);
-    for (int64_t u = u0 + wave; u < u1; u += 4) {
+    auto flush = [&](int gk) {
+        const float sc = lane < cnt ? bs[lane] : -INFINITY;
+        const int id = lane < cnt ? bi[lane] : INT_MAX;
+        __builtin_amdgcn_wave_barrier();
+        const int rest = cnt > 64 ? cnt - 64 : 0;
+        float ms = 0.f;
+        int mi = 0;
+        if (lane < rest) {
+            ms = bs[64 + lane];
+            mi = bi[64 + lane];
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane < rest) {
+            bs[lane] = ms;
+            bi[lane] = mi;
+        }
+        cnt = rest;
+        top.offer_seen(sc, id, lane, kCand, &wg_key, p.gbound + q, gk);
+    };
+    for (int64_t u = u0 + wave; u < u1; u += NW) {
         const uint4 w = row[u * 64 + lane];
         const int gk = __hip_atomic_load(p.gbound + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int bk = max(max(gk, wg_key), max(top.seen_g, fkey(top.th_s)));
+        const float thr = unfkey(bk);
         const _Float16 *h = reinterpret_cast<const _Float16 *>(&w);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -329,23 +372,46 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
                 const int t = p.tenants[v];
                 ok = (t >> 6) < p.W && ((allow_s[t >> 6] >> (t & 63)) & 1ull);
             }
-            top.offer_seen(ok ? (float)h[e] : -INFINITY, ok ? (int)v : INT_MAX, lane, kCand,
-                           &wg_key, p.gbound + q, gk);
+            const float val = (float)h[e];
+            const bool cand = ok && !(val < thr);
+            const uint64_t m = __ballot(cand);
+            if (m) {
+                if (cand) {
+                    const int pos = cnt + __popcll(m & below);
+                    bs[pos] = val;
+                    bi[pos] = (int)v;
+                }
+                cnt += __popcll(m);
+                __builtin_amdgcn_wave_barrier();
+                if (cnt >= 64) flush(gk);
+            }
         }
     }
-    // merge the 4 wave lists
-    st_s[wave * 64 + lane] = top.ls[0];
-    st_i[wave * 64 + lane] = top.li[0];
+    while (cnt > 0) flush(top.seen_g);
+    // merge the wave lists
+#pragma unroll
+    for (int a = 0; a < kCandS; ++a) {
+        st_s[wave * kCand + a * 64 + lane] = top.ls[a];
+        st_i[wave * kCand + a * 64 + lane] = top.li[a];
+    }
     __syncthreads();
     if (wave == 0) {
-        for (int w = 1; w < 4; ++w) {
-            float os[1] = {st_s[w * 64 + lane]};
-            int oi[1] = {st_i[w * 64 + lane]};
-            merge_lists<1>(top.ls, top.li, os, oi, lane);
+        for (int w = 1; w < NW; ++w) {
+            float os[kCandS];
+            int oi[kCandS];
+#pragma unroll
+            for (int a = 0; a < kCandS; ++a) {
+                os[a] = st_s[w * kCand + a * 64 + lane];
+                oi[a] = st_i[w * kCand + a * 64 + lane];
+            }
+            merge_lists<kCandS>(top.ls, top.li, os, oi, lane);
         }
         const int64_t base = ((int64_t)q * SEL_GROUPS + g) * kCand;
-        p.cand_s[base + lane] = top.ls[0];
-        p.cand_i[base + lane] = top.li[0];
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a) {
+            p.cand_s[base + a * 64 + lane] = top.ls[a];
+            p.cand_i[base + a * 64 + lane] = top.li[a];
+        }
     }
 }
 
@@ -354,29 +420,50 @@ __global__ __launch_bounds__(256) void select_merge_kernel(const float *__restri
                                                            const int *__restrict__ ci,
                                                            float *__restrict__ top_s,
                                                            int *__restrict__ top_i) {
-    __shared__ float st_s[4 * 64];
-    __shared__ int st_i[4 * 64];
+    __shared__ float st_s[4 * kCand];
+    __shared__ int st_i[4 * kCand];
     const int q = blockIdx.x;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    float ls[1] = {-INFINITY};
-    int li[1] = {INT_MAX};
+    float ls[kCandS];
+    int li[kCandS];
+#pragma unroll
+    for (int a = 0; a < kCandS; ++a) {
+        ls[a] = -INFINITY;
+        li[a] = INT_MAX;
+    }
     for (int g = wave; g < SEL_GROUPS; g += 4) {
         const int64_t base = ((int64_t)q * SEL_GROUPS + g) * kCand;
-        float os[1] = {cs[base + lane]};
-        int oi[1] = {ci[base + lane]};
-        merge_lists<1>(ls, li, os, oi, lane);
+        float os[kCandS];
+        int oi[kCandS];
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a) {
+            os[a] = cs[base + a * 64 + lane];
+            oi[a] = ci[base + a * 64 + lane];
+        }
+        merge_lists<kCandS>(ls, li, os, oi, lane);
     }
-    st_s[wave * 64 + lane] = ls[0];
-    st_i[wave * 64 + lane] = li[0];
+#pragma unroll
+    for (int a = 0; a < kCandS; ++a) {
+        st_s[wave * kCand + a * 64 + lane] = ls[a];
+        st_i[wave * kCand + a * 64 + lane] = li[a];
+    }
     __syncthreads();
     if (wave == 0) {
         for (int w = 1; w < 4; ++w) {
-            float os[1] = {st_s[w * 64 + lane]};
-            int oi[1] = {st_i[w * 64 + lane]};
-            merge_lists<1>(ls, li, os, oi, lane);
+            float os[kCandS];
+            int oi[kCandS];
+#pragma unroll
+            for (int a = 0; a < kCandS; ++a) {
+                os[a] = st_s[w * kCand + a * 64 + lane];
+                oi[a] = st_i[w * kCand + a * 64 + lane];
+            }
+            merge_lists<kCandS>(ls, li, os, oi, lane);
         }
-        top_s[(int64_t)q * kCand + lane] = ls[0];
-        top_i[(int64_t)q * kCand + lane] = li[0];
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a) {
+            top_s[(int64_t)q * kCand + a * 64 + lane] = ls[a];
+            top_i[(int64_t)q * kCand + a * 64 + lane] = li[a];
+        }
     }
 }
 
@@ -427,20 +514,40 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
     }
     __syncthreads();
     if (wave == 0) {
-        float s = ex_s[lane];
-        int i = ex_i[lane];
-        wave_sort64(s, i, lane);
-        if (lane < p.k) {
-            const bool empty = !(s > -INFINITY);
-            p.ids[(int64_t)q * p.k + lane] = empty ? -1 : (int64_t)i;
-            p.scores[(int64_t)q * p.k + lane] = empty ? -INFINITY : s;
+        // exact scores sorted into one list of kCand
+        float ls[kCandS];
+        int li[kCandS];
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a) {
+            ls[a] = -INFINITY;
+            li[a] = INT_MAX;
         }
-        // certificate
-        const int nvalid = __popcll(__ballot(p.top_i[(int64_t)q * kCand + lane] != INT_MAX));
-        const float ek = __shfl(s, p.k - 1, 64);
-        const float amin = p.top_s[(int64_t)q * kCand + kCand - 1];
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a) {
+            float s = ex_s[a * 64 + lane];
+            int i = ex_i[a * 64 + lane];
+            wave_sort64(s, i, lane);
+            merge_sorted64<kCandS>(ls, li, s, i, lane);
+        }
+        if (lane < p.k) {
+            const bool empty = !(ls[0] > -INFINITY);
+            p.ids[(int64_t)q * p.k + lane] = empty ? -1 : (int64_t)li[0];
+            p.scores[(int64_t)q * p.k + lane] = empty ? -INFINITY : ls[0];
+        }
+        // Certificate: a vector outside the candidates has a stored score at
+        // most the last candidate's, so its exact score is at most
+        // amin + 2^-11 |amin| + 2^-25 norm + err; below the k-th exact
+        // score it cannot enter the top k.
+        int nvalid = 0;
+#pragma unroll
+        for (int a = 0; a < kCandS; ++a)
+            nvalid += __popcll(__ballot(p.top_i[(int64_t)q * kCand + a * 64 + lane] != INT_MAX));
+        const float ek = __shfl(ls[0], p.k - 1, 64);
         const QInfo qi = p.info[q];
-        const bool cert = nvalid < kCand || (double)amin * qi.norm + (double)qi.err < (double)ek;
+        const double amin = (double)p.top_s[(int64_t)q * kCand + kCand - 1] * qi.norm;
+        const double reach = amin + ldexp(1.0, -11) * fabs(amin) + ldexp(1.0, -25) * qi.norm +
+                             (double)qi.err;
+        const bool cert = nvalid < kCand || reach < (double)ek;
         if (lane == 0) p.flags[q] = cert ? 0 : 1;
     }
 }
@@ -545,7 +652,7 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
 }  // namespace
 
 bool mfma_search_supported(const ScanShape &s, int k) {
-    return s.bits == 4 && s.chunks % 8 == 0 && k <= kCand && s.W <= 64;
+    return s.bits == 4 && s.chunks % 8 == 0 && k <= 64 && s.W <= 64;
 }
 
 size_t mfma_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid) {
@@ -563,7 +670,8 @@ hipError_t update_scale_max(const float *scales, int64_t n, float *smax, hipStre
 
 hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                        const float *smax, const uint16_t *tenants, const uint64_t *summaries,
-                       const float *cents32, float cmax, const float *Qrot, int64_t nq, int k,
+                       const float *cents32, float cmax16, float dmax, const float *Qrot,
+                       int64_t nq, int k,
                        const uint64_t *allow, int grid, void *ws, int64_t *ids, float *scores,
                        int *n_fallback, hipStream_t stream) {
     const BatchLayout L = batch_layout(s, nq, k, grid);
@@ -593,7 +701,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     for (int64_t q0 = 0; q0 < nq; q0 += kTile) {
         const int nqt = (int)((nq - q0) < kTile ? (nq - q0) : kTile);
         hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream, Qrot + q0 * s.d,
-                           nqt, s.d, smax, cmax, q16, info);
+                           nqt, s.d, smax, cmax16, dmax, q16, info);
         ScoreParams sp{};
         sp.codes = reinterpret_cast<const uint4 *>(blocked);
         sp.scales = scales;

@@ -87,6 +87,8 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
 
 // Batched search of a tile of queries on the matrix cores with exact
 // rescoring (b = 4, chunks % 8 == 0, k <= 64, at most 4096 tenants).
+// cmax16 = max |float16(c_l)|, dmax = max |float16(c_l) - c_l| over the
+// float32 centroids cents32.
 // Queries whose top k the certificate does not prove are re-run on the
 // single-query scan; their count goes to *n_fallback.  Synchronises
 // `stream` once to read the certificates.  `smax` is a device float: the
@@ -95,7 +97,8 @@ bool mfma_search_supported(const ScanShape &s, int k);
 size_t mfma_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid);
 hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                        const float *smax, const uint16_t *tenants, const uint64_t *summaries,
-                       const float *cents32, float cmax, const float *Qrot, int64_t nq, int k,
+                       const float *cents32, float cmax16, float dmax, const float *Qrot,
+                       int64_t nq, int k,
                        const uint64_t *allow, int grid, void *ws, int64_t *ids, float *scores,
                        int *n_fallback, hipStream_t stream);
 // *smax = max(*smax, max of scales[0..n)); scales are >= 0.

@@ -87,9 +87,10 @@ def test_ragged_index_and_filter(env):
 
 
 def test_certificate_failure_falls_back(env):
-    """200 copies of one vector tie every candidate score: no certificate can
-    hold, so every query is re-run on the single-query path."""
-    n = 200
+    """400 copies of one vector (more than the 256 candidates) tie every
+    score: no certificate can hold, so every query is re-run on the
+    single-query path."""
+    n = 400
     pk = torch.from_numpy(oracle.pack_codes(np.repeat(env.codes[:1], n, axis=0), 4)).cuda()
     sc0 = torch.from_numpy(np.repeat(env.scales[:1], n)).cuda()
     idx = tq.Index(env.cb, env.rot, n_tenants=1)
