@@ -42,6 +42,8 @@ constexpr int MF_THREADS = 512;    // 8 waves: two per SIMD, 256 registers each
 constexpr int MF_WAVES = MF_THREADS / 64;
 constexpr int SEL_THREADS = 256;
 constexpr int SEL_GROUPS = 32;     // select workgroups per query
+constexpr int kBoundStride = 32;  // ints between the global bounds of two queries
+constexpr int kBuf = 8 * 64 + 64;  // per-wave candidate buffer: one load of 8 scores per lane + a partial 64
 constexpr int kKeepVmemB = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
 
 // Per-query constants written by prep_kernel.
@@ -303,7 +305,7 @@ struct SelectParams {
     const uint64_t *allow;     // [nqt][W] or null
     float *cand_s;             // [nqt][SEL_GROUPS][kCand]
     int *cand_i;
-    int *gbound;               // [nqt] order keys
+    int *gbound;               // [nqt * kBoundStride] order keys
     int64_t n, npad;
     int W;
 };
@@ -318,8 +320,8 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     constexpr int NW = SEL_THREADS / 64;
     __shared__ float st_s[NW * kCand];
     __shared__ int st_i[NW * kCand];
-    __shared__ float buf_s[NW * 128];
-    __shared__ int buf_i[NW * 128];
+    __shared__ float buf_s[NW * kBuf];
+    __shared__ int buf_i[NW * kBuf];
     __shared__ int wg_key;
     __shared__ uint64_t allow_s[64];
     const int g = blockIdx.x, q = blockIdx.y;
@@ -329,8 +331,9 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     if (filtered)
         for (int w = tid; w < p.W && w < 64; w += SEL_THREADS) allow_s[w] = p.allow[(int64_t)q * p.W + w];
     __syncthreads();
-    float *bs = buf_s + wave * 128;
-    int *bi = buf_i + wave * 128;
+    int *gb = p.gbound + q * kBoundStride;
+    float *bs = buf_s + wave * kBuf;
+    int *bi = buf_i + wave * kBuf;
     int cnt = 0;   // wave-uniform
     const uint64_t below = (1ull << lane) - 1;
     // ranges of 512 vectors (one load per lane per wave)
@@ -339,31 +342,16 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     WaveTopK<kCandS> top;
     top.reset();
     const uint4 *row = reinterpret_cast<const uint4 *>(p.approx + (int64_t)q * p.npad);
-    auto flush = [&](int gk) {
-        const float sc = lane < cnt ? bs[lane] : -INFINITY;
-        const int id = lane < cnt ? bi[lane] : INT_MAX;
-        __builtin_amdgcn_wave_barrier();
-        const int rest = cnt > 64 ? cnt - 64 : 0;
-        float ms = 0.f;
-        int mi = 0;
-        if (lane < rest) {
-            ms = bs[64 + lane];
-            mi = bi[64 + lane];
-        }
-        __builtin_amdgcn_wave_barrier();
-        if (lane < rest) {
-            bs[lane] = ms;
-            bi[lane] = mi;
-        }
-        cnt = rest;
-        top.offer_seen(sc, id, lane, kCand, &wg_key, p.gbound + q, gk);
-    };
     for (int64_t u = u0 + wave; u < u1; u += NW) {
         const uint4 w = row[u * 64 + lane];
-        const int gk = __hip_atomic_load(p.gbound + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // the global bound is read on every 4th load (each read is a trip to L2)
+        const int gk = ((u - u0 - wave) & (4 * NW - 1)) == 0
+                           ? __hip_atomic_load(gb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                           : top.seen_g;
         const int bk = max(max(gk, wg_key), max(top.seen_g, fkey(top.th_s)));
         const float thr = unfkey(bk);
         const _Float16 *h = reinterpret_cast<const _Float16 *>(&w);
+        // append the 8 scores of each lane that pass the bound
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int64_t v = u * 512 + lane * 8 + e;
@@ -375,19 +363,28 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
             const float val = (float)h[e];
             const bool cand = ok && !(val < thr);
             const uint64_t m = __ballot(cand);
-            if (m) {
-                if (cand) {
-                    const int pos = cnt + __popcll(m & below);
-                    bs[pos] = val;
-                    bi[pos] = (int)v;
-                }
-                cnt += __popcll(m);
-                __builtin_amdgcn_wave_barrier();
-                if (cnt >= 64) flush(gk);
+            if (cand) {
+                const int pos = cnt + __popcll(m & below);
+                bs[pos] = val;
+                bi[pos] = (int)v;
             }
+            cnt += __popcll(m);
+        }
+        __builtin_amdgcn_wave_barrier();
+        // sort them in, 64 at a time (one copy of the sort in the code)
+        while (cnt >= 64) {
+            cnt -= 64;
+            const float sc = bs[cnt + lane];
+            const int id = bi[cnt + lane];
+            __builtin_amdgcn_wave_barrier();
+            top.offer_seen(sc, id, lane, kCand, &wg_key, gb, gk);
         }
     }
-    while (cnt > 0) flush(top.seen_g);
+    if (cnt > 0) {
+        const float sc = lane < cnt ? bs[lane] : -INFINITY;
+        const int id = lane < cnt ? bi[lane] : INT_MAX;
+        top.offer_seen(sc, id, lane, kCand, &wg_key, gb, top.seen_g);
+    }
     // merge the wave lists
 #pragma unroll
     for (int a = 0; a < kCandS; ++a) {
@@ -497,19 +494,30 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
     const int sh = build_nibble_table(lds, red, p.cents, ts, qv);
     __syncthreads();
     const char *lut = reinterpret_cast<const char *>(lds);
-    for (int j = wave; j < kCand; j += kTableWaves) {
-        const int v = p.top_i[(int64_t)q * kCand + j];
-        int part = 0;
-        const bool valid = v != INT_MAX;
-        if (valid && lane < p.chunks) {
-            const uint4 w = p.codes[((int64_t)(v >> 6) * p.chunks + lane) * 64 + (v & 63)];
-            part = nib_chunk(lut + lane * 2048, w);
+    // each wave scores kCand / 16 candidates, 4 at a time: their chunk loads
+    // are issued together
+    constexpr int PER = kCand / kTableWaves, GRP = 4;
+    for (int j0 = 0; j0 < PER; j0 += GRP) {
+        int v[GRP];
+        uint4 w[GRP];
+#pragma unroll
+        for (int t = 0; t < GRP; ++t) {
+            v[t] = p.top_i[(int64_t)q * kCand + wave * PER + j0 + t];
+            w[t] = make_uint4(0, 0, 0, 0);
+            if (v[t] != INT_MAX && lane < p.chunks)
+                w[t] = p.codes[((int64_t)(v[t] >> 6) * p.chunks + lane) * 64 + (v[t] & 63)];
         }
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-        if (lane == 0) {
-            ex_s[j] = valid ? ldexpf((float)part * p.scales[v], -sh) : -INFINITY;
-            ex_i[j] = valid ? v : INT_MAX;
+        for (int t = 0; t < GRP; ++t) {
+            const bool valid = v[t] != INT_MAX;
+            int part = (valid && lane < p.chunks) ? nib_chunk(lut + lane * 2048, w[t]) : 0;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+            if (lane == 0) {
+                const int j = wave * PER + j0 + t;
+                ex_s[j] = valid ? ldexpf((float)part * p.scales[v[t]], -sh) : -INFINITY;
+                ex_i[j] = valid ? v[t] : INT_MAX;
+            }
         }
     }
     __syncthreads();
@@ -553,8 +561,11 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
 }
 
 // ------------------------------------------------------ fallback helpers
+// Global bounds are kept one 128-byte line apart (kBoundStride ints): every
+// wave of a query's selection reads and raises its query's bound, and bounds
+// of different queries sharing a line serialise each other.
 __global__ void fill_order_keys(int *p, int n) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = fkey(-INFINITY);
+    for (int i = threadIdx.x; i < n * kBoundStride; i += blockDim.x) p[i] = fkey(-INFINITY);
 }
 
 __global__ void gather_allow(const uint64_t *__restrict__ src, const int *__restrict__ rows, int nr,
@@ -630,7 +641,7 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
     L.top_i = o;
     o += align256((size_t)kTile * kCand * 4);
     L.gbound = o;
-    o += align256(kTile * 4);
+    o += align256(kTile * kBoundStride * 4);
     L.flags = o;
     o += align256((size_t)nq * 4);
     L.rows = o;
