@@ -531,8 +531,8 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
     if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
-        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, k <= 64 "
-                                     "and at most 4096 tenants");
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
+                                     "k <= 64 and at most 4096 tenants");
     tq_status st = device_ready();
     if (st != TQ_OK) return st;
     *bytes_out = search_bytes(shape_of(idx), nq, k, base);
@@ -558,8 +558,8 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (st != TQ_OK) return st;
     const ScanShape sh = shape_of(idx);
     if (base == TQ_PATH_MFMA && !mfma_search_supported(sh, k))
-        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, k <= 64 "
-                                     "and at most 4096 tenants");
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
+                                     "k <= 64 and at most 4096 tenants");
     const int grid = scan_grid();
     const size_t need = search_bytes(sh, nq, k, base);
     if (workspace_bytes < need)

@@ -38,7 +38,9 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
 constexpr int kCand = 256;         // candidates per query kept for exact rescoring
 constexpr int kCandS = kCand / 64;  // 64-entry slots of a candidate list
-constexpr int MF_THREADS = 512;    // 8 waves: two per SIMD, 256 registers each
+constexpr int MF_THREADS = 768;    // 12 waves: three per SIMD, 168 registers each
+constexpr int MF_RING = 8;         // chunk loads in flight per wave
+constexpr int kTableBytes = 256 * 32 * 4;   // byte table, 32 replicas
 constexpr int MF_WAVES = MF_THREADS / 64;
 constexpr int SEL_THREADS = 256;
 constexpr int SEL_GROUPS = 32;     // select workgroups per query
@@ -148,39 +150,44 @@ struct ScoreParams {
     int d, chunks, nqt;
 };
 
-// Float16 centroid of every 4-bit field of a stored word w (the canonical
-// word rotated left by 2): element t is coordinate t of the word.  T holds
-// the 16 centroids at a 4-byte stride.
-__device__ inline half8 dequant8(const char *__restrict__ T, uint32_t w) {
-    uint32_t lo = w & 0x3C3C3C3Cu;                                  // byte b: field 2b   times 4
-    uint32_t hi = __builtin_amdgcn_alignbit(w, w, 4) & 0x3C3C3C3Cu; // byte b: field 2b+1 times 4
-    asm volatile("" : "+v"(lo), "+v"(hi));
-    half8 r;
-    r[0] = *reinterpret_cast<const _Float16 *>(T + (lo & 0xFFu));
-    r[1] = *reinterpret_cast<const _Float16 *>(T + (hi & 0xFFu));
-    r[2] = *reinterpret_cast<const _Float16 *>(T + ((lo >> 8) & 0xFFu));
-    r[3] = *reinterpret_cast<const _Float16 *>(T + ((hi >> 8) & 0xFFu));
-    r[4] = *reinterpret_cast<const _Float16 *>(T + ((lo >> 16) & 0xFFu));
-    r[5] = *reinterpret_cast<const _Float16 *>(T + ((hi >> 16) & 0xFFu));
-    r[6] = *reinterpret_cast<const _Float16 *>(T + (lo >> 24));
-    r[7] = *reinterpret_cast<const _Float16 *>(T + (hi >> 24));
-    return r;
+// Float16 centroids of the 8 4-bit fields of a stored word w (the canonical
+// word rotated left by 2): element t is coordinate t of the word.  The byte
+// table holds, for every byte value e, the pair (c[e & 15], c[e >> 4]) as
+// two float16 -- one lookup per two coordinates.  It is replicated 32 times
+// so that lane i reads only LDS bank i mod 32 (entry e of replica i is the
+// 32-bit word e * 32 + i): lookups of random bytes by different lanes never
+// meet in a bank.  `lb` is the lane's byte offset (lane mod 32) * 4.
+__device__ inline half8 dequant8(uint32_t w, uint32_t lb) {
+    typedef __attribute__((address_space(3))) const uint32_t lds_u32;
+    const uint32_t cw = __builtin_amdgcn_alignbit(w, w, 2);   // canonical word
+    union {
+        uint32_t u[4];
+        half8 h;
+    } r;
+    r.u[0] = *(lds_u32 *)(uintptr_t)(((cw << 7) & 0x7F80u) | lb);
+    r.u[1] = *(lds_u32 *)(uintptr_t)(((cw >> 1) & 0x7F80u) | lb);
+    r.u[2] = *(lds_u32 *)(uintptr_t)(((cw >> 9) & 0x7F80u) | lb);
+    r.u[3] = *(lds_u32 *)(uintptr_t)(((cw >> 17) & 0x7F80u) | lb);
+    return r.h;
 }
 
-// One workgroup of 8 waves per compute unit.  The query tile (32 rows of d
-// float16, rows padded by 16 bytes so the 16 rows read by one instruction
-// fall in distinct banks) stays in LDS.  Waves claim the workgroup's
+// One workgroup of 12 waves per compute unit.  The byte table and the query
+// tile (32 rows of d float16, rows padded by 16 bytes so the 16 rows read by
+// one instruction fall in distinct banks) stay in LDS.  Waves claim the workgroup's
 // 64-vector blocks one at a time from an LDS counter (one ahead, so the ring
-// of 8 chunk loads runs on into the next block).  For a chunk, lane 16q+i
-// has loaded the 4 words of vector 16q+i; two rounds of lane-quarter swaps
-// give it word q of vectors i, 16+i, 32+i, 48+i -- the B operand (k = 8q..8q+7,
-// column i) of the four 16-vector MFMAs.
+// of MF_RING chunk loads runs on into the next block).  For a chunk, lane 16q+i
+// has loaded the 4 words of vector 16q+i; written to the wave's LDS slot and
+// read back as word q of vectors i, 16+i, 32+i, 48+i (bank-conflict free),
+// they are the B operands (k = 8q..8q+7, column i) of the four 16-vector
+// MFMAs.
 __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int ld = p.d + 8;                                   // row stride in halves
-    _Float16 *Qs = reinterpret_cast<_Float16 *>(smem);       // [kTile][ld]
-    char *T = smem + (size_t)kTile * ld * 2;                 // 16 x 4 bytes
-    int *ctr = reinterpret_cast<int *>(T + 64);
+    uint32_t *T = reinterpret_cast<uint32_t *>(smem);          // byte table x 32, at 0
+    _Float16 *Qs = reinterpret_cast<_Float16 *>(smem + kTableBytes);   // [kTile][ld]
+    int *ctr = reinterpret_cast<int *>(smem + kTableBytes + (size_t)kTile * ld * 2);
+    // per-wave staging slot of one chunk (64 lanes x 16 bytes)
+    char *stg = smem + kTableBytes + (size_t)kTile * ld * 2 + 16 + (threadIdx.x >> 6) * 1024;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -196,11 +203,13 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
         if (r < p.nqt) v = reinterpret_cast<const uint4 *>(p.q16 + (int64_t)r * p.d)[c8];
         *reinterpret_cast<uint4 *>(Qs + r * ld + c8 * 8) = v;
     }
-    if (tid < 16) {
-        const _Float16 c = (_Float16)p.cents[tid];
-        uint32_t bits = (uint32_t)__builtin_bit_cast(uint16_t, c);
-        reinterpret_cast<uint32_t *>(T)[tid] = bits;
+    for (int e = tid; e < 256 * 32; e += MF_THREADS) {
+        const int v = e >> 5;   // byte value; e & 31 is the replica
+        const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v & 15]);
+        const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v >> 4]);
+        T[e] = lo | (hi << 16);
     }
+    const uint32_t lb = (uint32_t)(lane & 31) * 4;
     if (tid == 0) *ctr = 0;
     // per-lane query factors: tile t, rows 4*(lane/16) + r
     float qf[2][4];
@@ -209,7 +218,8 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int q = 16 * t + 4 * (lane >> 4) + r;
-            qf[t][r] = q < p.nqt ? p.info[q].f : 0.f;
+            const float f = p.info[q < p.nqt ? q : 0].f;
+            qf[t][r] = q < p.nqt ? f : 0.f;
         }
     __syncthreads();
 
@@ -222,12 +232,20 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
     if (cur >= nbw) return;
     int nxt = __builtin_amdgcn_readfirstlane(take());
     const uint4 *bsrc = p.codes + (gb0 + cur) * CH * 64;
-    uint4 buf[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        buf[i] = (bsrc + i * 64)[lane];
-        __builtin_amdgcn_sched_barrier(kKeepVmemB);
-    }
+    // the ring: named registers (an array would end up in scratch)
+    uint4 rb0, rb1, rb2, rb3, rb4, rb5, rb6, rb7;
+#define TQ_RING_LOAD(R, I)                          \
+    R = (bsrc + (I) * 64)[lane];                    \
+    __builtin_amdgcn_sched_barrier(kKeepVmemB);
+    TQ_RING_LOAD(rb0, 0)
+    TQ_RING_LOAD(rb1, 1)
+    TQ_RING_LOAD(rb2, 2)
+    TQ_RING_LOAD(rb3, 3)
+    TQ_RING_LOAD(rb4, 4)
+    TQ_RING_LOAD(rb5, 5)
+    TQ_RING_LOAD(rb6, 6)
+    TQ_RING_LOAD(rb7, 7)
+#undef TQ_RING_LOAD
     const int qrow = lane & 15, kq = lane >> 4;
     const _Float16 *qa0 = Qs + qrow * ld + kq * 8;
     const _Float16 *qa1 = Qs + (16 + qrow) * ld + kq * 8;
@@ -236,47 +254,51 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
         // the block after this one (or this one again past the end: cache hits)
         const uint4 *nsrc = nxt < nbw ? p.codes + (gb0 + nxt) * CH * 64 : bsrc;
         const int ticket = take();
+        // unconditional loads (clamped index): a load under a branch makes the
+        // wait-count pass drain the chunk ring in the loop below
         float scl[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int64_t v = blk * 64 + 16 * m + qrow;
-            scl[m] = v < p.n ? p.scales[v] : 0.f;
+            scl[m] = p.scales[v < p.n ? v : 0];
         }
         float4v acc[2][4];
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
             for (int m = 0; m < 4; ++m) acc[t][m] = float4v{0.f, 0.f, 0.f, 0.f};
-        for (int c0 = 0; c0 < CH; c0 += 8) {
+        // one chunk; the ring index is a compile-time constant at every call
+        auto chunk = [&](const int c, uint4 &slot) {
+            // the chunk goes through the wave's staging slot and comes back
+            // transposed (LDS runs a wave's operations in order)
+            *reinterpret_cast<uint4 *>(stg + lane * 16) = slot;
+            // refill MF_RING chunks ahead: this block, then the next one
+            const int nc = c + MF_RING;
+            slot = (nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64)[lane];
+            __builtin_amdgcn_sched_barrier(kKeepVmemB);
+            uint32_t r[4];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int c = c0 + i;
-                uint32_t r[4] = {buf[i].x, buf[i].y, buf[i].z, buf[i].w};
-                // refill 8 chunks ahead: this block, then the next one
-                const int nc = c + 8;
-                buf[i] = (nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64)[lane];
-                __builtin_amdgcn_sched_barrier(kKeepVmemB);
-                const auto s02 = __builtin_amdgcn_permlane32_swap(r[0], r[2], false, false);
-                const auto s13 = __builtin_amdgcn_permlane32_swap(r[1], r[3], false, false);
-                r[0] = s02[0];
-                r[2] = s02[1];
-                r[1] = s13[0];
-                r[3] = s13[1];
-                const auto s01 = __builtin_amdgcn_permlane16_swap(r[0], r[1], false, false);
-                const auto s23 = __builtin_amdgcn_permlane16_swap(r[2], r[3], false, false);
-                r[0] = s01[0];
-                r[1] = s01[1];
-                r[2] = s23[0];
-                r[3] = s23[1];
-                const half8 a0 = *reinterpret_cast<const half8 *>(qa0 + c * 32);
-                const half8 a1 = *reinterpret_cast<const half8 *>(qa1 + c * 32);
+            for (int m = 0; m < 4; ++m)
+                r[m] = *reinterpret_cast<const uint32_t *>(stg + (16 * m + qrow) * 16 + kq * 4);
+            const half8 a0 = *reinterpret_cast<const half8 *>(qa0 + c * 32);
+            const half8 a1 = *reinterpret_cast<const half8 *>(qa1 + c * 32);
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const half8 b = dequant8(T, r[m]);
-                    acc[0][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, b, acc[0][m], 0, 0, 0);
-                    acc[1][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, b, acc[1][m], 0, 0, 0);
-                }
+            for (int m = 0; m < 4; ++m) {
+                const half8 b = dequant8(r[m], lb);
+                acc[0][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, b, acc[0][m], 0, 0, 0);
+                acc[1][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, b, acc[1][m], 0, 0, 0);
             }
+        };
+        static_assert(MF_RING == 8, "the chunk calls below assume a ring of 8");
+        for (int c0 = 0; c0 < CH; c0 += MF_RING) {
+            chunk(c0 + 0, rb0);
+            chunk(c0 + 1, rb1);
+            chunk(c0 + 2, rb2);
+            chunk(c0 + 3, rb3);
+            chunk(c0 + 4, rb4);
+            chunk(c0 + 5, rb5);
+            chunk(c0 + 6, rb6);
+            chunk(c0 + 7, rb7);
         }
         // lane holds vectors 16m + qrow, queries 16t + 4*kq + r
 #pragma unroll
@@ -662,8 +684,14 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
 
 }  // namespace
 
+// LDS of the score kernel: replicated byte table, query tile, staging.
+size_t score_lds_bytes(int d) {
+    return kTableBytes + (size_t)kTile * (d + 8) * 2 + 16 + MF_WAVES * 1024;
+}
+
 bool mfma_search_supported(const ScanShape &s, int k) {
-    return s.bits == 4 && s.chunks % 8 == 0 && k <= 64 && s.W <= 64;
+    return s.bits == 4 && s.chunks % 8 == 0 && k <= 64 && s.W <= 64 &&
+           score_lds_bytes(s.d) <= 160 * 1024;
 }
 
 size_t mfma_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid) {
@@ -697,7 +725,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     int *gbound = reinterpret_cast<int *>(w8 + L.gbound);
     int *flags = reinterpret_cast<int *>(w8 + L.flags);
     const int64_t npad = approx_row(s);
-    const size_t lds_scores = (size_t)kTile * (s.d + 8) * 2 + 64 + 16;
+    const size_t lds_scores = score_lds_bytes(s.d);
     const size_t lds_rescore = (size_t)s.chunks * 2048 + (16 + 2 * kCand) * 4;
     static bool attr_set = false;
     if (!attr_set) {

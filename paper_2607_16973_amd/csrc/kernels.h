@@ -86,7 +86,8 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
                       int64_t *ids, float *scores, hipStream_t stream);
 
 // Batched search of a tile of queries on the matrix cores with exact
-// rescoring (b = 4, chunks % 8 == 0, k <= 64, at most 4096 tenants).
+// rescoring (b = 4, chunks % 8 == 0, d <= 1536, k <= 64, at most 4096
+// tenants).
 // cmax16 = max |float16(c_l)|, dmax = max |float16(c_l) - c_l| over the
 // float32 centroids cents32.
 // Queries whose top k the certificate does not prove are re-run on the
