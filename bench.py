@@ -65,6 +65,95 @@ def measured_traffic(queries_per_launch: int):
     return float(m.group(3)) + float(m.group(4))
 
 
+def timed(fn, reps=3):
+    """Mean wall time of fn() over reps calls after one warm-up call."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / reps
+
+
+def batched_path(tq, idx, Qrot, k, lut_ids, lut_scores, ex_ids, nr):
+    """The matrix-core path on the same queries: throughput, certificate
+    fallbacks, and agreement with the single-query path."""
+    import numpy as np
+    import torch
+    nq = Qrot.shape[0]
+    bi, bs = torch.empty_like(lut_ids), torch.empty_like(lut_scores)
+    t = timed(lambda: idx.search(Qrot, k, path="mfma", ids=bi, scores=bs, prerotated=True))
+    fb = tq.last_search_fallbacks()
+    same = bool(torch.equal(torch.sort(bs, dim=1).values, torch.sort(lut_scores, dim=1).values))
+    got = bi[:nr].cpu().numpy()
+    rec = float(np.mean([len(set(a) & set(b)) / k for a, b in zip(got, ex_ids)]))
+    log("batched path: %.0f queries/s, %d fallbacks, same scores as LUT: %s" % (nq / t, fb, same))
+    return {"queries_per_s": nq / t, "ms_per_step": t * 1e3, "queries_per_step": nq,
+            "certificate_fallbacks": fb, "same_scores_as_single_query_path": same,
+            "recall_at_k_vs_exact_fp32": rec}
+
+
+def filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev, T=100):
+    """Multi-tenant search: Zipf(1.1) tenants over T at random positions,
+    selective (one tenant) and broad (T/10 tenants) allowlists, single-query
+    path with block skipping.  GB/s counts the bytes the method must read:
+    codes, scale and tenant id of every vector in a block whose summary meets
+    the allowlist, plus every block summary."""
+    import numpy as np
+    import torch
+    nq = Qrot.shape[0]
+    ten = synth.zipf_tenants(n, T, seed=44)
+    idx_f = tq.Index(cb, rot, n_tenants=T)
+    idx_f.reserve(n)
+    idx_f.add(X, torch.from_numpy(ten.view(np.int16)).to(dev))
+    W = idx_f.words
+    nblk = (n + 63) // 64
+    summ = np.zeros((nblk, W), dtype=np.uint64)
+    np.bitwise_or.at(summ, (np.arange(n) // 64, ten.astype(np.int64) >> 6),
+                     np.left_shift(np.uint64(1), (ten.astype(np.uint64) & np.uint64(63))))
+    out = {"tenants": T}
+    for mode in ("selective", "broad"):
+        bm = synth.allowlist_bitmap(synth.allowlists(nq, T, mode, seed=45), T)
+        allow = torch.from_numpy(bm.view(np.int64)).to(dev)
+        t = timed(lambda: idx_f.search(Qrot, k, allow=allow, path="lut", prerotated=True))
+        scanned = sum(int(np.count_nonzero((summ & bm[q]).any(axis=1))) for q in range(nq))
+        alg = scanned * 64 * (d * bits // 8 + 4 + 2) + nq * nblk * W * 8
+        out[mode] = {"queries_per_s": nq / t, "blocks_scanned_fraction": scanned / (nq * nblk),
+                     "achieved_GBps": alg / t / 1e9}
+        log("filtered %s: %.0f queries/s, %.3f of blocks scanned, %.0f GB/s"
+            % (mode, nq / t, scanned / (nq * nblk), alg / t / 1e9))
+    return out
+
+
+def bit_sweep(tq, rot, X, Qrot, k, n, d, stream):
+    """Encode throughput (rotation GEMM + quantise + pack) and single-query
+    search throughput at each bit width."""
+    import torch
+    out = {}
+    for b in (2, 3, 4, 8):
+        cbb = tq.Codebook(d, b)
+        ib = tq.Index(cbb, rot, n_tenants=1)
+        ib.reserve(n)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ib.add(X)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_enc = e0.elapsed_time(e1) / 1e3
+        q = Qrot if b != 8 else Qrot[:200].contiguous()
+        t = timed(lambda: ib.search(q, k, path="lut", prerotated=True), reps=2)
+        bpq = n * (d * b // 8 + 4)
+        out["b%d" % b] = {"encode_vectors_per_s": n / t_enc, "queries_per_s": q.shape[0] / t,
+                          "achieved_GBps": bpq * q.shape[0] / t / 1e9}
+        log("b=%d: encode %.3g vectors/s, search %.0f queries/s, %.0f GB/s"
+            % (b, n / t_enc, q.shape[0] / t, bpq * q.shape[0] / t / 1e9))
+        del ib
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(X, Q, d, bits, k, n_full, sample_rows=131072, sample_queries=256):
     """The oracle as it stands, on a bounded sample, scaled to N = n_full."""
     import numpy as np
@@ -101,6 +190,8 @@ def main() -> int:
     ap.add_argument("--k", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip recall / latency extras")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also encode the corpus and search at b = 2, 3, 4, 8 bits")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run three 1 GiB device-to-device copies (a kernel of "
                          "known traffic for scaling the HBM byte counters)")
@@ -223,6 +314,10 @@ def main() -> int:
                 lat.append(a.elapsed_time(b))
         extra["single_query_latency_ms_p50"] = float(np.median(lat))
         log("recall@%d %.4f  single-query latency %.3f ms" % (k, rec, extra["single_query_latency_ms_p50"]))
+        extra["batched_mfma"] = batched_path(tq, idx, Qrot, k, ids, scores, ex_ids, nr)
+        extra["filtered_T100"] = filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev)
+    if args.sweep:
+        extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
     del X
     torch.cuda.empty_cache()
     if args.copy_calibration:
