@@ -52,8 +52,10 @@ __host__ __device__ inline bool blocked_rotated(int bits) { return bits == 1 || 
 __host__ __device__ inline uint32_t rotl2(uint32_t w) { return (w << 2) | (w >> 30); }
 __host__ __device__ inline uint32_t rotr2(uint32_t w) { return (w >> 2) | (w << 30); }
 inline int chunks_per_vector(int d, int bits) {
-    // 3-bit codes are stored 10 per 32-bit word (2 pad bits per word)
-    if (bits == 3) return (((d + 9) / 10) + 3) / 4;
+    // 3-bit codes are stored 10 per 32-bit word (2 pad bits per word), in a
+    // whole number of 4-chunk groups (zero codes past d) so the scan can keep
+    // at least 4 chunk loads in flight
+    if (bits == 3) return ((((d + 9) / 10) + 3) / 4 + 3) / 4 * 4;
     return d * bits / 128;
 }
 

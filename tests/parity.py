@@ -52,3 +52,44 @@ def check_topk(gpu_ids, gpu_scores, codes, scales, cents, qrot, qnorms, k,
         if not np.array_equal(v, ref_ids[b][:nv]):
             differ += 1
     return differ
+
+
+def check_topk_sampled(gpu_ids, gpu_scores, X, R32, cb, Q, k, sample, allowed=None):
+    """Validity of GPU top-k lists over a corpus too large for the oracle's
+    full search.  The oracle encodes the returned vectors and a random sample
+    of the corpus from the float rows X; then every returned score must match
+    the oracle's score for its id, the lists must be ordered, distinct,
+    allowed and full, and no sampled vector outside a list may beat its worst
+    entry by more than the tolerance.  `allowed`: boolean mask over the
+    corpus per query, or None."""
+    gpu_ids = np.asarray(gpu_ids)
+    gpu_scores = np.asarray(gpu_scores, dtype=np.float64)
+    n = X.shape[0]
+    rows = np.unique(np.concatenate([gpu_ids[gpu_ids >= 0].ravel(), np.asarray(sample)]))
+    codes, _, scales = oracle.encode(np.ascontiguousarray(X[rows]), R32, cb)
+    pos = {int(r): i for i, r in enumerate(rows)}
+    qrot = oracle.rotate_queries(R32, Q)
+    qn = np.linalg.norm(Q.astype(np.float64), axis=1)
+    for b in range(gpu_ids.shape[0]):
+        ids = gpu_ids[b]
+        mask = None if allowed is None else allowed[b]
+        n_allowed = n if mask is None else int(mask.sum())
+        nv = int((ids >= 0).sum())
+        assert nv == min(k, n_allowed), (b, nv)
+        assert np.all(ids[:nv] >= 0) and np.all(ids[nv:] == -1)
+        v = ids[:nv]
+        assert len(set(v.tolist())) == nv, "duplicate ids"
+        if mask is not None:
+            assert np.all(mask[v]), "disallowed id returned"
+        ref = oracle.scores_for_ids(codes, scales, cb.cents, qrot[b], [pos[int(i)] for i in v])
+        tol = score_tol(ref, qn[b])
+        assert np.all(np.abs(gpu_scores[b][:nv] - ref) <= tol), (b, float((np.abs(gpu_scores[b][:nv] - ref) / tol).max()))
+        assert np.all(np.diff(ref) <= 2 * tol[1:] + 1e-12), "not ordered"
+        s = np.setdiff1d(np.asarray(sample), v)
+        if mask is not None:
+            s = s[mask[s]]
+        if s.size and nv == k:
+            others = oracle.scores_for_ids(codes, scales, cb.cents, qrot[b], [pos[int(i)] for i in s])
+            worst = ref.min()
+            assert others.max() <= worst + score_tol(np.array([worst]), qn[b])[0], \
+                (b, float(others.max()), float(worst))
