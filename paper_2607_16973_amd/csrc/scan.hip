@@ -543,6 +543,186 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
     }
 }
 
+// Filtered scan for b in {1, 2, 4}: as split_scan_kernel, over the blocks
+// whose tenant summary meets the query's allowlist only.  At the start of a
+// query the workgroup lists those of its blocks (by summary & allowlist, in
+// windows of kListMax blocks; no code byte of a skipped block is read), then
+// waves claim 8-chunk groups of the listed blocks in passes of up to 64
+// blocks; the wave that completes a block drops vectors whose tenant is not
+// allowed and offers the rest to its top-k.  (The listing order is not
+// fixed; the result does not depend on it.)
+constexpr int kListMax = 4096;
+
+template <int S>
+__global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams p) {
+    extern __shared__ __attribute__((aligned(16))) float lds[];
+    const int aux = aux_words(p.lut_words, S);
+    int *accb = reinterpret_cast<int *>(lds + aux);   // [kPassBlocks][64] block sums
+    int *done = accb + kPassBlocks * 64;              // [kPassBlocks] finished groups
+    // [0] bound key, [1] and [3] group counters (alternate passes), [2] survivors
+    int *misc = done + kPassBlocks;
+    float *red = reinterpret_cast<float *>(misc + 4); // 16 wave sums of |q'|
+    float *cents_s = red + 16;                        // 16 levels
+    float *surv_s = cents_s + 16;                     // 64 survivors
+    int *surv_i = reinterpret_cast<int *>(surv_s + 64);
+    int *nlist = surv_i + 64;                         // listed blocks of the window
+    int *list = nlist + 4;                            // [kListMax] block offsets in the window
+    uint64_t *allow_s = reinterpret_cast<uint64_t *>(list + kListMax);   // [W]
+    float *stage_s = lds;
+    int *stage_i = reinterpret_cast<int *>(lds + SCAN_WAVES * 64 * S);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = gridDim.x;
+    const int g = blockIdx.x;
+    const int CH = p.chunks;          // multiple of 8
+    const int GPB = CH >> 3;          // 8-chunk groups per block
+    const int W = p.W;
+    const int64_t gb0 = p.nblk * g / G, gb1 = p.nblk * (g + 1) / G;
+    const char *lut = reinterpret_cast<const char *>(lds);
+    auto take = [&](int *ctr) {
+        int v = 0;
+        if (lane == 0) v = atomicAdd(ctr, 1);
+        return v;
+    };
+
+    for (int e = tid; e < kPassBlocks * 65; e += SCAN_THREADS) accb[e] = 0;   // sums and counts
+    if (tid < 16) cents_s[tid] = p.cents[tid];
+    if (tid == 0) {
+        misc[0] = fkey(-INFINITY);
+        misc[1] = 0;
+        misc[2] = 0;
+        misc[3] = 0;
+    }
+    if (p.nq == 0) return;
+    for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[w];
+    float qv[2][4];
+    load_nibble_query(table_shape(p), p.qrot, qv);
+    nibble_abs_sum(red, qv);
+    __syncthreads();
+    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+    __syncthreads();
+    for (int qi = 0; qi < p.nq; ++qi) {
+        WaveTopK<S> top;
+        top.reset();
+        int pass = 0;
+        for (int64_t w0 = gb0; w0 < gb1; w0 += kListMax) {
+            const int wn = (int)(gb1 - w0 < kListMax ? gb1 - w0 : kListMax);
+            if (w0 > gb0) __syncthreads();   // the previous window's list is no longer read
+            if (tid == 0) *nlist = 0;
+            __syncthreads();
+            for (int t = tid; t < wn; t += SCAN_THREADS) {
+                const uint64_t *sm = p.summaries + (w0 + t) * W;
+                bool hit = false;
+                for (int w = 0; w < W; ++w) hit |= (sm[w] & allow_s[w]) != 0;
+                if (hit) list[atomicAdd(nlist, 1)] = t;
+            }
+            __syncthreads();
+            const int nl = *nlist;
+            for (int l0 = 0; l0 < nl; l0 += kPassBlocks, ++pass) {
+                if (l0 > 0) __syncthreads();   // the previous pass's slots are free again
+                int *ctr = misc + 1 + 2 * (pass & 1);
+                if (tid == 0) misc[1 + 2 * ((pass + 1) & 1)] = 0;   // the next pass's counter
+                const int nb = nl - l0 < kPassBlocks ? nl - l0 : kPassBlocks;
+                const int ng = nb * GPB;
+                // address of group u of this pass (wave-uniform)
+                auto group_src = [&](int u) {
+                    const int bl = u / GPB;
+                    const int64_t blk = w0 + list[l0 + bl];
+                    return p.codes + (blk * CH + (int64_t)(u - bl * GPB) * 8) * 64;
+                };
+                int cur = __builtin_amdgcn_readfirstlane(take(ctr));
+                if (cur < ng) {
+                    int nxt = __builtin_amdgcn_readfirstlane(take(ctr));
+                    const uint4 *csrc = group_src(cur);
+                    uint4 buf[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        buf[i] = (csrc + i * 64)[lane];
+                        __builtin_amdgcn_sched_barrier(kKeepVmem);
+                    }
+                    while (true) {
+                        const int bl = cur / GPB;
+                        const int c0 = (cur - bl * GPB) * 8;
+                        const int64_t blk = w0 + list[l0 + bl];
+                        const int64_t vid = blk * 64 + lane;
+                        const bool inside = vid < p.n;
+                        const bool last = c0 == CH - 8;
+                        float scl = 0.f;
+                        int ten = 0, gk = 0;
+                        if (last) {
+                            scl = p.scales[inside ? vid : 0];
+                            ten = p.tenants[inside ? vid : 0];
+                            gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                        const uint4 *nsrc = nxt < ng ? group_src(nxt) : csrc;
+                        const int ticket = take(ctr);
+                        const char *Lb = lut + c0 * 2048;
+                        int acc = 0;
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            acc += nib_chunk(Lb + i * 2048, buf[i]);
+                            buf[i] = (nsrc + i * 64)[lane];
+                            __builtin_amdgcn_sched_barrier(kKeepVmem);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                        const int nxt2 = __builtin_amdgcn_readfirstlane(ticket);
+                        atomicAdd(&accb[bl * 64 + lane], acc);
+                        const int fin = __builtin_amdgcn_readfirstlane(take(done + bl));
+                        if (fin == GPB - 1) {
+                            if (!last) {
+                                scl = p.scales[inside ? vid : 0];
+                                ten = p.tenants[inside ? vid : 0];
+                                gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT);
+                            }
+                            const int sum = accb[bl * 64 + lane];
+                            accb[bl * 64 + lane] = 0;
+                            if (lane == 0) done[bl] = 0;
+                            const bool ok = inside && ((allow_s[ten >> 6] >> (ten & 63)) & 1ull);
+                            const float sc = ldexpf((float)sum * scl, -sh);
+                            top.offer_seen(ok ? sc : -INFINITY, ok ? (int)vid : INT_MAX, lane, p.k,
+                                           misc, p.gbound + qi, gk);
+                        }
+                        if (nxt >= ng) break;
+                        cur = nxt;
+                        nxt = nxt2;
+                        csrc = nsrc;
+                    }
+                }
+            }
+        }
+        const bool more = qi + 1 < p.nq;
+        if (more) {
+            load_nibble_query(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
+            nibble_abs_sum(red, qv);
+        }
+        __syncthreads();   // scan done: every offer made, the bound key final
+        const int64_t out = ((int64_t)qi * G + g) * p.k;
+        collect_survivors<S>(top, misc[0], surv_s, surv_i, misc + 2, lane);
+        __syncthreads();
+        const int ns = misc[2];
+        if (ns <= 64) {
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
+        } else {
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
+        }
+        if (more) {
+            sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+            for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)(qi + 1) * W + w];
+        }
+        if (tid == 0) {
+            misc[0] = fkey(-INFINITY);
+            misc[1] = 0;
+            misc[3] = 0;
+        }
+        __syncthreads();   // table and allowlist ready; survivor count read by every wave
+        if (tid == 0) misc[2] = 0;
+    }
+}
+
 template <int S>
 __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs,
                                                     const int *__restrict__ ci, int G, int k,
@@ -607,16 +787,20 @@ int lut_words_for(const ScanShape &s) {
     return s.chunks * 32 * 16;
 }
 
-// The split scan serves unfiltered searches over 1-, 2- and 4-bit codes
-// whose chunk count is a multiple of its 8-chunk groups.
-bool use_split(const ScanShape &s, bool filtered) {
-    return !filtered && (s.bits == 1 || s.bits == 2 || s.bits == 4) && s.chunks % 8 == 0;
+// The split scans serve searches over 1-, 2- and 4-bit codes whose chunk
+// count is a multiple of their 8-chunk groups, unfiltered or filtered.
+bool use_split(const ScanShape &s) {
+    return (s.bits == 1 || s.bits == 2 || s.bits == 4) && s.chunks % 8 == 0;
 }
 
-size_t lds_bytes_for(const ScanShape &s, int S, bool split) {
-    // split: block sums and counts, misc, |q'| sums, levels, 64 survivors
-    const size_t fixed = split ? (size_t)kPassBlocks * 65 * 4 + 16 + 64 + 64 + 512
-                               : (size_t)s.W * 8 + 16 + 64;
+size_t lds_bytes_for(const ScanShape &s, int S, bool split, bool filtered) {
+    // split: block sums and counts, misc, |q'| sums, levels, 64 survivors;
+    // filtered split: also the block list and the allowlist
+    size_t fixed = (size_t)s.W * 8 + 16 + 64;
+    if (split) {
+        fixed = (size_t)kPassBlocks * 65 * 4 + 16 + 64 + 64 + 512;
+        if (filtered) fixed += 16 + (size_t)kListMax * 4 + (size_t)s.W * 8;
+    }
     return (size_t)aux_words(lut_words_for(s), S) * 4 + fixed;
 }
 
@@ -661,10 +845,16 @@ hipError_t launch_split(const ScanParams &p, int grid, size_t lds, hipStream_t s
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)split_scan_kernel<S>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)split_filtered_kernel<S>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL(split_scan_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+    if (p.allow)
+        hipLaunchKernelGGL(split_filtered_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+    else
+        hipLaunchKernelGGL(split_scan_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
     return hipGetLastError();
 }
 
@@ -734,8 +924,8 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.k = k;
         p.nq = (int)m;
         p.lut_words = lut_words_for(s);
-        const bool split = use_split(s, allow != nullptr);
-        const size_t lds = lds_bytes_for(s, S, split);
+        const bool split = use_split(s) && lds_bytes_for(s, S, true, allow != nullptr) <= 160 * 1024;
+        const size_t lds = lds_bytes_for(s, S, split, allow != nullptr);
         hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
                            (int)(0x807FFFFFu));   // order key of -inf
         hipError_t e = hipGetLastError();
