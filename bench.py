@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 # rocprofv3 summary of the scan kernel at this workload; it carries the HBM
 # counter readings and a hash of the kernel sources they were taken on
 SCAN_PROFILE = os.path.join(ROOT, "profiles", "scan_lut_d1536_n1m_k10.md")
-SCAN_SOURCES = ("scan.hip", "lut.h", "topk.h", "kernels.h")
+SCAN_SOURCES = ("scan.hip", "lut.h", "topk.h", "stream.h", "kernels.h")
 METRIC = "queries/sec and achieved HBM GB/s, 4-bit scan, d=1536, N=1M, k=10 (1 GPU)"
 
 

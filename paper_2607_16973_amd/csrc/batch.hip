@@ -27,6 +27,7 @@
 
 #include "kernels.h"
 #include "lut.h"
+#include "stream.h"
 #include "topk.h"
 
 namespace tq {
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
     // the ring: named registers (an array would end up in scratch)
     uint4 rb0, rb1, rb2, rb3, rb4, rb5, rb6, rb7;
 #define TQ_RING_LOAD(R, I)                          \
-    R = (bsrc + (I) * 64)[lane];                    \
+    R = load_stream(bsrc + (I) * 64 + lane);        \
     __builtin_amdgcn_sched_barrier(kKeepVmemB);
     TQ_RING_LOAD(rb0, 0)
     TQ_RING_LOAD(rb1, 1)
@@ -274,7 +275,7 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
             *reinterpret_cast<uint4 *>(stg + lane * 16) = slot;
             // refill MF_RING chunks ahead: this block, then the next one
             const int nc = c + MF_RING;
-            slot = (nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64)[lane];
+            slot = load_stream((nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64) + lane);
             __builtin_amdgcn_sched_barrier(kKeepVmemB);
             uint32_t r[4];
 #pragma unroll

@@ -26,6 +26,7 @@
 
 #include "kernels.h"
 #include "lut.h"
+#include "stream.h"
 #include "topk.h"
 
 namespace tq {
@@ -316,7 +317,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
             uint4 buf[PF];
 #pragma unroll
             for (int i = 0; i < PF; ++i) {
-                buf[i] = (src + (int64_t)(i < F ? i : F - 1) * 64)[lane];
+                buf[i] = load_stream(src + (int64_t)(i < F ? i : F - 1) * 64 + lane);
                 __builtin_amdgcn_sched_barrier(kKeepVmem);
             }
             int64_t f = 0;
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                         // chunk of this block again: a cache hit, no HBM traffic
                         const int64_t nf = f + c0 + i + PF;
                         const uint4 *nsrc = nf < F ? src + nf * 64 : bsrc;
-                        buf[i] = nsrc[lane];
+                        buf[i] = load_stream(nsrc + lane);
                         __builtin_amdgcn_sched_barrier(kKeepVmem);
                     }
                 }
@@ -450,7 +451,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
     if (tk < total) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            buf[i] = (csrc + i * 64)[lane];
+            buf[i] = load_stream(csrc + i * 64 + lane);
             __builtin_amdgcn_sched_barrier(kKeepVmem);
         }
     }
@@ -492,7 +493,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
                 for (int i = 0; i < 8; ++i) {
                     // consume buf[i], then refill it with the next group
                     acc += nib_chunk(Lb + i * 2048, buf[i]);
-                    buf[i] = (nsrc + i * 64)[lane];
+                    buf[i] = load_stream(nsrc + i * 64 + lane);
                     __builtin_amdgcn_sched_barrier(kKeepVmem);
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -639,7 +640,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                     uint4 buf[8];
 #pragma unroll
                     for (int i = 0; i < 8; ++i) {
-                        buf[i] = (csrc + i * 64)[lane];
+                        buf[i] = load_stream(csrc + i * 64 + lane);
                         __builtin_amdgcn_sched_barrier(kKeepVmem);
                     }
                     while (true) {
@@ -664,7 +665,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
 #pragma unroll
                         for (int i = 0; i < 8; ++i) {
                             acc += nib_chunk(Lb + i * 2048, buf[i]);
-                            buf[i] = (nsrc + i * 64)[lane];
+                            buf[i] = load_stream(nsrc + i * 64 + lane);
                             __builtin_amdgcn_sched_barrier(kKeepVmem);
                         }
                         __builtin_amdgcn_sched_barrier(0);
