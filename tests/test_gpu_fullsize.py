@@ -71,6 +71,15 @@ def test_search_full_size(big, path):
         assert torch.equal(torch.sort(sc, 1).values, torch.sort(ls, 1).values)
 
 
+def test_top64_of_k64_and_k65_agree_full_size(big):
+    """k = 64 keeps one 64-entry slot per wave list, k = 65 two; both sum the
+    same integer table entries, so the leading 64 entries agree exactly."""
+    print("search N=%d k=64 and k=65" % N, flush=True)
+    a_i, a_s = big.idx.search(big.Qrot, 64, path="lut", prerotated=True)
+    b_i, b_s = big.idx.search(big.Qrot, 65, path="lut", prerotated=True)
+    assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
+
+
 def test_filtered_full_size(big):
     T = 100
     ten = synth.zipf_tenants(N, T, seed=44)

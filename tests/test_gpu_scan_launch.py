@@ -1,0 +1,81 @@
+"""GPU parity of the single-query scan (section II-B step 5, section III-B)
+across launch shapes: many queries in one launch (the scan keeps per-query
+state across its query loop), results that must not depend on the other
+queries of a launch, four dimensions and three bit widths with 1 to 6
+eight-chunk groups per vector, and exact agreement between the top-64 lists
+of k = 64 and k = 65 (wave lists of one and of two 64-entry slots; both sum
+the same integer table entries)."""
+import numpy as np
+import pytest
+
+import oracle
+from tests.conftest import gpu_available
+from tests.parity import check_topk
+
+pytestmark = pytest.mark.gpu
+if not gpu_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import torch  # noqa: E402
+
+import paper_2607_16973_amd as tq  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def env(small_env):
+    return small_env
+
+
+def test_many_queries_per_launch(env):
+    print("scan: 300 queries in one launch", flush=True)
+    rng = np.random.default_rng(51)
+    noisy = [env.Q + np.float32(0.01) * rng.standard_normal(env.Q.shape).astype(np.float32)
+             for _ in range(4)]
+    Q = np.ascontiguousarray(np.concatenate([env.Q] + noisy)[:300])
+    Qd = torch.from_numpy(Q).cuda()
+    ids, sc = env.idx.search(Qd, 10)
+    ref_i, ref_s = oracle.search(env.codes, env.scales, env.ocb.cents, env.R32, Q, 10)
+    qrot = oracle.rotate_queries(env.R32, Q)
+    qn = np.linalg.norm(Q.astype(np.float64), axis=1)
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents, qrot,
+               qn, 10, ref_i, ref_s)
+    # a query's result does not depend on the other queries of its launch
+    for lo, hi in [(0, 1), (0, 2), (1, 4), (150, 153), (299, 300)]:
+        a_i, a_s = env.idx.search(Qd[lo:hi].contiguous(), 10)
+        assert torch.equal(a_i, ids[lo:hi]) and torch.equal(a_s, sc[lo:hi]), (lo, hi)
+
+
+def test_top64_of_k64_and_k65_agree(env):
+    a_i, a_s = env.idx.search(env.Qd, 64)
+    b_i, b_s = env.idx.search(env.Qd, 65)
+    assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
+
+
+# (d, b): code chunks per vector d*b/128, eight-chunk groups chunks/8
+@pytest.mark.parametrize("d,bits", [(256, 4), (1024, 4), (1280, 4), (512, 2), (1024, 1)])
+def test_other_dimensions(d, bits):
+    print("scan d=%d b=%d" % (d, bits), flush=True)
+    rng = np.random.default_rng(d + bits)
+    n, nq = 3013, 24
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    Q = (X[:nq] + np.float32(0.05) * rng.standard_normal((nq, d)).astype(np.float32))
+    Q = np.ascontiguousarray(Q.astype(np.float32))
+    rot = tq.Rotation(d, 11)
+    R32 = rot.matrix()
+    ocb = oracle.lloyd_max(d, bits)
+    codes, _, scales = oracle.encode(X, R32, ocb)
+    idx = tq.Index(tq.Codebook(d, bits), rot, n_tenants=1)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
+                  torch.from_numpy(scales).cuda())
+    Qd = torch.from_numpy(Q).cuda()
+    qrot = oracle.rotate_queries(R32, Q)
+    qn = np.linalg.norm(Q.astype(np.float64), axis=1)
+    for k in (10, 64):
+        ids, sc = idx.search(Qd, k)
+        ref_i, ref_s = oracle.search(codes, scales, ocb.cents, R32, Q, k)
+        check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, qrot, qn, k,
+                   ref_i, ref_s)
+    a_i, a_s = idx.search(Qd, 64)
+    b_i, b_s = idx.search(Qd, 65)
+    assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
