@@ -301,6 +301,16 @@ def main() -> int:
         rec = float(np.mean([len(set(a) & set(b)) / k for a, b in zip(got, ex_ids)]))
         extra["recall_at_k_vs_exact_fp32"] = rec
         del g
+        # Hit@k and MRR@20 (section IV-E): rank of the exact top-1 in the top 20
+        i20, _ = idx.search(Qrot[:nr].contiguous(), 20, path="lut", prerotated=True)
+        a20 = i20.cpu().numpy()
+        ranks = np.array([(np.nonzero(a == t)[0][:1] + 1).tolist()[0] if np.any(a == t) else 0
+                          for a, t in zip(a20, ex_ids[:, 0])])
+        hit = {"hit_at_%d" % h: float(np.mean((ranks > 0) & (ranks <= h))) for h in (1, 3, 5, 10)}
+        hit["mrr_at_20"] = float(np.mean(np.where(ranks > 0, 1.0 / np.maximum(ranks, 1), 0.0)))
+        hit["queries"] = nr
+        extra["rag_metrics_vs_exact_fp32"] = hit
+        log("Hit@1 %.3f Hit@5 %.3f MRR@20 %.3f" % (hit["hit_at_1"], hit["hit_at_5"], hit["mrr_at_20"]))
         # single-query latency (one call: rotation + scan + merge)
         lat = []
         q1 = Q[:1].contiguous()

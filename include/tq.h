@@ -158,6 +158,32 @@ tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev,
                           float *scales_dev, uint16_t *tenants_dev,
                           void *stream);
 
+/* The index's d, bits, n_tenants and vector count n (any output may be
+ * NULL). */
+tq_status tq_index_info(const tq_index *idx, int32_t *d, int32_t *bits,
+                        int32_t *n_tenants, int64_t *n);
+
+/* Persistence (section III-A: both index types persist to disk).
+ * save() writes the index to `path` (created or truncated): a 48-byte header
+ * (magic "TQINDEX1", format version 1, flags 0, d, bits, rotation seed, n,
+ * n_tenants), the canonical codes [n][d*bits/8], the scales [n] float32 and
+ * the tenant ids [n] uint16, all little-endian, then a 64-bit FNV-1a hash of
+ * every preceding byte.  The content is read back from the device with
+ * blocking copies, and host memory of the file's size is used.  A file that
+ * cannot be created or written is TQ_EINVAL. */
+tq_status tq_index_save(const tq_index *idx, const char *path);
+
+/* load() reads a file written by save() into a new index on the current
+ * device, built on `cb` and `rot`; they must match the file's d, bits and
+ * rotation seed (TQ_EINVAL otherwise).  The whole file is read and checked --
+ * magic, header ranges, hash, no trailing bytes -- before any device work,
+ * so a damaged or truncated file is TQ_EINVAL (TQ_EUNSUPPORTED for another
+ * format version) and no index is made.  The caller frees *out with
+ * tq_index_free.  Searches on the loaded index return what searches on the
+ * saved one did. */
+tq_status tq_index_load(const char *path, const tq_codebook *cb,
+                        const tq_rotation *rot, tq_index **out);
+
 void tq_index_free(tq_index *idx);
 
 /* ------------------------------------------------------------ search ------

@@ -17,14 +17,15 @@ follows:
                 section II-B steps 1-5 (sequential float64 arithmetic in C).
 * search     -- query rotation, scoring, allowlist filter and top-k,
                 sections II-B step 5 and III-B; exact ground truth and
-                Recall@k as in section IV-A.
+                Recall@k as in section IV-A; Hit@k and MRR@20 as in
+                section IV-E.
 """
 from .marginal import density, tail_prob, cell_mass, cell_first_moment, mse_per_coord
 from .codebook import lloyd_max, Codebook
 from .rotation import splitmix64, uniforms53, gaussians, haar_rotation
 from .encode import encode, pack_codes, unpack_codes, code_bytes_per_vector
 from .search import (rotate_queries, scores_for_ids, search, exact_search,
-                     recall_at_k, allowed_mask)
+                     recall_at_k, hit_at_k, mrr_at_k, allowed_mask)
 
 __all__ = [
     "density", "tail_prob", "cell_mass", "cell_first_moment", "mse_per_coord",
@@ -32,5 +33,5 @@ __all__ = [
     "splitmix64", "uniforms53", "gaussians", "haar_rotation",
     "encode", "pack_codes", "unpack_codes", "code_bytes_per_vector",
     "rotate_queries", "scores_for_ids", "search", "exact_search",
-    "recall_at_k", "allowed_mask",
+    "recall_at_k", "hit_at_k", "mrr_at_k", "allowed_mask",
 ]

@@ -125,3 +125,37 @@ def recall_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int) -> float:
         a_set = set(int(v) for v in a if v >= 0)
         vals.append(len(a_set & e_set) / len(e_set))
     return float(np.mean(vals)) if vals else float("nan")
+
+
+def _rank_of_top1(approx_row, top1, k):
+    """1-based position of top1 among the first k approximate ids, or 0."""
+    for r, v in enumerate(approx_row[:k]):
+        if int(v) == int(top1):
+            return r + 1
+    return 0
+
+
+def hit_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int) -> float:
+    """Hit@k of section IV-E: the fraction of queries whose exact top-1 id is
+    among the first k approximate ids.  exact_ids: [nq, >=1], column 0 the
+    exact best (queries with no eligible vector, id -1, are skipped)."""
+    approx_ids = np.atleast_2d(approx_ids)
+    exact_ids = np.atleast_2d(exact_ids)
+    vals = [1.0 if _rank_of_top1(a, e[0], k) > 0 else 0.0
+            for a, e in zip(approx_ids, exact_ids) if e[0] >= 0]
+    return float(np.mean(vals)) if vals else float("nan")
+
+
+def mrr_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int = 20) -> float:
+    """MRR@k of section IV-E: the mean over queries of 1 / rank of the exact
+    top-1 id in the approximate list, counting 0 when it is not among the
+    first k (the paper reports k = 20)."""
+    approx_ids = np.atleast_2d(approx_ids)
+    exact_ids = np.atleast_2d(exact_ids)
+    vals = []
+    for a, e in zip(approx_ids, exact_ids):
+        if e[0] < 0:
+            continue
+        r = _rank_of_top1(a, e[0], k)
+        vals.append(1.0 / r if r else 0.0)
+    return float(np.mean(vals)) if vals else float("nan")

@@ -12,6 +12,7 @@ the current stream; every step of the method runs in the HIP library.
 from __future__ import annotations
 
 import ctypes
+import os
 
 import numpy as np
 
@@ -136,10 +137,29 @@ class Index:
     def __init__(self, cb: Codebook, rot: Rotation, n_tenants: int = 1):
         h = ctypes.c_void_p()
         check(lib.tq_index_create(cb._h, rot._h, n_tenants, ctypes.byref(h)))
+        self._adopt(h)
+
+    def _adopt(self, h) -> None:
         self._h = h
-        self.d, self.bits, self.n_tenants = cb.d, cb.bits, n_tenants
-        self.words = (n_tenants + 63) // 64
+        d, bits, t = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        check(lib.tq_index_info(h, ctypes.byref(d), ctypes.byref(bits), ctypes.byref(t), None))
+        self.d, self.bits, self.n_tenants = d.value, bits.value, t.value
+        self.words = (self.n_tenants + 63) // 64
         self._ws = None
+
+    def save(self, path) -> None:
+        """Writes the index to a file (tq_index_save)."""
+        check(lib.tq_index_save(self._h, os.fsencode(path)))
+
+    @classmethod
+    def load(cls, cb: Codebook, rot: Rotation, path) -> "Index":
+        """Reads an index written by save(); cb and rot must match its d,
+        bits and rotation seed (tq_index_load)."""
+        h = ctypes.c_void_p()
+        check(lib.tq_index_load(os.fsencode(path), cb._h, rot._h, ctypes.byref(h)))
+        obj = cls.__new__(cls)
+        obj._adopt(h)
+        return obj
 
     def __len__(self) -> int:
         n = ctypes.c_int64()

@@ -52,6 +52,9 @@ def _load():
         "tq_index_add_codes": ([P, P, P, P, I64, P], ctypes.c_int),
         "tq_index_size": ([P, P], ctypes.c_int),
         "tq_index_export": ([P, P, P, P, P], ctypes.c_int),
+        "tq_index_info": ([P, P, P, P, P], ctypes.c_int),
+        "tq_index_save": ([P, ctypes.c_char_p], ctypes.c_int),
+        "tq_index_load": ([ctypes.c_char_p, P, P, P], ctypes.c_int),
         "tq_index_free": ([P], None),
         "tq_search": ([P, P, I64, I32, P, P, P, P], ctypes.c_int),
         "tq_search_workspace_size": ([P, I64, I32, I32, P], ctypes.c_int),
@@ -70,7 +73,8 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_codebook_mse", "tq_codebook_free", "tq_rotation_create", "tq_rotation_matrix",
             "tq_rotation_free", "tq_rotate_quantize", "tq_rotate_queries", "tq_index_create",
             "tq_index_reserve", "tq_index_add", "tq_index_add_codes", "tq_index_size",
-            "tq_index_export", "tq_index_free", "tq_search", "tq_search_workspace_size",
+            "tq_index_export", "tq_index_info", "tq_index_save", "tq_index_load",
+            "tq_index_free", "tq_search", "tq_search_workspace_size",
             "tq_search_ex", "tq_last_search_fallbacks")
 
 

@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <new>
 #include <string>
@@ -473,6 +474,191 @@ tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev, float *scales
                                       hipMemcpyDeviceToDevice, s);
         if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(tenants)");
     }
+    return TQ_OK;
+}
+
+tq_status tq_index_info(const tq_index *idx, int32_t *d, int32_t *bits, int32_t *n_tenants,
+                        int64_t *n) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (d) *d = idx->d;
+    if (bits) *bits = idx->bits;
+    if (n_tenants) *n_tenants = idx->T;
+    if (n) *n = idx->n;
+    return TQ_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// ------------------------------------------------------------ persistence
+// File layout (little-endian): FileHeader, then the canonical codes
+// [n][d*bits/8], the scales [n] float32 and the tenant ids [n] uint16, then
+// a 64-bit FNV-1a hash of every preceding byte.
+constexpr char kFileMagic[8] = {'T', 'Q', 'I', 'N', 'D', 'E', 'X', '1'};
+constexpr uint32_t kFileVersion = 1;
+
+struct FileHeader {
+    char magic[8];
+    uint32_t version;
+    uint32_t flags;          // no optional sections defined yet: 0
+    int32_t d, bits;
+    uint64_t seed;           // rotation seed
+    int64_t n;
+    int32_t n_tenants;
+    int32_t reserved;
+};
+static_assert(sizeof(FileHeader) == 48, "file header layout");
+
+struct Fnv1a {
+    uint64_t h = 1469598103934665603ull;
+    void add(const void *p, size_t n) {
+        const uint8_t *b = static_cast<const uint8_t *>(p);
+        for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+    }
+};
+
+struct FileCloser {
+    FILE *f;
+    ~FileCloser() {
+        if (f) fclose(f);
+    }
+};
+
+// Device scratch released on destruction (synchronous allocation).
+struct DevBuf {
+    void *p = nullptr;
+    hipError_t alloc(size_t bytes) { return hipMalloc(&p, bytes ? bytes : 1); }
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+};
+
+}  // namespace
+
+extern "C" {
+
+tq_status tq_index_save(const tq_index *idx, const char *path) {
+    if (!idx || !path) return fail(TQ_EINVAL, "NULL argument");
+    const int64_t n = idx->n;
+    const size_t cbytes = (size_t)idx->d * idx->bits / 8;
+    std::vector<uint8_t> codes((size_t)n * cbytes);
+    std::vector<float> scales((size_t)n);
+    std::vector<uint16_t> ten((size_t)n);
+    if (n > 0) {
+        tq_status st = device_ready();
+        if (st != TQ_OK) return st;
+        DevBuf c, sc, t;
+        hipError_t e = c.alloc(codes.size());
+        if (e == hipSuccess) e = sc.alloc(scales.size() * 4);
+        if (e == hipSuccess) e = t.alloc(ten.size() * 2);
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc(save staging)");
+        st = tq_index_export(idx, static_cast<uint8_t *>(c.p), static_cast<float *>(sc.p),
+                             static_cast<uint16_t *>(t.p), nullptr);
+        if (st != TQ_OK) return st;
+        e = hipMemcpy(codes.data(), c.p, codes.size(), hipMemcpyDeviceToHost);
+        if (e == hipSuccess) e = hipMemcpy(scales.data(), sc.p, scales.size() * 4, hipMemcpyDeviceToHost);
+        if (e == hipSuccess) e = hipMemcpy(ten.data(), t.p, ten.size() * 2, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "index read-back");
+    }
+    FileHeader h{};
+    std::memcpy(h.magic, kFileMagic, 8);
+    h.version = kFileVersion;
+    h.flags = 0;
+    h.d = idx->d;
+    h.bits = idx->bits;
+    h.seed = idx->rot.seed;
+    h.n = n;
+    h.n_tenants = idx->T;
+    FileCloser fc{fopen(path, "wb")};
+    if (!fc.f) return fail(TQ_EINVAL, std::string("cannot open ") + path + " for writing");
+    Fnv1a fnv;
+    bool ok = true;
+    auto put = [&](const void *p, size_t bytes) {
+        if (ok && bytes && fwrite(p, 1, bytes, fc.f) != bytes) ok = false;
+        fnv.add(p, bytes);
+    };
+    put(&h, sizeof h);
+    put(codes.data(), codes.size());
+    put(scales.data(), scales.size() * 4);
+    put(ten.data(), ten.size() * 2);
+    const uint64_t sum = fnv.h;
+    if (ok && fwrite(&sum, 1, 8, fc.f) != 8) ok = false;
+    const int rc = fclose(fc.f);
+    fc.f = nullptr;
+    if (!ok || rc != 0) return fail(TQ_EINVAL, std::string("write to ") + path + " failed");
+    return TQ_OK;
+}
+
+tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotation *rot,
+                        tq_index **out) {
+    if (!out) return fail(TQ_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!path || !cb || !rot) return fail(TQ_EINVAL, "NULL argument");
+    FileCloser fc{fopen(path, "rb")};
+    if (!fc.f) return fail(TQ_EINVAL, std::string("cannot open ") + path);
+    Fnv1a fnv;
+    bool ok = true;
+    auto get = [&](void *p, size_t bytes) {
+        if (ok && bytes && fread(p, 1, bytes, fc.f) != bytes) ok = false;
+        if (ok) fnv.add(p, bytes);
+    };
+    FileHeader h{};
+    get(&h, sizeof h);
+    if (!ok || std::memcmp(h.magic, kFileMagic, 8) != 0)
+        return fail(TQ_EINVAL, std::string(path) + " is not an index file");
+    if (h.version != kFileVersion || h.flags != 0)
+        return fail(TQ_EUNSUPPORTED, "index file version or sections not supported");
+    if (h.d != cb->t.d || h.bits != cb->t.bits)
+        return fail(TQ_EINVAL, "index file d/bits differ from the codebook's");
+    if (h.d != rot->d || h.seed != rot->seed)
+        return fail(TQ_EINVAL, "index file d/seed differ from the rotation's");
+    if (h.n < 0 || h.n > (int64_t)INT32_MAX || h.n_tenants < 1 || h.n_tenants > 65535)
+        return fail(TQ_EINVAL, "index file header out of range");
+    const int64_t n = h.n;
+    const size_t cbytes = (size_t)h.d * h.bits / 8;
+    std::vector<uint8_t> codes;
+    std::vector<float> scales;
+    std::vector<uint16_t> ten;
+    try {
+        codes.resize((size_t)n * cbytes);
+        scales.resize((size_t)n);
+        ten.resize((size_t)n);
+    } catch (const std::bad_alloc &) {
+        return fail(TQ_ENOMEM, "host allocation failed");
+    }
+    get(codes.data(), codes.size());
+    get(scales.data(), scales.size() * 4);
+    get(ten.data(), ten.size() * 2);
+    uint64_t sum = 0;
+    if (!ok || fread(&sum, 1, 8, fc.f) != 8) return fail(TQ_EINVAL, std::string(path) + " is truncated");
+    if (sum != fnv.h) return fail(TQ_EINVAL, std::string(path) + " fails its checksum");
+    if (fgetc(fc.f) != EOF) return fail(TQ_EINVAL, std::string(path) + " has trailing bytes");
+    tq_index *x = nullptr;
+    tq_status st = tq_index_create(cb, rot, h.n_tenants, &x);
+    if (st != TQ_OK) return st;
+    if (n > 0) {
+        st = index_grow(x, n, nullptr);
+        DevBuf c, sc, t;
+        hipError_t e = hipSuccess;
+        if (st == TQ_OK) {
+            e = c.alloc(codes.size());
+            if (e == hipSuccess) e = sc.alloc(scales.size() * 4);
+            if (e == hipSuccess) e = t.alloc(ten.size() * 2);
+            if (e == hipSuccess) e = hipMemcpy(c.p, codes.data(), codes.size(), hipMemcpyHostToDevice);
+            if (e == hipSuccess) e = hipMemcpy(sc.p, scales.data(), scales.size() * 4, hipMemcpyHostToDevice);
+            if (e == hipSuccess) e = hipMemcpy(t.p, ten.data(), ten.size() * 2, hipMemcpyHostToDevice);
+            st = e != hipSuccess ? hip_fail(e, "index upload")
+                                 : tq_index_add_codes(x, static_cast<const uint8_t *>(c.p),
+                                                      static_cast<const float *>(sc.p),
+                                                      static_cast<const uint16_t *>(t.p), n, nullptr);
+        }
+        if (st != TQ_OK) {
+            tq_index_free(x);
+            return st;
+        }
+    }
+    *out = x;
     return TQ_OK;
 }
 

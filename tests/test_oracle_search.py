@@ -90,3 +90,33 @@ def test_exact_search_and_recall():
     assert sc[0, 0] == np.dot(X[5].astype(np.float64), X[5].astype(np.float64))
     assert oracle.recall_at_k(ids, ids, 3) == 1.0
     assert oracle.recall_at_k(np.array([[5, -1, -1]]), np.array([[5, 9, 2]]), 3) == 1 / 3
+
+
+def test_hit_and_mrr_hand_worked():
+    """Hit@k and MRR@k (section IV-E) on lists worked out by hand."""
+    approx = np.array([[5, 3, 1], [2, 9, 7], [4, 6, 8], [1, 2, 3]])
+    exact = np.array([[3], [7], [0], [-1]])          # last query: nothing eligible
+    assert oracle.hit_at_k(approx, exact, 1) == 0.0
+    assert oracle.hit_at_k(approx, exact, 2) == 1 / 3
+    assert oracle.hit_at_k(approx, exact, 3) == 2 / 3
+    assert abs(oracle.mrr_at_k(approx, exact, 3) - (1 / 2 + 1 / 3 + 0) / 3) < 1e-15
+    assert abs(oracle.mrr_at_k(approx, exact, 2) - (1 / 2) / 3) < 1e-15
+
+
+def test_hit_and_mrr_properties():
+    X = np.random.default_rng(21).standard_normal((300, 32)).astype(np.float32)
+    Q = np.random.default_rng(22).standard_normal((40, 32)).astype(np.float32)
+    ex, _ = oracle.exact_search(X, Q, k=20)
+    # exact search scores perfectly against itself
+    assert oracle.hit_at_k(ex, ex, 1) == 1.0 and oracle.mrr_at_k(ex, ex, 20) == 1.0
+    # a perturbed ranking: Hit@1 <= MRR@k <= Hit@k, and Hit@k grows with k
+    rng = np.random.default_rng(23)
+    approx = np.array([rng.permutation(row) for row in ex])
+    h = [oracle.hit_at_k(approx, ex, k) for k in (1, 3, 5, 10, 20)]
+    assert all(a <= b for a, b in zip(h, h[1:])) and h[-1] == 1.0
+    m = oracle.mrr_at_k(approx, ex, 20)
+    assert h[0] <= m <= h[-1]
+    # the top-1 moved to rank r everywhere gives MRR exactly 1/r
+    shifted = np.concatenate([ex[:, 1:4], ex[:, :1], ex[:, 4:]], axis=1)
+    assert abs(oracle.mrr_at_k(shifted, ex, 20) - 1 / 4) < 1e-15
+    assert oracle.hit_at_k(shifted, ex, 3) == 0.0 and oracle.hit_at_k(shifted, ex, 4) == 1.0
