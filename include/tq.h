@@ -149,7 +149,7 @@ tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev,
                              const uint16_t *tenants_dev, int64_t n,
                              void *stream);
 
-/* Number of vectors in the index. */
+/* Number of vectors in the index (for an id-map index: not deleted). */
 tq_status tq_index_size(const tq_index *idx, int64_t *n_out);
 
 /* Copies the index content back in the canonical layout: codes_dev
@@ -158,10 +158,11 @@ tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev,
                           float *scales_dev, uint16_t *tenants_dev,
                           void *stream);
 
-/* The index's d, bits, n_tenants and vector count n (any output may be
- * NULL). */
+/* The index's d, bits, n_tenants, slot count n -- vectors ever added,
+ * deleted ones included -- and whether it is an id-map index (1) or a
+ * positional one (0); any output may be NULL. */
 tq_status tq_index_info(const tq_index *idx, int32_t *d, int32_t *bits,
-                        int32_t *n_tenants, int64_t *n);
+                        int32_t *n_tenants, int64_t *n, int32_t *idmap);
 
 /* Persistence (section III-A: both index types persist to disk).
  * save() writes the index to `path` (created or truncated): a 48-byte header
@@ -185,6 +186,62 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb,
                         const tq_rotation *rot, tq_index **out);
 
 void tq_index_free(tq_index *idx);
+
+/* ---------------------------------------------------------- id-map index --
+ * IdMapIndex (section III-A): the flat index of tq_index_create whose vectors
+ * carry caller-chosen uint64 ids, with O(1) deletion and id-based access
+ * control.  Vectors still occupy positions ("slots") in the store in the
+ * order they are added; a deleted vector's slot stays, marked dead in its
+ * block's live-slot mask, and the block's tenant summary is rebuilt over
+ * its live slots, so deletions are folded into the block-skip test of the
+ * scan (section III-B).  Searches return the external ids (uint64 bit
+ * patterns in the int64 output; 2^64-1 is reserved, so -1 still marks
+ * padding).  tq_index_add / tq_index_add_codes are TQ_EINVAL on it.  The
+ * search, export, save and load calls work on both index types; an id-map
+ * index with deleted vectors, or a search with a slot allowlist, always runs
+ * the single-query scan (TQ_PATH_MFMA is TQ_EUNSUPPORTED then). */
+tq_status tq_idmap_create(const tq_codebook *cb, const tq_rotation *rot,
+                          int32_t n_tenants, tq_index **out);
+
+/* As tq_index_add / tq_index_add_codes, with external ids ids_host [n]
+ * (host memory).  Every id must be new to the index, distinct within the
+ * call and not 2^64-1; otherwise TQ_EINVAL and nothing is added.
+ * Synchronises `stream`. */
+tq_status tq_index_add_ids(tq_index *idx, const float *X_dev,
+                           const uint64_t *ids_host,
+                           const uint16_t *tenants_dev, int64_t n,
+                           void *stream);
+tq_status tq_index_add_codes_ids(tq_index *idx, const uint8_t *codes_dev,
+                                 const float *scales_dev,
+                                 const uint64_t *ids_host,
+                                 const uint16_t *tenants_dev, int64_t n,
+                                 void *stream);
+
+/* Deletes the vectors with ids ids_host [n] (host memory; ids not in the
+ * index are ignored), each in O(1): the id leaves the host map, its slot's
+ * live bit is cleared and its block's tenant summary is rebuilt.  A deleted
+ * id may be added again (it gets a new slot).  *removed_out (may be NULL)
+ * receives the number deleted.  Runs on the null stream and returns after
+ * the device update; it must not overlap searches of the index. */
+tq_status tq_index_remove_ids(tq_index *idx, const uint64_t *ids_host,
+                              int64_t n, int64_t *removed_out);
+
+/* The slot of each id in ids_host [n], or -1 when the index does not hold
+ * it, into slots_host [n] (host memory).  On a positional index an id is its
+ * slot (-1 past the end). */
+tq_status tq_index_slots(const tq_index *idx, const uint64_t *ids_host,
+                         int64_t n, int64_t *slots_host);
+
+/* Slot-level allowlists (section III-B: access control by id).  Builds, for
+ * nq queries, the bitmaps bitmap_dev [nq][ceil(n/64)] uint64 (n = the index's
+ * slot count; slot v is bit v & 63 of word v >> 6) from the id lists
+ * ids_host[offsets_host[q] .. offsets_host[q+1]) (host memory, offsets
+ * [nq+1] starting at 0).  Ids the index does not hold are ignored.  Pass the
+ * result to tq_search_ex with TQ_FLAG_SLOT_ALLOW; it is valid for the
+ * index's current slot count.  Synchronises `stream`. */
+tq_status tq_slot_allowlist(const tq_index *idx, const uint64_t *ids_host,
+                            const int64_t *offsets_host, int64_t nq,
+                            uint64_t *bitmap_dev, void *stream);
 
 /* ------------------------------------------------------------ search ------
  * search(Q, k, allowlist) -> ids + scores -- section II-B step 5 and section
@@ -211,7 +268,7 @@ tq_status tq_search(const tq_index *idx, const float *Q_dev, int64_t nq,
  *  TQ_PATH_LUT   one pass over the code store per query, with the query's
  *                lookup table in LDS.
  *  TQ_PATH_MFMA  one pass per tile of 32 queries: approximate float16 scores
- *                on the matrix cores select 64 candidates per query, which
+ *                on the matrix cores select 256 candidates per query, which
  *                are rescored exactly (the same scores as TQ_PATH_LUT).  A
  *                per-query certificate -- a rigorous bound on the
  *                approximation error -- proves that the exact top k lies
@@ -229,6 +286,12 @@ typedef enum {
 /* Flag ORed into `path`: Q_dev already holds rotated queries R q (for
  * instance from tq_rotate_queries), so the rotation step is skipped. */
 #define TQ_FLAG_PREROTATED 0x100
+
+/* Flag ORed into `path`: allow_dev holds slot-level allowlists [nq][ceil(n/64)]
+ * (see tq_slot_allowlist) instead of tenant allowlists: a vector may be
+ * returned when its slot's bit is set.  Blocks with no allowed live slot are
+ * skipped before their codes are read. */
+#define TQ_FLAG_SLOT_ALLOW 0x200
 
 /* Workspace size in bytes needed by tq_search_ex for (nq, k, path). */
 tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k,

@@ -64,9 +64,13 @@ def _pad(ids, sc, k):
 
 def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
            R32: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,
-           chunk: int = 65536):
+           chunk: int = 65536, masks=None):
     """Top-k over TurboQuant codes for every query.  Returns (ids int64 [nq,k],
-    scores float64 [nq,k])."""
+    scores float64 [nq,k]).  The eligible vectors of query b are those whose
+    tenant the allowlist row allow[b] admits (section III-B) and, when masks
+    is given, those with masks[b][i] true: a per-query set of allowed
+    positions (slot-level allowlists, and the vectors of an id-map index not
+    deleted, section III-A)."""
     if k <= 0:
         raise ValueError("k must be positive")
     qrot = rotate_queries(R32, Q)
@@ -83,6 +87,9 @@ def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
     all_ids = np.arange(n, dtype=np.int64)
     for b in range(nq):
         m = allowed_mask(tenants, None if allow is None else allow[b])
+        if masks is not None and masks[b] is not None:
+            mb = np.asarray(masks[b], dtype=bool)
+            m = mb if m is None else (m & mb)
         ids = all_ids if m is None else all_ids[m]
         sc = sc_all[b] if m is None else sc_all[b][m]
         i, s_ = _order(sc, ids, k)

@@ -16,7 +16,7 @@ import os
 
 import numpy as np
 
-from ._lib import FLAG_PREROTATED, PATHS, TQError, check, lib
+from ._lib import FLAG_PREROTATED, FLAG_SLOT_ALLOW, PATHS, TQError, check, lib
 
 __all__ = ["Codebook", "Rotation", "Index", "TQError", "rotate_quantize",
            "rotate_queries", "version", "last_search_fallbacks"]
@@ -142,10 +142,40 @@ class Index:
     def _adopt(self, h) -> None:
         self._h = h
         d, bits, t = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
-        check(lib.tq_index_info(h, ctypes.byref(d), ctypes.byref(bits), ctypes.byref(t), None))
+        check(lib.tq_index_info(h, ctypes.byref(d), ctypes.byref(bits), ctypes.byref(t), None, None))
         self.d, self.bits, self.n_tenants = d.value, bits.value, t.value
         self.words = (self.n_tenants + 63) // 64
         self._ws = None
+
+    @property
+    def n_slots(self) -> int:
+        """Vectors ever added (deleted ones of an id-map index included)."""
+        n = ctypes.c_int64()
+        check(lib.tq_index_info(self._h, None, None, None, ctypes.byref(n), None))
+        return n.value
+
+    def slots(self, ids) -> np.ndarray:
+        """Slot of each id (-1 if absent); on a positional index an id is its slot."""
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        out = np.empty(ids.shape[0], dtype=np.int64)
+        check(lib.tq_index_slots(self._h, ids.ctypes.data_as(ctypes.c_void_p), ids.shape[0],
+                                 out.ctypes.data_as(ctypes.c_void_p)))
+        return out
+
+    def slot_allowlist(self, id_lists, device="cuda"):
+        """Slot-level allowlists for search(slot_allow=...): one list of ids
+        per query -> cuda int64 [nq, ceil(n_slots/64)] (tq_slot_allowlist)."""
+        torch = _torch()
+        nq = len(id_lists)
+        offs = np.zeros(nq + 1, dtype=np.int64)
+        offs[1:] = np.cumsum([len(x) for x in id_lists])
+        flat = np.ascontiguousarray(np.concatenate([np.asarray(x, dtype=np.uint64) for x in id_lists])
+                                    if nq else np.zeros(0, np.uint64))
+        out = torch.zeros((nq, (self.n_slots + 63) // 64), dtype=torch.int64, device=device)
+        check(lib.tq_slot_allowlist(self._h, flat.ctypes.data_as(ctypes.c_void_p),
+                                    offs.ctypes.data_as(ctypes.c_void_p), nq,
+                                    ctypes.c_void_p(out.data_ptr()), _stream(out.device)))
+        return out
 
     def save(self, path) -> None:
         """Writes the index to a file (tq_index_save)."""
@@ -157,7 +187,9 @@ class Index:
         bits and rotation seed (tq_index_load)."""
         h = ctypes.c_void_p()
         check(lib.tq_index_load(os.fsencode(path), cb._h, rot._h, ctypes.byref(h)))
-        obj = cls.__new__(cls)
+        idm = ctypes.c_int32()
+        check(lib.tq_index_info(h, None, None, None, None, ctypes.byref(idm)))
+        obj = (IdMapIndex if idm.value else Index).__new__(IdMapIndex if idm.value else Index)
         obj._adopt(h)
         return obj
 
@@ -199,18 +231,27 @@ class Index:
         return b.value
 
     def search(self, Q, k: int, allow=None, path: str = "auto", ids=None, scores=None,
-               workspace=None, prerotated: bool = False):
+               workspace=None, prerotated: bool = False, slot_allow=None):
         """Top-k per query row of Q (cuda float32 [nq, d]).  allow: cuda int64
         tensor [nq, words] (bit patterns of the uint64 allowlist words) or None.
+        slot_allow: slot-level allowlists from slot_allowlist() instead.
         prerotated: Q already holds R q (see rotate_queries).
-        Returns (ids int64 [nq, k], scores float32 [nq, k])."""
+        Returns (ids int64 [nq, k], scores float32 [nq, k]); an id-map index
+        returns its external ids (uint64 bit patterns)."""
         torch = _torch()
         nq = Q.shape[0]
+        flags = FLAG_PREROTATED if prerotated else 0
+        if slot_allow is not None:
+            if allow is not None:
+                raise ValueError("give allow or slot_allow, not both")
+            if tuple(slot_allow.shape) != (nq, (self.n_slots + 63) // 64):
+                raise ValueError("slot_allow must have shape (nq, %d)" % ((self.n_slots + 63) // 64))
+            allow, flags = slot_allow, flags | FLAG_SLOT_ALLOW
         if ids is None:
             ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
         if scores is None:
             scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
-        if allow is not None and tuple(allow.shape) != (nq, self.words):
+        elif allow is not None and tuple(allow.shape) != (nq, self.words):
             raise ValueError("allow must have shape (nq, %d)" % self.words)
         need = self.workspace_bytes(nq, k, path)
         if workspace is None:
@@ -219,7 +260,7 @@ class Index:
             workspace = self._ws
         check(lib.tq_search_ex(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k,
                                _dev_ptr(allow, torch.int64, "allow") if allow is not None else None,
-                               PATHS[path] | (FLAG_PREROTATED if prerotated else 0),
+                               PATHS[path] | flags,
                                ctypes.c_void_p(workspace.data_ptr()),
                                workspace.numel(), _dev_ptr(ids, torch.int64, "ids"),
                                _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
@@ -244,3 +285,42 @@ class Index:
         if h is not None and h.value:
             _free(h)
             self._h = None
+
+
+class IdMapIndex(Index):
+    """IdMapIndex (tq_idmap_create): vectors carry uint64 ids, deletions are
+    O(1), and searches return the ids."""
+
+    def __init__(self, cb: Codebook, rot: Rotation, n_tenants: int = 1):
+        h = ctypes.c_void_p()
+        check(lib.tq_idmap_create(cb._h, rot._h, n_tenants, ctypes.byref(h)))
+        self._adopt(h)
+
+    def add(self, X, ids, tenants=None) -> None:
+        torch = _torch()
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        if ids.shape != (X.shape[0],):
+            raise ValueError("ids must have shape (n,)")
+        check(lib.tq_index_add_ids(self._h, _dev_ptr(X, torch.float32, "X", 2),
+                                   ids.ctypes.data_as(ctypes.c_void_p),
+                                   _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
+                                   X.shape[0], _stream(X.device)))
+
+    def add_codes(self, codes, scales, ids, tenants=None) -> None:
+        torch = _torch()
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        if ids.shape != (codes.shape[0],):
+            raise ValueError("ids must have shape (n,)")
+        check(lib.tq_index_add_codes_ids(self._h, _dev_ptr(codes, torch.uint8, "codes", 2),
+                                         _dev_ptr(scales, torch.float32, "scales", 1),
+                                         ids.ctypes.data_as(ctypes.c_void_p),
+                                         _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
+                                         codes.shape[0], _stream(codes.device)))
+
+    def remove(self, ids) -> int:
+        """Deletes the vectors with these ids; returns how many were present."""
+        ids = np.ascontiguousarray(ids, dtype=np.uint64)
+        r = ctypes.c_int64()
+        check(lib.tq_index_remove_ids(self._h, ids.ctypes.data_as(ctypes.c_void_p), ids.shape[0],
+                                      ctypes.byref(r)))
+        return r.value

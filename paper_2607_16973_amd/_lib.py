@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libtq.so")
 TQ_OK, TQ_EINVAL, TQ_ENOMEM, TQ_EDEVICE, TQ_EUNSUPPORTED = 0, -1, -2, -3, -4
 PATHS = {"auto": 0, "lut": 1, "mfma": 2}
 FLAG_PREROTATED = 0x100
+FLAG_SLOT_ALLOW = 0x200
 _STATUS = {TQ_EINVAL: "TQ_EINVAL", TQ_ENOMEM: "TQ_ENOMEM", TQ_EDEVICE: "TQ_EDEVICE",
            TQ_EUNSUPPORTED: "TQ_EUNSUPPORTED"}
 
@@ -52,7 +53,13 @@ def _load():
         "tq_index_add_codes": ([P, P, P, P, I64, P], ctypes.c_int),
         "tq_index_size": ([P, P], ctypes.c_int),
         "tq_index_export": ([P, P, P, P, P], ctypes.c_int),
-        "tq_index_info": ([P, P, P, P, P], ctypes.c_int),
+        "tq_index_info": ([P, P, P, P, P, P], ctypes.c_int),
+        "tq_idmap_create": ([P, P, I32, P], ctypes.c_int),
+        "tq_index_add_ids": ([P, P, P, P, I64, P], ctypes.c_int),
+        "tq_index_add_codes_ids": ([P, P, P, P, P, I64, P], ctypes.c_int),
+        "tq_index_remove_ids": ([P, P, I64, P], ctypes.c_int),
+        "tq_index_slots": ([P, P, I64, P], ctypes.c_int),
+        "tq_slot_allowlist": ([P, P, P, I64, P, P], ctypes.c_int),
         "tq_index_save": ([P, ctypes.c_char_p], ctypes.c_int),
         "tq_index_load": ([ctypes.c_char_p, P, P, P], ctypes.c_int),
         "tq_index_free": ([P], None),
@@ -74,6 +81,8 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_rotation_free", "tq_rotate_quantize", "tq_rotate_queries", "tq_index_create",
             "tq_index_reserve", "tq_index_add", "tq_index_add_codes", "tq_index_size",
             "tq_index_export", "tq_index_info", "tq_index_save", "tq_index_load",
+            "tq_idmap_create", "tq_index_add_ids", "tq_index_add_codes_ids", "tq_index_remove_ids",
+            "tq_index_slots", "tq_slot_allowlist",
             "tq_index_free", "tq_search", "tq_search_workspace_size",
             "tq_search_ex", "tq_last_search_fallbacks")
 

@@ -7,6 +7,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "kernels.h"
@@ -94,6 +95,15 @@ tq_status rotation_dev(const tq_rotation *rot, const float **out) {
 }
 
 // Stream-ordered scratch allocation released on destruction.
+// Device scratch released on destruction (synchronous allocation).
+struct DevBuf {
+    void *p = nullptr;
+    hipError_t alloc(size_t bytes) { return hipMalloc(&p, bytes ? bytes : 1); }
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+};
+
 struct AsyncBuf {
     void *p = nullptr;
     hipStream_t s = nullptr;
@@ -132,6 +142,14 @@ struct tq_index {
     float *cents_dev = nullptr;    // levels
     int *status = nullptr;         // device status word
     int device = -1;
+    // IdMapIndex (section III-A): the external id of every slot and the
+    // live-slot mask of every block on the device, the map from external id
+    // to slot on the host.  Deleted slots stay in the store, dead.
+    bool idmap = false;
+    uint64_t *ext = nullptr;       // cap
+    uint64_t *live = nullptr;      // cap/64
+    std::unordered_map<uint64_t, int64_t> slot_of;
+    int64_t n_deleted = 0;
 };
 
 namespace {
@@ -149,6 +167,10 @@ void index_release(tq_index *x) {
     if (x->summ) (void)hipFree(x->summ);
     if (x->cents_dev) (void)hipFree(x->cents_dev);
     if (x->status) (void)hipFree(x->status);
+    if (x->ext) (void)hipFree(x->ext);
+    if (x->live) (void)hipFree(x->live);
+    x->ext = nullptr;
+    x->live = nullptr;
     x->codes = nullptr;
     x->scales = nullptr;
     x->tenants = nullptr;
@@ -184,22 +206,30 @@ tq_status index_grow(tq_index *x, int64_t need, hipStream_t stream) {
     uint8_t *codes = nullptr;
     float *scales = nullptr;
     uint16_t *ten = nullptr;
-    uint64_t *summ = nullptr;
-    hipError_t e;
-    if ((e = hipMalloc(&codes, nb * block_bytes(x))) != hipSuccess ||
-        (e = hipMalloc(&scales, cap * sizeof(float))) != hipSuccess ||
-        (e = hipMalloc(&ten, cap * sizeof(uint16_t))) != hipSuccess ||
-        (e = hipMalloc(&summ, nb * x->W * sizeof(uint64_t))) != hipSuccess) {
+    uint64_t *summ = nullptr, *ext = nullptr, *live = nullptr;
+    auto free_new = [&]() {
         if (codes) (void)hipFree(codes);
         if (scales) (void)hipFree(scales);
         if (ten) (void)hipFree(ten);
         if (summ) (void)hipFree(summ);
+        if (ext) (void)hipFree(ext);
+        if (live) (void)hipFree(live);
+    };
+    hipError_t e;
+    if ((e = hipMalloc(&codes, nb * block_bytes(x))) != hipSuccess ||
+        (e = hipMalloc(&scales, cap * sizeof(float))) != hipSuccess ||
+        (e = hipMalloc(&ten, cap * sizeof(uint16_t))) != hipSuccess ||
+        (e = hipMalloc(&summ, nb * x->W * sizeof(uint64_t))) != hipSuccess ||
+        (x->idmap && (e = hipMalloc(&ext, cap * sizeof(uint64_t))) != hipSuccess) ||
+        (x->idmap && (e = hipMalloc(&live, nb * sizeof(uint64_t))) != hipSuccess)) {
+        free_new();
         return hip_fail(e, "hipMalloc(index storage)");
     }
     e = hipMemsetAsync(codes, 0, nb * block_bytes(x), stream);
     if (e == hipSuccess) e = hipMemsetAsync(scales, 0, cap * sizeof(float), stream);
     if (e == hipSuccess) e = hipMemsetAsync(ten, 0, cap * sizeof(uint16_t), stream);
     if (e == hipSuccess) e = hipMemsetAsync(summ, 0, nb * x->W * sizeof(uint64_t), stream);
+    if (e == hipSuccess && live) e = hipMemsetAsync(live, 0, nb * sizeof(uint64_t), stream);
     if (e == hipSuccess && x->cap > 0) {
         const int64_t ob = x->cap / 64;
         e = hipMemcpyAsync(codes, x->codes, ob * block_bytes(x), hipMemcpyDeviceToDevice, stream);
@@ -209,23 +239,28 @@ tq_status index_grow(tq_index *x, int64_t need, hipStream_t stream) {
             e = hipMemcpyAsync(ten, x->tenants, x->cap * sizeof(uint16_t), hipMemcpyDeviceToDevice, stream);
         if (e == hipSuccess)
             e = hipMemcpyAsync(summ, x->summ, ob * x->W * sizeof(uint64_t), hipMemcpyDeviceToDevice, stream);
+        if (e == hipSuccess && ext)
+            e = hipMemcpyAsync(ext, x->ext, x->cap * sizeof(uint64_t), hipMemcpyDeviceToDevice, stream);
+        if (e == hipSuccess && live)
+            e = hipMemcpyAsync(live, x->live, ob * sizeof(uint64_t), hipMemcpyDeviceToDevice, stream);
     }
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) {
-        (void)hipFree(codes);
-        (void)hipFree(scales);
-        (void)hipFree(ten);
-        (void)hipFree(summ);
+        free_new();
         return hip_fail(e, "index growth");
     }
     if (x->codes) (void)hipFree(x->codes);
     if (x->scales) (void)hipFree(x->scales);
     if (x->tenants) (void)hipFree(x->tenants);
     if (x->summ) (void)hipFree(x->summ);
+    if (x->ext) (void)hipFree(x->ext);
+    if (x->live) (void)hipFree(x->live);
     x->codes = codes;
     x->scales = scales;
     x->tenants = ten;
     x->summ = summ;
+    x->ext = ext;
+    x->live = live;
     x->cap = cap;
     return TQ_OK;
 }
@@ -404,11 +439,8 @@ static tq_status finish_add(tq_index *x, const uint16_t *tenants_dev, int64_t n,
     return TQ_OK;
 }
 
-tq_status tq_index_add(tq_index *idx, const float *X_dev, const uint16_t *tenants_dev, int64_t n,
-                       void *stream) {
-    if (!idx) return fail(TQ_EINVAL, "NULL index");
-    if (n < 0) return fail(TQ_EINVAL, "n < 0");
-    if (n == 0) return TQ_OK;
+static tq_status add_vectors(tq_index *idx, const float *X_dev, const uint16_t *tenants_dev,
+                             int64_t n, void *stream) {
     if (!X_dev) return fail(TQ_EINVAL, "NULL device pointer");
     if (idx->n + n > (int64_t)INT32_MAX) return fail(TQ_EUNSUPPORTED, "index limited to 2^31-1 vectors");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -435,11 +467,8 @@ tq_status tq_index_add(tq_index *idx, const float *X_dev, const uint16_t *tenant
     return finish_add(idx, tenants_dev, n, s);
 }
 
-tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev, const float *scales_dev,
-                             const uint16_t *tenants_dev, int64_t n, void *stream) {
-    if (!idx) return fail(TQ_EINVAL, "NULL index");
-    if (n < 0) return fail(TQ_EINVAL, "n < 0");
-    if (n == 0) return TQ_OK;
+static tq_status add_codes_impl(tq_index *idx, const uint8_t *codes_dev, const float *scales_dev,
+                                const uint16_t *tenants_dev, int64_t n, void *stream) {
     if (!codes_dev || !scales_dev) return fail(TQ_EINVAL, "NULL device pointer");
     if (idx->n + n > (int64_t)INT32_MAX) return fail(TQ_EUNSUPPORTED, "index limited to 2^31-1 vectors");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -451,9 +480,171 @@ tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev, const floa
     return finish_add(idx, tenants_dev, n, s);
 }
 
+tq_status tq_index_add(tq_index *idx, const float *X_dev, const uint16_t *tenants_dev, int64_t n,
+                       void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (idx->idmap) return fail(TQ_EINVAL, "an id-map index takes vectors with ids (tq_index_add_ids)");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    return add_vectors(idx, X_dev, tenants_dev, n, stream);
+}
+
+tq_status tq_index_add_codes(tq_index *idx, const uint8_t *codes_dev, const float *scales_dev,
+                             const uint16_t *tenants_dev, int64_t n, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (idx->idmap) return fail(TQ_EINVAL, "an id-map index takes vectors with ids (tq_index_add_codes_ids)");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    return add_codes_impl(idx, codes_dev, scales_dev, tenants_dev, n, stream);
+}
+
+tq_status tq_idmap_create(const tq_codebook *cb, const tq_rotation *rot, int32_t n_tenants,
+                          tq_index **out) {
+    tq_status st = tq_index_create(cb, rot, n_tenants, out);
+    if (st == TQ_OK) (*out)->idmap = true;
+    return st;
+}
+
+}  // extern "C"
+
+// New external ids must be valid, absent from the index and distinct.
+static tq_status check_new_ids(const tq_index *x, const uint64_t *ids, int64_t n) {
+    if (!ids) return fail(TQ_EINVAL, "NULL ids");
+    std::unordered_map<uint64_t, int> seen;
+    seen.reserve((size_t)n);
+    for (int64_t i = 0; i < n; ++i) {
+        if (ids[i] == UINT64_MAX) return fail(TQ_EINVAL, "id 2^64-1 is reserved");
+        if (x->slot_of.count(ids[i])) return fail(TQ_EINVAL, "id already in the index");
+        if (!seen.emplace(ids[i], 0).second) return fail(TQ_EINVAL, "repeated id in the batch");
+    }
+    return TQ_OK;
+}
+
+// Records the ids of the n slots from `base` on: external ids on the device,
+// live bits, and the host map.
+static tq_status commit_ids(tq_index *x, const uint64_t *ids, int64_t base, int64_t n,
+                            hipStream_t s) {
+    hipError_t e = hipMemcpyAsync(x->ext + base, ids, n * sizeof(uint64_t), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = set_live(x->live, base, n, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "id upload");
+    for (int64_t i = 0; i < n; ++i) x->slot_of.emplace(ids[i], base + i);
+    return TQ_OK;
+}
+
+static int64_t slot_lookup(const tq_index *x, uint64_t id) {
+    if (!x->idmap) return id < (uint64_t)x->n ? (int64_t)id : -1;
+    auto it = x->slot_of.find(id);
+    return it == x->slot_of.end() ? -1 : it->second;
+}
+
+extern "C" {
+
+tq_status tq_index_add_ids(tq_index *idx, const float *X_dev, const uint64_t *ids_host,
+                           const uint16_t *tenants_dev, int64_t n, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (!idx->idmap) return fail(TQ_EINVAL, "not an id-map index");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    tq_status st = check_new_ids(idx, ids_host, n);
+    if (st != TQ_OK) return st;
+    const int64_t base = idx->n;
+    st = add_vectors(idx, X_dev, tenants_dev, n, stream);
+    if (st != TQ_OK) return st;
+    return commit_ids(idx, ids_host, base, n, static_cast<hipStream_t>(stream));
+}
+
+tq_status tq_index_add_codes_ids(tq_index *idx, const uint8_t *codes_dev, const float *scales_dev,
+                                 const uint64_t *ids_host, const uint16_t *tenants_dev, int64_t n,
+                                 void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (!idx->idmap) return fail(TQ_EINVAL, "not an id-map index");
+    if (n < 0) return fail(TQ_EINVAL, "n < 0");
+    if (n == 0) return TQ_OK;
+    tq_status st = check_new_ids(idx, ids_host, n);
+    if (st != TQ_OK) return st;
+    const int64_t base = idx->n;
+    st = add_codes_impl(idx, codes_dev, scales_dev, tenants_dev, n, stream);
+    if (st != TQ_OK) return st;
+    return commit_ids(idx, ids_host, base, n, static_cast<hipStream_t>(stream));
+}
+
+tq_status tq_index_remove_ids(tq_index *idx, const uint64_t *ids_host, int64_t n,
+                              int64_t *removed_out) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (!idx->idmap) return fail(TQ_EINVAL, "not an id-map index");
+    if (n < 0 || (n > 0 && !ids_host)) return fail(TQ_EINVAL, "bad id list");
+    std::unordered_map<int64_t, uint64_t> clear;   // block -> slots to retire
+    int64_t removed = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        auto it = idx->slot_of.find(ids_host[i]);
+        if (it == idx->slot_of.end()) continue;
+        const int64_t v = it->second;
+        idx->slot_of.erase(it);
+        clear[v >> 6] |= 1ull << (v & 63);
+        ++removed;
+    }
+    if (removed > 0) {
+        std::vector<int64_t> blocks;
+        std::vector<uint64_t> masks;
+        for (const auto &kv : clear) {
+            blocks.push_back(kv.first);
+            masks.push_back(kv.second);
+        }
+        DevBuf b, m;
+        hipError_t e = b.alloc(blocks.size() * 8);
+        if (e == hipSuccess) e = m.alloc(masks.size() * 8);
+        if (e == hipSuccess) e = hipMemcpy(b.p, blocks.data(), blocks.size() * 8, hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(m.p, masks.data(), masks.size() * 8, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = retire_slots(static_cast<const int64_t *>(b.p), static_cast<const uint64_t *>(m.p),
+                             (int64_t)blocks.size(), idx->live, idx->tenants, idx->W, idx->summ, nullptr);
+        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+        if (e != hipSuccess) return hip_fail(e, "deletion");
+        idx->n_deleted += removed;
+    }
+    if (removed_out) *removed_out = removed;
+    return TQ_OK;
+}
+
+tq_status tq_index_slots(const tq_index *idx, const uint64_t *ids_host, int64_t n,
+                         int64_t *slots_host) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (n < 0 || (n > 0 && (!ids_host || !slots_host))) return fail(TQ_EINVAL, "bad id list");
+    for (int64_t i = 0; i < n; ++i) slots_host[i] = slot_lookup(idx, ids_host[i]);
+    return TQ_OK;
+}
+
+tq_status tq_slot_allowlist(const tq_index *idx, const uint64_t *ids_host,
+                            const int64_t *offsets_host, int64_t nq, uint64_t *bitmap_dev,
+                            void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (nq < 0 || (nq > 0 && (!offsets_host || !bitmap_dev))) return fail(TQ_EINVAL, "bad arguments");
+    if (nq == 0) return TQ_OK;
+    if (offsets_host[0] != 0) return fail(TQ_EINVAL, "offsets must start at 0");
+    for (int64_t q = 0; q < nq; ++q)
+        if (offsets_host[q + 1] < offsets_host[q]) return fail(TQ_EINVAL, "offsets must not decrease");
+    if (offsets_host[nq] > 0 && !ids_host) return fail(TQ_EINVAL, "NULL ids");
+    const int64_t nblk = (idx->n + 63) / 64;
+    std::vector<uint64_t> bm((size_t)(nq * nblk), 0);
+    for (int64_t q = 0; q < nq; ++q)
+        for (int64_t j = offsets_host[q]; j < offsets_host[q + 1]; ++j) {
+            const int64_t v = slot_lookup(idx, ids_host[j]);
+            if (v >= 0) bm[(size_t)(q * nblk + (v >> 6))] |= 1ull << (v & 63);
+        }
+    if (bm.empty()) return TQ_OK;
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(bitmap_dev, bm.data(), bm.size() * 8, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "allowlist upload");
+    return TQ_OK;
+}
+
 tq_status tq_index_size(const tq_index *idx, int64_t *n_out) {
     if (!idx || !n_out) return fail(TQ_EINVAL, "NULL argument");
-    *n_out = idx->n;
+    *n_out = idx->n - idx->n_deleted;
     return TQ_OK;
 }
 
@@ -478,12 +669,13 @@ tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev, float *scales
 }
 
 tq_status tq_index_info(const tq_index *idx, int32_t *d, int32_t *bits, int32_t *n_tenants,
-                        int64_t *n) {
+                        int64_t *n, int32_t *idmap) {
     if (!idx) return fail(TQ_EINVAL, "NULL index");
     if (d) *d = idx->d;
     if (bits) *bits = idx->bits;
     if (n_tenants) *n_tenants = idx->T;
     if (n) *n = idx->n;
+    if (idmap) *idmap = idx->idmap ? 1 : 0;
     return TQ_OK;
 }
 
@@ -493,15 +685,18 @@ namespace {
 
 // ------------------------------------------------------------ persistence
 // File layout (little-endian): FileHeader, then the canonical codes
-// [n][d*bits/8], the scales [n] float32 and the tenant ids [n] uint16, then
-// a 64-bit FNV-1a hash of every preceding byte.
+// [n][d*bits/8], the scales [n] float32 and the tenant ids [n] uint16; for
+// an id-map index (flag 1) the external ids [n] uint64 and the live-slot
+// masks [ceil(n/64)] uint64; then a 64-bit FNV-1a hash of every preceding
+// byte.
 constexpr char kFileMagic[8] = {'T', 'Q', 'I', 'N', 'D', 'E', 'X', '1'};
 constexpr uint32_t kFileVersion = 1;
+constexpr uint32_t kFileIds = 1;
 
 struct FileHeader {
     char magic[8];
     uint32_t version;
-    uint32_t flags;          // no optional sections defined yet: 0
+    uint32_t flags;          // kFileIds: id-map sections present
     int32_t d, bits;
     uint64_t seed;           // rotation seed
     int64_t n;
@@ -525,15 +720,6 @@ struct FileCloser {
     }
 };
 
-// Device scratch released on destruction (synchronous allocation).
-struct DevBuf {
-    void *p = nullptr;
-    hipError_t alloc(size_t bytes) { return hipMalloc(&p, bytes ? bytes : 1); }
-    ~DevBuf() {
-        if (p) (void)hipFree(p);
-    }
-};
-
 }  // namespace
 
 extern "C" {
@@ -545,6 +731,8 @@ tq_status tq_index_save(const tq_index *idx, const char *path) {
     std::vector<uint8_t> codes((size_t)n * cbytes);
     std::vector<float> scales((size_t)n);
     std::vector<uint16_t> ten((size_t)n);
+    const int64_t nb = (n + 63) / 64;
+    std::vector<uint64_t> ext(idx->idmap ? (size_t)n : 0), live(idx->idmap ? (size_t)nb : 0);
     if (n > 0) {
         tq_status st = device_ready();
         if (st != TQ_OK) return st;
@@ -559,12 +747,16 @@ tq_status tq_index_save(const tq_index *idx, const char *path) {
         e = hipMemcpy(codes.data(), c.p, codes.size(), hipMemcpyDeviceToHost);
         if (e == hipSuccess) e = hipMemcpy(scales.data(), sc.p, scales.size() * 4, hipMemcpyDeviceToHost);
         if (e == hipSuccess) e = hipMemcpy(ten.data(), t.p, ten.size() * 2, hipMemcpyDeviceToHost);
+        if (e == hipSuccess && idx->idmap)
+            e = hipMemcpy(ext.data(), idx->ext, ext.size() * 8, hipMemcpyDeviceToHost);
+        if (e == hipSuccess && idx->idmap)
+            e = hipMemcpy(live.data(), idx->live, live.size() * 8, hipMemcpyDeviceToHost);
         if (e != hipSuccess) return hip_fail(e, "index read-back");
     }
     FileHeader h{};
     std::memcpy(h.magic, kFileMagic, 8);
     h.version = kFileVersion;
-    h.flags = 0;
+    h.flags = idx->idmap ? kFileIds : 0;
     h.d = idx->d;
     h.bits = idx->bits;
     h.seed = idx->rot.seed;
@@ -582,6 +774,8 @@ tq_status tq_index_save(const tq_index *idx, const char *path) {
     put(codes.data(), codes.size());
     put(scales.data(), scales.size() * 4);
     put(ten.data(), ten.size() * 2);
+    put(ext.data(), ext.size() * 8);
+    put(live.data(), live.size() * 8);
     const uint64_t sum = fnv.h;
     if (ok && fwrite(&sum, 1, 8, fc.f) != 8) ok = false;
     const int rc = fclose(fc.f);
@@ -607,8 +801,9 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
     get(&h, sizeof h);
     if (!ok || std::memcmp(h.magic, kFileMagic, 8) != 0)
         return fail(TQ_EINVAL, std::string(path) + " is not an index file");
-    if (h.version != kFileVersion || h.flags != 0)
+    if (h.version != kFileVersion || (h.flags & ~kFileIds) != 0)
         return fail(TQ_EUNSUPPORTED, "index file version or sections not supported");
+    const bool ids = (h.flags & kFileIds) != 0;
     if (h.d != cb->t.d || h.bits != cb->t.bits)
         return fail(TQ_EINVAL, "index file d/bits differ from the codebook's");
     if (h.d != rot->d || h.seed != rot->seed)
@@ -617,25 +812,51 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
         return fail(TQ_EINVAL, "index file header out of range");
     const int64_t n = h.n;
     const size_t cbytes = (size_t)h.d * h.bits / 8;
+    const int64_t nb = (n + 63) / 64;
     std::vector<uint8_t> codes;
     std::vector<float> scales;
     std::vector<uint16_t> ten;
+    std::vector<uint64_t> ext, live;
     try {
         codes.resize((size_t)n * cbytes);
         scales.resize((size_t)n);
         ten.resize((size_t)n);
+        if (ids) {
+            ext.resize((size_t)n);
+            live.resize((size_t)nb);
+        }
     } catch (const std::bad_alloc &) {
         return fail(TQ_ENOMEM, "host allocation failed");
     }
     get(codes.data(), codes.size());
     get(scales.data(), scales.size() * 4);
     get(ten.data(), ten.size() * 2);
+    get(ext.data(), ext.size() * 8);
+    get(live.data(), live.size() * 8);
     uint64_t sum = 0;
     if (!ok || fread(&sum, 1, 8, fc.f) != 8) return fail(TQ_EINVAL, std::string(path) + " is truncated");
     if (sum != fnv.h) return fail(TQ_EINVAL, std::string(path) + " fails its checksum");
     if (fgetc(fc.f) != EOF) return fail(TQ_EINVAL, std::string(path) + " has trailing bytes");
+    // the id sections: live bits only on existing slots, live ids distinct
+    std::unordered_map<uint64_t, int64_t> slot_of;
+    int64_t n_live = 0;
+    if (ids) {
+        for (int64_t b = 0; b < nb; ++b) {
+            const int valid = (int)std::min<int64_t>(64, n - b * 64);
+            if (valid < 64 && (live[(size_t)b] >> valid) != 0)
+                return fail(TQ_EINVAL, std::string(path) + ": live bit on a missing slot");
+        }
+        slot_of.reserve((size_t)n);
+        for (int64_t v = 0; v < n; ++v) {
+            if (!((live[(size_t)(v >> 6)] >> (v & 63)) & 1ull)) continue;
+            if (ext[(size_t)v] == UINT64_MAX || !slot_of.emplace(ext[(size_t)v], v).second)
+                return fail(TQ_EINVAL, std::string(path) + ": invalid or repeated live id");
+            ++n_live;
+        }
+    }
     tq_index *x = nullptr;
-    tq_status st = tq_index_create(cb, rot, h.n_tenants, &x);
+    tq_status st = ids ? tq_idmap_create(cb, rot, h.n_tenants, &x)
+                       : tq_index_create(cb, rot, h.n_tenants, &x);
     if (st != TQ_OK) return st;
     if (n > 0) {
         st = index_grow(x, n, nullptr);
@@ -649,9 +870,36 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
             if (e == hipSuccess) e = hipMemcpy(sc.p, scales.data(), scales.size() * 4, hipMemcpyHostToDevice);
             if (e == hipSuccess) e = hipMemcpy(t.p, ten.data(), ten.size() * 2, hipMemcpyHostToDevice);
             st = e != hipSuccess ? hip_fail(e, "index upload")
-                                 : tq_index_add_codes(x, static_cast<const uint8_t *>(c.p),
-                                                      static_cast<const float *>(sc.p),
-                                                      static_cast<const uint16_t *>(t.p), n, nullptr);
+                                 : add_codes_impl(x, static_cast<const uint8_t *>(c.p),
+                                                  static_cast<const float *>(sc.p),
+                                                  static_cast<const uint16_t *>(t.p), n, nullptr);
+        }
+        if (st == TQ_OK && ids) {
+            // ids and live masks as saved; blocks with dead slots get their
+            // summaries rebuilt over the live ones
+            hipError_t e = hipMemcpy(x->ext, ext.data(), ext.size() * 8, hipMemcpyHostToDevice);
+            if (e == hipSuccess) e = hipMemcpy(x->live, live.data(), live.size() * 8, hipMemcpyHostToDevice);
+            std::vector<int64_t> blocks;
+            for (int64_t b = 0; b < nb; ++b) {
+                const int valid = (int)std::min<int64_t>(64, n - b * 64);
+                const uint64_t full = valid == 64 ? ~0ull : ((1ull << valid) - 1);
+                if (live[(size_t)b] != full) blocks.push_back(b);
+            }
+            if (e == hipSuccess && !blocks.empty()) {
+                std::vector<uint64_t> zero(blocks.size(), 0);
+                DevBuf bb, zz;
+                e = bb.alloc(blocks.size() * 8);
+                if (e == hipSuccess) e = zz.alloc(zero.size() * 8);
+                if (e == hipSuccess) e = hipMemcpy(bb.p, blocks.data(), blocks.size() * 8, hipMemcpyHostToDevice);
+                if (e == hipSuccess) e = hipMemcpy(zz.p, zero.data(), zero.size() * 8, hipMemcpyHostToDevice);
+                if (e == hipSuccess)
+                    e = retire_slots(static_cast<const int64_t *>(bb.p), static_cast<const uint64_t *>(zz.p),
+                                     (int64_t)blocks.size(), x->live, x->tenants, x->W, x->summ, nullptr);
+                if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+            }
+            if (e != hipSuccess) st = hip_fail(e, "id upload");
+            x->slot_of.swap(slot_of);
+            x->n_deleted = n - n_live;
         }
         if (st != TQ_OK) {
             tq_index_free(x);
@@ -713,7 +961,7 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
     if (!idx || !bytes_out) return fail(TQ_EINVAL, "NULL argument");
     if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
     if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
-    const int base = path & ~TQ_FLAG_PREROTATED;
+    const int base = path & ~(TQ_FLAG_PREROTATED | TQ_FLAG_SLOT_ALLOW);
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
     if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
@@ -733,7 +981,8 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
     if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
     const bool prerotated = (path & TQ_FLAG_PREROTATED) != 0;
-    const int base = path & ~TQ_FLAG_PREROTATED;
+    const bool slot_allow = (path & TQ_FLAG_SLOT_ALLOW) != 0;
+    const int base = path & ~(TQ_FLAG_PREROTATED | TQ_FLAG_SLOT_ALLOW);
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
     if (nq == 0) return TQ_OK;
@@ -746,6 +995,16 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (base == TQ_PATH_MFMA && !mfma_search_supported(sh, k))
         return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
                                      "k <= 64 and at most 4096 tenants");
+    if (slot_allow && !allow_dev) return fail(TQ_EINVAL, "slot allowlist flag without an allowlist");
+    SearchFilter filter;
+    if (slot_allow)
+        filter.slot_allow = allow_dev;
+    else
+        filter.allow = allow_dev;
+    if (idx->idmap && idx->n_deleted > 0) filter.live = idx->live;
+    if (base == TQ_PATH_MFMA && (filter.live || filter.slot_allow))
+        return fail(TQ_EUNSUPPORTED, "matrix-core path takes tenant allowlists only "
+                                     "(no deleted slots, no slot allowlists)");
     const int grid = scan_grid();
     const size_t need = search_bytes(sh, nq, k, base);
     if (workspace_bytes < need)
@@ -781,12 +1040,17 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
                                    allow_dev, grid, workspace_dev, ids_dev, scores_dev,
                                    &n_fallback, s);
         if (e != hipSuccess) return hip_fail(e, "matrix-core search");
+        if (idx->idmap && (e = map_ids(ids_dev, nq * k, idx->ext, s)) != hipSuccess)
+            return hip_fail(e, "id mapping");
         g_last_fallbacks = n_fallback;
         return TQ_OK;
     }
-    hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev, Qrot, nq, k,
-                   allow_dev, grid, workspace_dev, workspace_bytes, ids_dev, scores_dev, s);
+    hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev,
+                              Qrot, nq, k, filter, grid, workspace_dev, workspace_bytes, ids_dev,
+                              scores_dev, s);
     if (e != hipSuccess) return hip_fail(e, "scan");
+    if (idx->idmap && (e = map_ids(ids_dev, nq * k, idx->ext, s)) != hipSuccess)
+        return hip_fail(e, "id mapping");
     g_last_fallbacks = 0;
     return TQ_OK;
 }

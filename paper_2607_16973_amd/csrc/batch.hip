@@ -814,7 +814,9 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         hipLaunchKernelGGL(gather_allow, dim3(64), dim3(256), 0, stream, allow, rows_d, nr, s.W,
                            allow_c);
     }
-    e = lut_search(s, blocked, scales, tenants, summaries, cents32, qc, nr, k, allow_c, grid,
+    SearchFilter f;
+    f.allow = allow_c;
+    e = lut_search(s, blocked, scales, tenants, summaries, cents32, qc, nr, k, f, grid,
                    w8 + L.lut, lut_search_workspace_bytes(s, nq, k, grid), ids_c, scores_c, stream);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(scatter_results, dim3(256), dim3(256), 0, stream, ids_c, scores_c, rows_d, nr,

@@ -72,6 +72,15 @@ hipError_t add_tenants(const uint16_t *tenants, int64_t n, int64_t base,
                        int n_tenants, int W, uint16_t *tenant_store,
                        uint64_t *summaries, int *status_dev, hipStream_t stream);
 
+// IdMapIndex support (layout.hip).  set_live marks slots [base, base+n)
+// live; retire_slots clears, for each listed block, the slots of its `clear`
+// mask and rebuilds the block's tenant summary over its live slots (W <=
+// 1024); map_ids replaces slot ids >= 0 by ext[slot].
+hipError_t set_live(uint64_t *live, int64_t base, int64_t n, hipStream_t stream);
+hipError_t retire_slots(const int64_t *blocks, const uint64_t *clear, int64_t nb, uint64_t *live,
+                        const uint16_t *tenants, int W, uint64_t *summaries, hipStream_t stream);
+hipError_t map_ids(int64_t *ids, int64_t count, const uint64_t *ext, hipStream_t stream);
+
 // ----------------------------------------------------------------- search
 struct ScanShape {
     int d, bits, chunks;     // code geometry
@@ -81,10 +90,21 @@ struct ScanShape {
 };
 
 size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid);
+// Which slots a search may return: tenant allowlists [nq][W] (null: every
+// tenant), per-block live-slot masks [nblk] (null: no slot deleted) and
+// per-query slot allowlists [nq][nblk] (null: none).  Any non-null member
+// sends the search through the filtered scans.
+struct SearchFilter {
+    const uint64_t *allow = nullptr;
+    const uint64_t *live = nullptr;
+    const uint64_t *slot_allow = nullptr;
+    bool any() const { return allow || live || slot_allow; }
+};
+
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries,
                       const float *cents32, const float *Qrot, int64_t nq, int k,
-                      const uint64_t *allow, int grid, void *ws, size_t ws_bytes,
+                      const SearchFilter &filter, int grid, void *ws, size_t ws_bytes,
                       int64_t *ids, float *scores, hipStream_t stream);
 
 // Batched search of a tile of queries on the matrix cores with exact

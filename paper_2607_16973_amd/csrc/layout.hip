@@ -125,6 +125,48 @@ __global__ void add_tenants_kernel(const uint16_t *__restrict__ tenants, int64_t
     }
 }
 
+// Marks slots [base, base + n) live.
+__global__ void set_live_kernel(unsigned long long *__restrict__ live, int64_t base, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t v = base + i;
+        atomicOr(&live[v >> 6], 1ull << (v & 63));
+    }
+}
+
+// One 64-lane workgroup per listed block: clears the block's slots in
+// `clear` from its live mask, then rebuilds its tenant summary from the
+// slots still live (W words, staged in LDS).
+__global__ __launch_bounds__(64) void retire_kernel(const int64_t *__restrict__ blocks,
+                                                    const uint64_t *__restrict__ clear,
+                                                    uint64_t *__restrict__ live,
+                                                    const uint16_t *__restrict__ tenants, int W,
+                                                    uint64_t *__restrict__ summaries) {
+    __shared__ unsigned long long words[1024];
+    const int64_t b = blocks[blockIdx.x];
+    const int lane = threadIdx.x;
+    const uint64_t m = live[b] & ~clear[blockIdx.x];
+    for (int w = lane; w < W; w += 64) words[w] = 0;
+    __syncthreads();
+    if ((m >> lane) & 1ull) {
+        const int t = tenants[b * 64 + lane];
+        atomicOr(&words[t >> 6], 1ull << (t & 63));
+    }
+    __syncthreads();
+    for (int w = lane; w < W; w += 64) summaries[b * W + w] = words[w];
+    if (lane == 0) live[b] = m;
+}
+
+// Search results in slots -> the slots' external ids (-1 stays -1).
+__global__ void map_ids_kernel(int64_t *__restrict__ ids, int64_t count,
+                               const uint64_t *__restrict__ ext) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t v = ids[i];
+        if (v >= 0) ids[i] = (int64_t)ext[v];
+    }
+}
+
 int grid_for(int64_t items) {
     int64_t g = (items + 255) / 256;
     if (g > 8192) g = 8192;
@@ -162,6 +204,28 @@ hipError_t add_tenants(const uint16_t *tenants, int64_t n, int64_t base, int n_t
     hipLaunchKernelGGL(add_tenants_kernel, dim3(grid_for(n)), dim3(256), 0, stream, tenants, n,
                        base, n_tenants, W, tenant_store,
                        reinterpret_cast<unsigned long long *>(summaries), status_dev);
+    return hipGetLastError();
+}
+
+hipError_t set_live(uint64_t *live, int64_t base, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(set_live_kernel, dim3(grid_for(n)), dim3(256), 0, stream,
+                       reinterpret_cast<unsigned long long *>(live), base, n);
+    return hipGetLastError();
+}
+
+hipError_t retire_slots(const int64_t *blocks, const uint64_t *clear, int64_t nb, uint64_t *live,
+                        const uint16_t *tenants, int W, uint64_t *summaries, hipStream_t stream) {
+    if (nb <= 0) return hipSuccess;
+    if (W > 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(retire_kernel, dim3((unsigned)nb), dim3(64), 0, stream, blocks, clear, live,
+                       tenants, W, summaries);
+    return hipGetLastError();
+}
+
+hipError_t map_ids(int64_t *ids, int64_t count, const uint64_t *ext, hipStream_t stream) {
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(map_ids_kernel, dim3(grid_for(count)), dim3(256), 0, stream, ids, count, ext);
     return hipGetLastError();
 }
 

@@ -45,7 +45,9 @@ struct ScanParams {
     const float *scales;
     const uint16_t *tenants;
     const uint64_t *summaries;
-    const uint64_t *allow;      // [nq][W] or null
+    const uint64_t *allow;      // [nq][W] tenant allowlists, or null: every tenant
+    const uint64_t *live;       // [nblk] live-slot masks (bit v: slot 64b+v not deleted), or null
+    const uint64_t *slot_allow; // [nq][nblk] allowed-slot masks (instead of allow), or null
     const float *qrot;          // [nq][d]
     const float *cents;         // [levels]
     float *cand_s;              // [nq][G][k]
@@ -55,6 +57,15 @@ struct ScanParams {
     int d, bits, chunks, W, k, nq;
     int lut_words;              // 32-bit words of LDS used by the table
 };
+
+// Slots of block b that query qi may return: the live ones (all if no slot
+// was deleted), restricted to the query's allowed slots when slot-level
+// allowlists are given.  Tenant allowlists are tested separately.
+__device__ inline uint64_t block_mask(const ScanParams &p, int qi, int64_t b) {
+    uint64_t m = p.live ? p.live[b] : ~0ull;
+    if (p.slot_allow) m &= p.slot_allow[(int64_t)qi * p.nblk + b];
+    return m;
+}
 
 __device__ inline TableShape table_shape(const ScanParams &p) {
     return TableShape{p.d, p.bits, p.lut_words};
@@ -267,7 +278,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int G = gridDim.x;
     const int g = blockIdx.x;
-    const bool filtered = p.allow != nullptr;
+    const bool filtered = p.allow || p.live || p.slot_allow;
     const int CH = p.chunks;
 
     // contiguous block range of this wave
@@ -278,7 +289,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
     if (tid == 0) misc[2] = 0;
     for (int qi = 0; qi < p.nq; ++qi) {
         const int sh = build_table<MODE>(lds, red, p, p.qrot + (int64_t)qi * p.d);
-        if (filtered)
+        if (p.allow)
             for (int w = tid; w < p.W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)qi * p.W + w];
         if (tid == 0) misc[0] = fkey(-INFINITY);
         __syncthreads();
@@ -290,20 +301,25 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
             // next run of consecutive blocks to scan
             int64_t r0 = blk, r1 = b1;
             if (filtered) {
-                // skip blocks whose tenant summary misses the allowlist, then
-                // extend the run over blocks that meet it
-                for (; r0 < b1; ++r0) {
-                    bool hit = false;
-                    for (int w = lane; w < p.W; w += 64)
-                        hit |= (p.summaries[r0 * p.W + w] & allow_s[w]) != 0;
-                    if (__any(hit)) break;
-                }
-                for (r1 = r0 + 1; r1 < b1; ++r1) {
-                    bool hit = false;
-                    for (int w = lane; w < p.W; w += 64)
-                        hit |= (p.summaries[r1 * p.W + w] & allow_s[w]) != 0;
-                    if (!__any(hit)) break;
-                }
+                // a block is scanned when its tenant summary meets the
+                // allowlist and it holds a live, allowed slot
+                auto listed = [&](int64_t r) {
+                    bool hit = true;
+                    if (p.allow) {
+                        bool h = false;
+                        for (int w = lane; w < p.W; w += 64)
+                            h |= (p.summaries[r * p.W + w] & allow_s[w]) != 0;
+                        hit = __any(h);
+                    }
+                    if (hit && (p.live || p.slot_allow)) hit = block_mask(p, qi, r) != 0;
+                    return hit;
+                };
+                // skip blocks that are not listed, then extend the run over
+                // blocks that are
+                for (; r0 < b1; ++r0)
+                    if (listed(r0)) break;
+                for (r1 = r0 + 1; r1 < b1; ++r1)
+                    if (!listed(r1)) break;
                 if (r0 >= b1) break;
             }
             // stream the run as one sequence of F 16-byte chunks per lane
@@ -328,7 +344,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                 const int64_t vid = b * 64 + lane;
                 const bool inside = vid < p.n;
                 const float scl = p.scales[vid];
-                const int ten = filtered ? (int)p.tenants[vid] : 0;
+                const int ten = p.allow ? (int)p.tenants[vid] : 0;
+                const uint64_t bm = filtered ? block_mask(p, qi, b) : ~0ull;
                 acc_t acc = 0;
                 for (int c0 = 0; c0 < CH; c0 += PF) {
 #pragma unroll
@@ -345,8 +362,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                     }
                 }
                 f += CH;
-                bool ok = inside;
-                if (ok && filtered) ok = (allow_s[ten >> 6] >> (ten & 63)) & 1ull;
+                bool ok = inside && ((bm >> lane) & 1ull);
+                if (ok && p.allow) ok = (allow_s[ten >> 6] >> (ten & 63)) & 1ull;
                 float sc;
                 if constexpr (MODE == NIBBLE)
                     sc = ldexpf((float)acc * scl, -sh);
@@ -597,7 +614,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
         misc[3] = 0;
     }
     if (p.nq == 0) return;
-    for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[w];
+    if (p.allow)
+        for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[w];
     float qv[2][4];
     load_nibble_query(table_shape(p), p.qrot, qv);
     nibble_abs_sum(red, qv);
@@ -614,9 +632,19 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
             if (tid == 0) *nlist = 0;
             __syncthreads();
             for (int t = tid; t < wn; t += SCAN_THREADS) {
-                const uint64_t *sm = p.summaries + (w0 + t) * W;
-                bool hit = false;
-                for (int w = 0; w < W; ++w) hit |= (sm[w] & allow_s[w]) != 0;
+                const int64_t b = w0 + t;
+                bool hit;
+                if (p.slot_allow) {
+                    hit = (block_mask(p, qi, b) != 0);
+                } else {
+                    hit = !p.live || p.live[b] != 0;
+                    if (p.allow) {
+                        const uint64_t *sm = p.summaries + b * W;
+                        bool any = false;
+                        for (int w = 0; w < W; ++w) any |= (sm[w] & allow_s[w]) != 0;
+                        hit = hit && any;
+                    }
+                }
                 if (hit) list[atomicAdd(nlist, 1)] = t;
             }
             __syncthreads();
@@ -652,9 +680,11 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                         const bool last = c0 == CH - 8;
                         float scl = 0.f;
                         int ten = 0, gk = 0;
+                        uint64_t bm = 0;
                         if (last) {
                             scl = p.scales[inside ? vid : 0];
                             ten = p.tenants[inside ? vid : 0];
+                            bm = block_mask(p, qi, blk);
                             gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_AGENT);
                         }
@@ -676,13 +706,15 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                             if (!last) {
                                 scl = p.scales[inside ? vid : 0];
                                 ten = p.tenants[inside ? vid : 0];
+                                bm = block_mask(p, qi, blk);
                                 gk = __hip_atomic_load(p.gbound + qi, __ATOMIC_RELAXED,
                                                        __HIP_MEMORY_SCOPE_AGENT);
                             }
                             const int sum = accb[bl * 64 + lane];
                             accb[bl * 64 + lane] = 0;
                             if (lane == 0) done[bl] = 0;
-                            const bool ok = inside && ((allow_s[ten >> 6] >> (ten & 63)) & 1ull);
+                            const bool ok = inside && ((bm >> lane) & 1ull) &&
+                                            (!p.allow || ((allow_s[ten >> 6] >> (ten & 63)) & 1ull));
                             const float sc = ldexpf((float)sum * scl, -sh);
                             top.offer_seen(ok ? sc : -INFINITY, ok ? (int)vid : INT_MAX, lane, p.k,
                                            misc, p.gbound + qi, gk);
@@ -712,7 +744,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
         }
         if (more) {
             sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
-            for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)(qi + 1) * W + w];
+            if (p.allow)
+                for (int w = tid; w < W; w += SCAN_THREADS)
+                    allow_s[w] = p.allow[(int64_t)(qi + 1) * W + w];
         }
         if (tid == 0) {
             misc[0] = fkey(-INFINITY);
@@ -852,7 +886,7 @@ hipError_t launch_split(const ScanParams &p, int grid, size_t lds, hipStream_t s
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    if (p.allow)
+    if (p.allow || p.live || p.slot_allow)
         hipLaunchKernelGGL(split_filtered_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
     else
         hipLaunchKernelGGL(split_scan_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
@@ -890,9 +924,10 @@ size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int gri
 
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries, const float *cents32,
-                      const float *Qrot, int64_t nq, int k, const uint64_t *allow, int grid,
+                      const float *Qrot, int64_t nq, int k, const SearchFilter &filter, int grid,
                       void *ws, size_t ws_bytes, int64_t *ids, float *scores,
                       hipStream_t stream) {
+    const uint64_t *allow = filter.allow;
     const int64_t qc = query_chunk(s, nq, k, grid);
     uint8_t *p8 = static_cast<uint8_t *>(ws);
     p8 += ((size_t)nq * s.d * sizeof(float) + 255) & ~(size_t)255;   // rotated queries live here
@@ -911,6 +946,8 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.tenants = tenants;
         p.summaries = summaries;
         p.allow = allow ? allow + q0 * s.W : nullptr;
+        p.live = filter.live;
+        p.slot_allow = filter.slot_allow ? filter.slot_allow + q0 * s.nblk : nullptr;
         p.qrot = Qrot + q0 * s.d;
         p.cents = cents32;
         p.cand_s = cand_s;
@@ -925,8 +962,8 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.k = k;
         p.nq = (int)m;
         p.lut_words = lut_words_for(s);
-        const bool split = use_split(s) && lds_bytes_for(s, S, true, allow != nullptr) <= 160 * 1024;
-        const size_t lds = lds_bytes_for(s, S, split, allow != nullptr);
+        const bool split = use_split(s) && lds_bytes_for(s, S, true, filter.any()) <= 160 * 1024;
+        const size_t lds = lds_bytes_for(s, S, split, filter.any());
         hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
                            (int)(0x807FFFFFu));   // order key of -inf
         hipError_t e = hipGetLastError();

@@ -74,3 +74,19 @@ def test_damaged_and_mismatched_files_rejected(parts, tmp_path):
     _expect("TQ_EINVAL", cb, tq.Rotation(256, 6), good, "rotation")
     with pytest.raises(tq.TQError, match="TQ_EINVAL"):
         tq.Index.load(cb, rot, tmp_path / "missing.tq")
+
+
+def test_empty_idmap_index_file(parts, tmp_path):
+    cb, rot = parts
+    path = tmp_path / "idmap.tq"
+    tq.IdMapIndex(cb, rot, n_tenants=2).save(path)
+    data = path.read_bytes()
+    assert HEADER.unpack(data[:HEADER.size])[2] == 1        # flags: id-map sections
+    assert struct.unpack("<Q", data[-8:])[0] == fnv1a64(data[:-8])
+    back = tq.Index.load(cb, rot, path)
+    assert isinstance(back, tq.IdMapIndex) and len(back) == 0
+    body = bytearray(data[:-8])
+    body[12:16] = struct.pack("<I", 3)                      # an undefined section flag
+    bad = tmp_path / "bad.tq"
+    bad.write_bytes(bytes(body) + struct.pack("<Q", fnv1a64(bytes(body))))
+    _expect("TQ_EUNSUPPORTED", cb, rot, bad, "sections")

@@ -120,3 +120,26 @@ def test_hit_and_mrr_properties():
     shifted = np.concatenate([ex[:, 1:4], ex[:, :1], ex[:, 4:]], axis=1)
     assert abs(oracle.mrr_at_k(shifted, ex, 20) - 1 / 4) < 1e-15
     assert oracle.hit_at_k(shifted, ex, 3) == 0.0 and oracle.hit_at_k(shifted, ex, 4) == 1.0
+
+
+def test_search_masks_equal_subset_search():
+    """A per-query position mask (deleted vectors, slot allowlists) gives the
+    search over the masked subset, with ids mapped back."""
+    rng = np.random.default_rng(31)
+    d = 64
+    cb = oracle.lloyd_max(d, 4)
+    R = oracle.haar_rotation(d, 3)[1]
+    X = rng.standard_normal((500, d)).astype(np.float32)
+    codes, _, scales = oracle.encode(X, R, cb)
+    Q = rng.standard_normal((3, d)).astype(np.float32)
+    masks = [rng.random(500) < p for p in (0.5, 0.05, 0.0)]
+    ids, sc = oracle.search(codes, scales, cb.cents, R, Q, 8, masks=masks)
+    for b in range(3):
+        sub = np.nonzero(masks[b])[0]
+        si, ss = oracle.search(codes[sub], scales[sub], cb.cents, R, Q[b:b + 1], 8)
+        valid = si[0] >= 0
+        assert np.array_equal(ids[b][valid], sub[si[0][valid]])
+        assert np.array_equal(ids[b][~valid], si[0][~valid])
+        # the subset's matrix product may sum in another order: last-bit differences
+        assert np.allclose(sc[b], ss[0], rtol=1e-12, atol=0)
+    assert np.all(ids[2] == -1)
