@@ -25,7 +25,7 @@
  *  - Functions that need a GPU return TQ_EDEVICE when none is usable.  The
  *    codebook and rotation constructors are host-only and work without one.
  *  - Sizes: 64 <= d <= 2048 with d % 64 == 0; bits in {1, 2, 3, 4, 8}
- *    (bits == 3 additionally needs d % 128 == 0); k in 1..256.
+ *    (bits == 3 additionally needs d % 128 == 0); k in 1..4096.
  */
 #ifndef TQ_H
 #define TQ_H
@@ -261,6 +261,23 @@ tq_status tq_slot_allowlist(const tq_index *idx, const uint64_t *ids_host,
 tq_status tq_search(const tq_index *idx, const float *Q_dev, int64_t nq,
                     int32_t k, const uint64_t *allow_dev, int64_t *ids_dev,
                     float *scores_dev, void *stream);
+
+/* Large k: for k <= 256 each wave of the scan keeps its best entries in
+ * registers; for 256 < k <= 4096 the scan writes every vector's score (-inf
+ * for filtered ones) to the workspace and a radix selection per query picks
+ * the k best -- same scores, same order and tie rule. */
+
+/* Over-fetch post-filter baseline (section V-C): the unfiltered top
+ * k * overfetch of each query (k * overfetch <= 4096, else TQ_EUNSUPPORTED),
+ * then, in that order, the first k vectors whose tenant the query's
+ * allowlist row allow_dev[q*W .. q*W+W) admits; fewer than k leave padding
+ * (-1, -inf).  This is the comparison method of the paper's filtered-search
+ * study, not a filtered search: allowed vectors outside the over-fetched
+ * list are missed.  Allocates its workspace on `stream` (stream-ordered). */
+tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev,
+                               int64_t nq, int32_t k, int32_t overfetch,
+                               const uint64_t *allow_dev, int64_t *ids_dev,
+                               float *scores_dev, void *stream);
 
 /* Scan path selection for tq_search_ex (section II-B step 5; the batched
  * path is this library's, not the paper's).

@@ -18,14 +18,15 @@ follows:
 * search     -- query rotation, scoring, allowlist filter and top-k,
                 sections II-B step 5 and III-B; exact ground truth and
                 Recall@k as in section IV-A; Hit@k and MRR@20 as in
-                section IV-E.
+                section IV-E; the over-fetch post-filter baseline of
+                section V-C.
 """
 from .marginal import density, tail_prob, cell_mass, cell_first_moment, mse_per_coord
 from .codebook import lloyd_max, Codebook
 from .rotation import splitmix64, uniforms53, gaussians, haar_rotation
 from .encode import encode, pack_codes, unpack_codes, code_bytes_per_vector
 from .search import (rotate_queries, scores_for_ids, search, exact_search,
-                     recall_at_k, hit_at_k, mrr_at_k, allowed_mask)
+                     recall_at_k, hit_at_k, mrr_at_k, allowed_mask, postfilter_search)
 
 __all__ = [
     "density", "tail_prob", "cell_mass", "cell_first_moment", "mse_per_coord",
@@ -33,5 +34,5 @@ __all__ = [
     "splitmix64", "uniforms53", "gaussians", "haar_rotation",
     "encode", "pack_codes", "unpack_codes", "code_bytes_per_vector",
     "rotate_queries", "scores_for_ids", "search", "exact_search",
-    "recall_at_k", "hit_at_k", "mrr_at_k", "allowed_mask",
+    "recall_at_k", "hit_at_k", "mrr_at_k", "allowed_mask", "postfilter_search",
 ]

@@ -166,3 +166,21 @@ def mrr_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int = 20) -> floa
         r = _rank_of_top1(a, e[0], k)
         vals.append(1.0 / r if r else 0.0)
     return float(np.mean(vals)) if vals else float("nan")
+
+
+def postfilter_search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
+                      R32: np.ndarray, Q: np.ndarray, k: int, overfetch: int, tenants,
+                      allow, masks=None):
+    """The over-fetch post-filter baseline of section V-C: the unfiltered top
+    k * overfetch of each query (over the vectors in masks, if given), then,
+    in that order, the first k whose tenant the query's allowlist admits.
+    Returns (ids int64 [nq,k], scores float64 [nq,k]), padded with (-1, -inf)."""
+    ids, sc = search(codes, scales, cents, R32, Q, k * overfetch, masks=masks)
+    out_i = np.full((ids.shape[0], k), -1, dtype=np.int64)
+    out_s = np.full((ids.shape[0], k), -np.inf, dtype=np.float64)
+    for b in range(ids.shape[0]):
+        m = allowed_mask(tenants, allow[b])
+        kept = [(i, v) for i, v in zip(ids[b], sc[b]) if i >= 0 and m[i]][:k]
+        for r, (i, v) in enumerate(kept):
+            out_i[b, r], out_s[b, r] = i, v
+    return out_i, out_s

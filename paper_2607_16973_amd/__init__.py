@@ -266,6 +266,22 @@ class Index:
                                _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
         return ids, scores
 
+    def search_postfilter(self, Q, k: int, overfetch: int, allow):
+        """Over-fetch post-filter baseline (tq_search_postfilter): the
+        unfiltered top k * overfetch, then the first k allowed by `allow`
+        (cuda int64 [nq, words])."""
+        torch = _torch()
+        nq = Q.shape[0]
+        if tuple(allow.shape) != (nq, self.words):
+            raise ValueError("allow must have shape (nq, %d)" % self.words)
+        ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
+        scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        check(lib.tq_search_postfilter(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k, overfetch,
+                                       _dev_ptr(allow, torch.int64, "allow"),
+                                       _dev_ptr(ids, torch.int64, "ids"),
+                                       _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
+        return ids, scores
+
     def search_alloc(self, Q, k: int, allow=None):
         """tq_search: the library allocates its own stream-ordered workspace."""
         torch = _torch()

@@ -64,6 +64,7 @@ def _load():
         "tq_index_load": ([ctypes.c_char_p, P, P, P], ctypes.c_int),
         "tq_index_free": ([P], None),
         "tq_search": ([P, P, I64, I32, P, P, P, P], ctypes.c_int),
+        "tq_search_postfilter": ([P, P, I64, I32, I32, P, P, P, P], ctypes.c_int),
         "tq_search_workspace_size": ([P, I64, I32, I32, P], ctypes.c_int),
         "tq_search_ex": ([P, P, I64, I32, P, I32, P, SZ, P, P, P], ctypes.c_int),
         "tq_last_search_fallbacks": ([], ctypes.c_int32),
@@ -83,7 +84,7 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_index_export", "tq_index_info", "tq_index_save", "tq_index_load",
             "tq_idmap_create", "tq_index_add_ids", "tq_index_add_codes_ids", "tq_index_remove_ids",
             "tq_index_slots", "tq_slot_allowlist",
-            "tq_index_free", "tq_search", "tq_search_workspace_size",
+            "tq_index_free", "tq_search", "tq_search_postfilter", "tq_search_workspace_size",
             "tq_search_ex", "tq_last_search_fallbacks")
 
 

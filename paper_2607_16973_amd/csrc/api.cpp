@@ -960,7 +960,7 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
                                    size_t *bytes_out) {
     if (!idx || !bytes_out) return fail(TQ_EINVAL, "NULL argument");
     if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
-    if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
+    if (k < 1 || k > kMaxK) return fail(TQ_EINVAL, "k must be in 1..4096");
     const int base = path & ~(TQ_FLAG_PREROTATED | TQ_FLAG_SLOT_ALLOW);
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
@@ -979,7 +979,7 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
                        void *stream) {
     if (!idx) return fail(TQ_EINVAL, "NULL index");
     if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
-    if (k < 1 || k > 256) return fail(TQ_EINVAL, "k must be in 1..256");
+    if (k < 1 || k > kMaxK) return fail(TQ_EINVAL, "k must be in 1..4096");
     const bool prerotated = (path & TQ_FLAG_PREROTATED) != 0;
     const bool slot_allow = (path & TQ_FLAG_SLOT_ALLOW) != 0;
     const int base = path & ~(TQ_FLAG_PREROTATED | TQ_FLAG_SLOT_ALLOW);
@@ -1051,6 +1051,60 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (e != hipSuccess) return hip_fail(e, "scan");
     if (idx->idmap && (e = map_ids(ids_dev, nq * k, idx->ext, s)) != hipSuccess)
         return hip_fail(e, "id mapping");
+    g_last_fallbacks = 0;
+    return TQ_OK;
+}
+
+tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev, int64_t nq, int32_t k,
+                               int32_t overfetch, const uint64_t *allow_dev, int64_t *ids_dev,
+                               float *scores_dev, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (nq < 0) return fail(TQ_EINVAL, "nq < 0");
+    if (k < 1 || overfetch < 1) return fail(TQ_EINVAL, "k and overfetch must be positive");
+    if ((int64_t)k * overfetch > kMaxK) return fail(TQ_EUNSUPPORTED, "k * overfetch must be <= 4096");
+    if (nq == 0) return TQ_OK;
+    if (!Q_dev || !allow_dev || !ids_dev || !scores_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    tq_status st = device_ready();
+    if (st != TQ_OK) return st;
+    const int kk = k * overfetch;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (idx->n == 0) {
+        // nothing indexed: every slot is padding
+        std::vector<int64_t> pad_i((size_t)nq * k, -1);
+        std::vector<float> pad_s((size_t)nq * k, -INFINITY);
+        hipError_t e = hipMemcpyAsync(ids_dev, pad_i.data(), pad_i.size() * 8, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(scores_dev, pad_s.data(), pad_s.size() * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "padding copy");
+        return TQ_OK;
+    }
+    const ScanShape sh = shape_of(idx);
+    const int grid = scan_grid();
+    const size_t sbytes = (lut_search_workspace_bytes(sh, nq, kk, grid) + 255) & ~(size_t)255;
+    const size_t tbytes = (size_t)nq * kk * (sizeof(int64_t) + sizeof(float));
+    AsyncBuf ws;
+    hipError_t e = ws.alloc(sbytes + tbytes, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(post-filter workspace)");
+    uint8_t *w8 = static_cast<uint8_t *>(ws.p);
+    int64_t *ids_tmp = reinterpret_cast<int64_t *>(w8 + sbytes);
+    float *sc_tmp = reinterpret_cast<float *>(ids_tmp + (size_t)nq * kk);
+    const float *R = nullptr;
+    st = rotation_dev(&idx->rot, &R);
+    if (st != TQ_OK) return st;
+    float *qr = reinterpret_cast<float *>(w8);
+    e = rotate_rows_f32(Q_dev, nq, idx->d, R, qr, s);
+    if (e != hipSuccess) return hip_fail(e, "query rotation");
+    // the unfiltered top k * overfetch (deleted vectors excluded) ...
+    SearchFilter f;
+    if (idx->idmap && idx->n_deleted > 0) f.live = idx->live;
+    e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev, qr, nq, kk,
+                   f, grid, w8, sbytes, ids_tmp, sc_tmp, s);
+    if (e != hipSuccess) return hip_fail(e, "scan");
+    // ... then the first k whose tenant is allowed
+    e = postfilter(ids_tmp, sc_tmp, nq, kk, idx->tenants, allow_dev, idx->W, k, ids_dev, scores_dev, s);
+    if (e == hipSuccess && idx->idmap) e = map_ids(ids_dev, nq * k, idx->ext, s);
+    if (e != hipSuccess) return hip_fail(e, "post-filter");
     g_last_fallbacks = 0;
     return TQ_OK;
 }

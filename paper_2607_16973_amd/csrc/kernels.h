@@ -81,6 +81,12 @@ hipError_t retire_slots(const int64_t *blocks, const uint64_t *clear, int64_t nb
                         const uint16_t *tenants, int W, uint64_t *summaries, hipStream_t stream);
 hipError_t map_ids(int64_t *ids, int64_t count, const uint64_t *ext, hipStream_t stream);
 
+// Over-fetch post-filter: from lists of kk (slot id, score) in rank order,
+// the first k whose tenant the query's allowlist row admits.
+hipError_t postfilter(const int64_t *ids_in, const float *sc_in, int64_t nq, int kk,
+                      const uint16_t *tenants, const uint64_t *allow, int W, int k,
+                      int64_t *ids_out, float *sc_out, hipStream_t stream);
+
 // ----------------------------------------------------------------- search
 struct ScanShape {
     int d, bits, chunks;     // code geometry
@@ -88,6 +94,11 @@ struct ScanShape {
     int64_t nblk;            // 64-vector blocks
     int W;                   // allowlist words per query
 };
+
+// Largest k of the per-wave top-k scans; larger k (up to kMaxK) scores every
+// vector and selects per query.
+constexpr int kMaxTopK = 256;
+constexpr int kMaxK = 4096;
 
 size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid);
 // Which slots a search may return: tenant allowlists [nq][W] (null: every

@@ -261,7 +261,10 @@ __device__ inline void workgroup_merge(WaveTopK<S> &top, float *stage_s, int *st
     if (threadIdx.x == 0) misc[2] = 0;
 }
 
-template <int MODE, int S, int PF>
+// ALL: no top-k; every vector's score (-inf when the filter drops it) goes to
+// cand_s[qi * n + vid] (vectors of skipped blocks keep what the buffer
+// held: the caller fills it with -inf first).
+template <int MODE, int S, int PF, bool ALL = false>
 __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
     // [0, aux): the table, later the merge stage; then the fixed regions
@@ -369,12 +372,19 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                     sc = ldexpf((float)acc * scl, -sh);
                 else
                     sc = acc * scl;
-                top.offer(ok ? sc : -INFINITY, ok ? (int)vid : INT_MAX, lane, p.k, misc,
-                          p.gbound + qi);
+                if constexpr (ALL) {
+                    if (inside) p.cand_s[(int64_t)qi * p.n + vid] = ok ? sc : -INFINITY;
+                } else {
+                    top.offer(ok ? sc : -INFINITY, ok ? (int)vid : INT_MAX, lane, p.k, misc,
+                              p.gbound + qi);
+                }
             }
             blk = r1;
         }
-        workgroup_merge<S>(top, stage_s, stage_i, misc, wave, lane, p, qi);
+        if constexpr (ALL)
+            __syncthreads();   // every lookup done before the next table is built
+        else
+            workgroup_merge<S>(top, stage_s, stage_i, misc, wave, lane, p, qi);
     }
 }
 
@@ -816,6 +826,168 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
     }
 }
 
+// ---------------------------------------------------------------- large k
+// Top k (kMaxK >= k > kMaxTopK) of a query's n scores by radix selection:
+// scores map to order-preserving unsigned keys (larger score, larger key);
+// three histogram passes over 11, 11 and 10 key bits find the key T of the
+// k-th best; the vectors with a larger key and, in id order, the first ones
+// with key T make up the k best (ties broken by id, as everywhere); a
+// bitonic sort in LDS orders them by (score descending, id ascending).
+// One workgroup of 1024 threads per query.  Entries of score -inf (vectors
+// the filter dropped) become padding (-1, -inf).
+constexpr int SEL_T = 1024;
+
+__device__ inline uint32_t ukey(float f) { return (uint32_t)fkey(f) ^ 0x80000000u; }
+__device__ inline float unukey(uint32_t u) { return unfkey((int)(u ^ 0x80000000u)); }
+
+__global__ __launch_bounds__(SEL_T) void select_topk_kernel(const float *__restrict__ scores,
+                                                           int64_t n, int k,
+                                                           int64_t *__restrict__ ids_out,
+                                                           float *__restrict__ scores_out) {
+    __shared__ uint32_t hist[2048];
+    __shared__ uint64_t cand[kMaxK];          // (key << 32) | (0xFFFFFFFF - id)
+    __shared__ int wave_eq[SEL_T / 64];
+    __shared__ uint32_t sel[4];               // [0] prefix, [1] still needed, [2] candidates
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const float *sc = scores + (int64_t)blockIdx.x * n;
+    const int kk = (int64_t)k < n ? k : (int)n;       // entries to return
+    uint32_t prefix = 0, pmask = 0;
+    uint32_t need = (uint32_t)kk;
+    if (kk > 0) {
+        for (int pass = 0; pass < 3; ++pass) {
+            const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+            const int bins = pass == 2 ? 1024 : 2048;
+            for (int b = tid; b < 2048; b += SEL_T) hist[b] = 0;
+            __syncthreads();
+            for (int64_t i = tid; i < n; i += SEL_T) {
+                const uint32_t u = ukey(sc[i]);
+                if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & (bins - 1)], 1u);
+            }
+            __syncthreads();
+            if (tid == 0) {
+                // bin of the need-th largest key within the prefix class
+                uint32_t above = 0;
+                int b = bins - 1;
+                for (; b > 0; --b) {
+                    if (above + hist[b] >= need) break;
+                    above += hist[b];
+                }
+                sel[0] = prefix | ((uint32_t)b << shift);
+                sel[1] = need - above;
+            }
+            __syncthreads();
+            prefix = sel[0];
+            need = sel[1];
+            pmask |= (uint32_t)(bins - 1) << shift;
+            __syncthreads();
+        }
+    }
+    // prefix is now the key T of the kk-th best; `need` of the keys equal to
+    // T are taken, the ones with the smallest ids
+    const uint32_t T = prefix;
+    const int64_t len = ((n + SEL_T / 64 - 1) / (SEL_T / 64) + 63) / 64 * 64;   // per wave
+    const int64_t w0 = wave * len, w1 = w0 + len < n ? w0 + len : n;
+    int eq = 0;
+    if (kk > 0)
+        for (int64_t i = w0 + lane; i < w1; i += 64) eq += ukey(sc[i]) == T;
+    for (int m = 32; m > 0; m >>= 1) eq += __shfl_xor(eq, m, 64);
+    if (lane == 0) wave_eq[wave] = eq;
+    if (tid == 0) sel[2] = 0;
+    __syncthreads();
+    if (kk > 0) {
+        int before = 0;
+        for (int w = 0; w < wave; ++w) before += wave_eq[w];
+        for (int64_t i0 = w0; i0 < w1; i0 += 64) {
+            const int64_t i = i0 + lane;
+            const uint32_t u = i < w1 ? ukey(sc[i]) : 0u;
+            const bool is_eq = i < w1 && u == T;
+            const uint64_t m = __ballot(is_eq);
+            const int rank = before + __popcll(m & ((1ull << lane) - 1));
+            const bool take = (i < w1 && u > T) || (is_eq && rank < (int)need);
+            if (take) {
+                const uint32_t at = atomicAdd(&sel[2], 1u);
+                cand[at] = ((uint64_t)u << 32) | (0xFFFFFFFFu - (uint32_t)i);
+            }
+            before += __popcll(m);
+        }
+    }
+    __syncthreads();
+    // pad to a power of two and sort descending
+    int P = 1;
+    while (P < kk) P <<= 1;
+    for (int e = kk + tid; e < P; e += SEL_T) cand[e] = 0;
+    __syncthreads();
+    for (int size = 2; size <= P; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int e = tid; e < P / 2; e += SEL_T) {
+                const int lo = 2 * e - (e & (stride - 1));
+                const int hi = lo + stride;
+                const bool desc = (lo & size) == 0;
+                const uint64_t a = cand[lo], b = cand[hi];
+                if ((a < b) == desc) {
+                    cand[lo] = b;
+                    cand[hi] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    int64_t *io = ids_out + (int64_t)blockIdx.x * k;
+    float *so = scores_out + (int64_t)blockIdx.x * k;
+    for (int r = tid; r < k; r += SEL_T) {
+        int64_t id = -1;
+        float s = -INFINITY;
+        if (r < kk) {
+            const float v = unukey((uint32_t)(cand[r] >> 32));
+            if (v > -INFINITY) {
+                s = v;
+                id = (int64_t)(0xFFFFFFFFu - (uint32_t)(cand[r] & 0xFFFFFFFFu));
+            }
+        }
+        io[r] = id;
+        so[r] = s;
+    }
+}
+
+// Over-fetch post-filter (section V-C baseline): from each query's list of
+// kk entries in rank order, the first k whose tenant the query's allowlist
+// admits (padding -1 / -inf after them).  One wave per query.
+__global__ __launch_bounds__(64) void postfilter_kernel(const int64_t *__restrict__ ids_in,
+                                                       const float *__restrict__ sc_in, int kk,
+                                                       const uint16_t *__restrict__ tenants,
+                                                       const uint64_t *__restrict__ allow, int W,
+                                                       int k, int64_t *__restrict__ ids_out,
+                                                       float *__restrict__ sc_out) {
+    const int q = blockIdx.x, lane = threadIdx.x;
+    const int64_t *ii = ids_in + (int64_t)q * kk;
+    const float *ss = sc_in + (int64_t)q * kk;
+    const uint64_t *al = allow + (int64_t)q * W;
+    int64_t *io = ids_out + (int64_t)q * k;
+    float *so = sc_out + (int64_t)q * k;
+    int kept = 0;
+    for (int r0 = 0; r0 < kk && kept < k; r0 += 64) {
+        const int r = r0 + lane;
+        const int64_t id = r < kk ? ii[r] : -1;
+        bool keep = false;
+        if (id >= 0) {
+            const int t = tenants[id];
+            keep = (al[t >> 6] >> (t & 63)) & 1ull;
+        }
+        const uint64_t m = __ballot(keep);
+        const int pos = kept + __popcll(m & ((1ull << lane) - 1));
+        if (keep && pos < k) {
+            io[pos] = id;
+            so[pos] = ss[r];
+        }
+        kept += __popcll(m);
+    }
+    for (int r = (kept < k ? kept : k) + lane; r < k; r += 64) {
+        io[r] = -1;
+        so[r] = -INFINITY;
+    }
+}
+
 int lut_words_for(const ScanShape &s) {
     if (s.bits == 8) return 256 + s.d;
     if (s.bits == 3) return s.chunks * 40 * 8;
@@ -852,16 +1024,16 @@ int64_t query_chunk(const ScanShape &s, int64_t nq, int k, int grid) {
     return nq < qc ? nq : qc;
 }
 
-template <int MODE, int S, int PF>
+template <int MODE, int S, int PF, bool ALL = false>
 hipError_t launch_scan(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<MODE, S, PF>,
+        hipError_t e = hipFuncSetAttribute((const void *)scan_kernel<MODE, S, PF, ALL>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((scan_kernel<MODE, S, PF>), dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+    hipLaunchKernelGGL((scan_kernel<MODE, S, PF, ALL>), dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
     return hipGetLastError();
 }
 
@@ -872,6 +1044,15 @@ hipError_t launch_scan_pf(const ScanParams &p, int grid, size_t lds, hipStream_t
     if (p.chunks % 4 == 0) return launch_scan<MODE, S, 4>(p, grid, lds, stream);
     if (p.chunks % 2 == 0) return launch_scan<MODE, S, 2>(p, grid, lds, stream);
     return launch_scan<MODE, S, 1>(p, grid, lds, stream);
+}
+
+// The all-scores scan (large k), prefetching 8 chunks when the count allows.
+template <int MODE>
+hipError_t launch_scan_all(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
+    if (p.chunks % 8 == 0) return launch_scan<MODE, 1, 8, true>(p, grid, lds, stream);
+    if (p.chunks % 4 == 0) return launch_scan<MODE, 1, 4, true>(p, grid, lds, stream);
+    if (p.chunks % 2 == 0) return launch_scan<MODE, 1, 2, true>(p, grid, lds, stream);
+    return launch_scan<MODE, 1, 1, true>(p, grid, lds, stream);
 }
 
 template <int S>
@@ -911,7 +1092,23 @@ int device_cu_count() {
     return cus;
 }
 
+// Queries per launch of the large-k path: their scores (n floats each) fill
+// at most 256 MiB.
+int64_t all_scores_chunk(const ScanShape &s, int64_t nq) {
+    const int64_t per = (s.n > 0 ? s.n : 1) * (int64_t)sizeof(float);
+    int64_t qc = ((int64_t)256 << 20) / per;
+    if (qc < 1) qc = 1;
+    return nq < qc ? nq : qc;
+}
+
 size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int grid) {
+    if (k > kMaxTopK) {
+        size_t b = (size_t)nq * s.d * sizeof(float);
+        b = (b + 255) & ~(size_t)255;
+        b += (size_t)all_scores_chunk(s, nq) * (s.n > 0 ? s.n : 1) * sizeof(float);
+        b = (b + 255) & ~(size_t)255;
+        return b + 256;
+    }
     const int64_t qc = query_chunk(s, nq, k, grid);
     size_t b = (size_t)nq * s.d * sizeof(float);
     b = (b + 255) & ~(size_t)255;
@@ -937,6 +1134,51 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
     int *gbound = reinterpret_cast<int *>(
         (reinterpret_cast<uintptr_t>(after) + 255) & ~(uintptr_t)255);
     (void)ws_bytes;
+    if (k > kMaxTopK) {
+        // every score, then a radix selection per query
+        float *all = reinterpret_cast<float *>(p8);
+        const int64_t qa = all_scores_chunk(s, nq);
+        const size_t lds = lds_bytes_for(s, 1, false, filter.any());
+        for (int64_t q0 = 0; q0 < nq; q0 += qa) {
+            const int64_t m = (nq - q0) < qa ? (nq - q0) : qa;
+            ScanParams p{};
+            p.codes = reinterpret_cast<const uint4 *>(blocked);
+            p.scales = scales;
+            p.tenants = tenants;
+            p.summaries = summaries;
+            p.allow = allow ? allow + q0 * s.W : nullptr;
+            p.live = filter.live;
+            p.slot_allow = filter.slot_allow ? filter.slot_allow + q0 * s.nblk : nullptr;
+            p.qrot = Qrot + q0 * s.d;
+            p.cents = cents32;
+            p.cand_s = all;
+            p.n = s.n;
+            p.nblk = s.nblk;
+            p.d = s.d;
+            p.bits = s.bits;
+            p.chunks = s.chunks;
+            p.W = s.W;
+            p.k = k;
+            p.nq = (int)m;
+            p.lut_words = lut_words_for(s);
+            hipLaunchKernelGGL(fill_keys, dim3(1024), dim3(256), 0, stream,
+                               reinterpret_cast<int *>(all), m * s.n, (int)0xFF800000u);   // -inf
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            if (s.bits == 8)
+                e = launch_scan_all<BYTE>(p, grid, lds, stream);
+            else if (s.bits == 3)
+                e = launch_scan_all<TRIBIT>(p, grid, lds, stream);
+            else
+                e = launch_scan_all<NIBBLE>(p, grid, lds, stream);
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)m), dim3(SEL_T), 0, stream, all,
+                               s.n, k, ids + q0 * k, scores + q0 * k);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
     const int S = k <= 64 ? 1 : (k <= 128 ? 2 : 4);
     for (int64_t q0 = 0; q0 < nq; q0 += qc) {
         const int64_t m = (nq - q0) < qc ? (nq - q0) : qc;
@@ -988,6 +1230,15 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t postfilter(const int64_t *ids_in, const float *sc_in, int64_t nq, int kk,
+                      const uint16_t *tenants, const uint64_t *allow, int W, int k,
+                      int64_t *ids_out, float *sc_out, hipStream_t stream) {
+    if (nq <= 0) return hipSuccess;
+    hipLaunchKernelGGL(postfilter_kernel, dim3((unsigned)nq), dim3(64), 0, stream, ids_in, sc_in, kk,
+                       tenants, allow, W, k, ids_out, sc_out);
+    return hipGetLastError();
 }
 
 }  // namespace tq

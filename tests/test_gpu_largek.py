@@ -1,0 +1,136 @@
+"""GPU parity of searches with 256 < k <= 4096 (every score written, then a
+radix selection per query) and of the over-fetch post-filter baseline of
+section V-C (the unfiltered top k * overfetch, then the first k allowed),
+against the oracle on the small workload."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.conftest import gpu_available
+from tests.parity import check_topk
+
+pytestmark = pytest.mark.gpu
+if not gpu_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import torch  # noqa: E402
+
+import paper_2607_16973_amd as tq  # noqa: E402
+
+D = 1536
+
+
+@pytest.fixture(scope="module")
+def env(small_env):
+    return small_env
+
+
+def ref(s, k, tenants=None, bm=None, masks=None):
+    return oracle.search(s.codes, s.scales, s.ocb.cents, s.R32, s.Q, k, tenants, bm, masks=masks)
+
+
+@pytest.mark.parametrize("k", [257, 1000, 4096])
+def test_large_k_matches_oracle(env, k):
+    print("large k=%d" % k, flush=True)
+    ids, sc = env.idx.search(env.Qd, k)
+    ref_i, ref_s = ref(env, k)
+    got = ids.cpu().numpy()
+    check_topk(got, sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents, env.qrot, env.qn, k,
+               ref_i, ref_s)
+    # with k in the thousands some list differs from the oracle's by a swap of
+    # scores tied within the tolerance (which check_topk allows); the sets
+    # stay almost equal
+    overlap = np.mean([len(set(a) & set(b)) / k for a, b in zip(got, ref_i)])
+    assert overlap >= 0.99, overlap
+
+
+def test_large_k_extends_small_k(env):
+    """Both selections order by (score desc, id asc) over the same scores:
+    the first 256 entries of k = 4096 are the k = 256 list."""
+    a_i, a_s = env.idx.search(env.Qd, 256)
+    b_i, b_s = env.idx.search(env.Qd, 4096)
+    assert torch.equal(a_i, b_i[:, :256]) and torch.equal(a_s, b_s[:, :256])
+
+
+def test_large_k_filtered(env):
+    n, T, nq = env.X.shape[0], 100, env.Q.shape[0]
+    ten = synth.zipf_tenants(n, T, seed=44)
+    idx = tq.Index(env.cb, env.rot, n_tenants=T)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(env.codes, 4)).cuda(),
+                  torch.from_numpy(env.scales).cuda(), torch.from_numpy(ten.view(np.int16)).cuda())
+    for mode in ("selective", "broad"):
+        print("large k filtered %s" % mode, flush=True)
+        bm = synth.allowlist_bitmap(synth.allowlists(nq, T, mode, seed=45), T)
+        ids, sc = idx.search(env.Qd, 600, allow=torch.from_numpy(bm.view(np.int64)).cuda())
+        ref_i, ref_s = ref(env, 600, ten, bm)
+        masks = [oracle.allowed_mask(ten, bm[b]) for b in range(nq)]
+        check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents,
+                   env.qrot, env.qn, 600, ref_i, ref_s, allowed=masks)
+    # slot allowlists
+    rng = np.random.default_rng(71)
+    masks = [rng.random(n) < 0.05 for _ in range(nq)]
+    sa = idx.slot_allowlist([np.nonzero(m)[0].astype(np.uint64) for m in masks])
+    ids, sc = idx.search(env.Qd, 300, slot_allow=sa)
+    ref_i, ref_s = ref(env, 300, masks=masks)
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), env.codes, env.scales, env.ocb.cents,
+               env.qrot, env.qn, 300, ref_i, ref_s, allowed=masks)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 8])
+def test_large_k_other_bit_widths(env, bits):
+    print("large k bits=%d" % bits, flush=True)
+    n = 2000
+    ocb = oracle.lloyd_max(D, bits)
+    codes, _, scales = oracle.encode(env.X[:n], env.R32, ocb)
+    idx = tq.Index(tq.Codebook(D, bits), env.rot, n_tenants=1)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
+                  torch.from_numpy(scales).cuda())
+    ids, sc = idx.search(env.Qd, 700)
+    ref_i, ref_s = oracle.search(codes, scales, ocb.cents, env.R32, env.Q, 700)
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, env.qrot, env.qn, 700,
+               ref_i, ref_s, n=n)
+
+
+@pytest.mark.parametrize("T,overfetch", [(10, 1), (100, 10), (1000, 100), (100, 3)])
+def test_postfilter_matches_oracle(env, T, overfetch):
+    print("post-filter T=%d overfetch=%d" % (T, overfetch), flush=True)
+    n, nq, k = env.X.shape[0], env.Q.shape[0], 10
+    ten = synth.uniform_partition_tenants(n, T, seed=44)
+    idx = tq.Index(env.cb, env.rot, n_tenants=T)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(env.codes, 4)).cuda(),
+                  torch.from_numpy(env.scales).cuda(), torch.from_numpy(ten.view(np.int16)).cuda())
+    bm = synth.allowlist_bitmap(synth.allowlists(nq, T, "selective", seed=45), T)
+    ids, sc = idx.search_postfilter(env.Qd, k, overfetch, torch.from_numpy(bm.view(np.int64)).cuda())
+    ref_i, ref_s = oracle.postfilter_search(env.codes, env.scales, env.ocb.cents, env.R32, env.Q, k,
+                                            overfetch, ten, bm)
+    gi, gs = ids.cpu().numpy(), sc.cpu().numpy().astype(np.float64)
+    valid = ref_i >= 0
+    assert np.array_equal(gi >= 0, valid)
+    # scores within the tolerance, ids equal except where scores tie at the cut
+    tol = np.maximum(1e-4 * np.abs(ref_s[valid]), 1e-6 * np.repeat(env.qn, k).reshape(nq, k)[valid])
+    assert np.all(np.abs(gs[valid] - ref_s[valid]) <= tol)
+    assert np.mean(np.all(gi == ref_i, axis=1)) >= 0.9
+    m = np.array([[oracle.allowed_mask(ten, bm[b])[i] if i >= 0 else True for i in gi[b]]
+                  for b in range(nq)])
+    assert np.all(m), "post-filter returned a disallowed vector"
+
+
+def test_postfilter_on_idmap_with_deletions(env):
+    n, T, nq = env.X.shape[0], 10, env.Q.shape[0]
+    ten = synth.uniform_partition_tenants(n, T, seed=44)
+    ids = np.arange(n, dtype=np.uint64) * np.uint64(7) + np.uint64(3)
+    idx = tq.IdMapIndex(env.cb, env.rot, n_tenants=T)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(env.codes, 4)).cuda(),
+                  torch.from_numpy(env.scales).cuda(), ids, torch.from_numpy(ten.view(np.int16)).cuda())
+    kill = np.random.default_rng(72).choice(n, 4000, replace=False)
+    idx.remove(ids[kill])
+    live = np.ones(n, dtype=bool)
+    live[kill] = False
+    bm = synth.allowlist_bitmap(synth.allowlists(nq, T, "selective", seed=45), T)
+    got, _ = idx.search_postfilter(env.Qd, 10, 1, torch.from_numpy(bm.view(np.int64)).cuda())
+    ref_i, _ = oracle.postfilter_search(env.codes, env.scales, env.ocb.cents, env.R32, env.Q, 10, 1,
+                                        ten, bm, masks=[live] * nq)
+    g = got.cpu().numpy().view(np.uint64)
+    want = np.where(ref_i >= 0, ids[np.maximum(ref_i, 0)], np.uint64(2**64 - 1))
+    assert np.mean(np.all(g == want, axis=1)) >= 0.9

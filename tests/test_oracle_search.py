@@ -143,3 +143,32 @@ def test_search_masks_equal_subset_search():
         # the subset's matrix product may sum in another order: last-bit differences
         assert np.allclose(sc[b], ss[0], rtol=1e-12, atol=0)
     assert np.all(ids[2] == -1)
+
+
+def test_postfilter_baseline():
+    """The over-fetch post-filter of section V-C: with every tenant allowed
+    it is the plain search; on a hand-made case it keeps, in rank order, the
+    allowed vectors of the over-fetched list only."""
+    rng = np.random.default_rng(41)
+    d = 64
+    cb = oracle.lloyd_max(d, 4)
+    R = oracle.haar_rotation(d, 3)[1]
+    X = rng.standard_normal((400, d)).astype(np.float32)
+    codes, _, scales = oracle.encode(X, R, cb)
+    Q = rng.standard_normal((4, d)).astype(np.float32)
+    ten = (np.arange(400) % 4).astype(np.uint16)
+    everyone = np.full((4, 1), 0b1111, dtype=np.uint64)
+    a_i, a_s = oracle.postfilter_search(codes, scales, cb.cents, R, Q, 5, 3, ten, everyone)
+    b_i, b_s = oracle.search(codes, scales, cb.cents, R, Q, 5)
+    assert np.array_equal(a_i, b_i) and np.array_equal(a_s, b_s)
+    # tenant 2 only, over-fetch 3: the tenant-2 members of the top 15, first 5
+    only2 = np.full((4, 1), 0b0100, dtype=np.uint64)
+    p_i, _ = oracle.postfilter_search(codes, scales, cb.cents, R, Q, 5, 3, ten, only2)
+    top15, _ = oracle.search(codes, scales, cb.cents, R, Q, 15)
+    for b in range(4):
+        want = [i for i in top15[b] if ten[i] == 2][:5]
+        assert list(p_i[b][:len(want)]) == want and np.all(p_i[b][len(want):] == -1)
+    # an over-fetch that covers the corpus gives the filtered search
+    f_i, _ = oracle.postfilter_search(codes, scales, cb.cents, R, Q, 5, 80, ten, only2)
+    g_i, _ = oracle.search(codes, scales, cb.cents, R, Q, 5, ten, only2)
+    assert np.array_equal(f_i, g_i)
