@@ -127,6 +127,62 @@ def filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev, T=100):
     return out
 
 
+def filter_study(tq, synth, cb, rot, d, k, dev, stream):
+    """The filtered-search comparison of section V-C on synthetic data: 100K
+    power-law vectors in T equal tenant partitions (T = 10, 100, 1000), each
+    of the 1,000 queries restricted to one tenant.  Kernel allowlists
+    against the over-fetch post-filter baseline (factor T/10): Recall@10
+    against exact float32 filtered search, and the median latency of a
+    single-query call."""
+    import numpy as np
+    import torch
+    X_np, Q_np = synth.workload("powerlaw100k", d=d)
+    X = torch.from_numpy(X_np).to(dev)
+    Q = torch.from_numpy(Q_np).to(dev)
+    n, nq = X.shape[0], Q.shape[0]
+    G = Q @ X.T                                   # exact float32 inner products
+    out = {"n": n, "queries": nq, "k": k}
+    for T in (10, 100, 1000):
+        ten = synth.uniform_partition_tenants(n, T, seed=44)
+        allowed = synth.allowlists(nq, T, "selective", seed=45)
+        bm = torch.from_numpy(synth.allowlist_bitmap(allowed, T).view(np.int64)).to(dev)
+        idx = tq.Index(cb, rot, n_tenants=T)
+        idx.add(X, torch.from_numpy(ten.view(np.int16)).to(dev))
+        qt = torch.tensor([int(a[0]) for a in allowed], device=dev)
+        mask = torch.from_numpy(ten.astype(np.int64)).to(dev)[None, :] == qt[:, None]
+        exact = torch.topk(G.masked_fill(~mask, float("-inf")), k, dim=1).indices.cpu().numpy()
+        f = max(1, T // 10)
+
+        def rec(ids):
+            return float(np.mean([len(set(a[a >= 0].tolist()) & set(b.tolist())) / k
+                                  for a, b in zip(ids.cpu().numpy(), exact)]))
+
+        def lat(fn):
+            ts = []
+            for i in range(35):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                fn(i)
+                b.record(stream)
+                torch.cuda.synchronize()
+                if i >= 5:
+                    ts.append(a.elapsed_time(b))
+            return float(np.median(ts))
+        ia, _ = idx.search(Q, k, allow=bm)
+        ip, _ = idx.search_postfilter(Q, k, f, bm)
+        la = lat(lambda i: idx.search(Q[i:i + 1], k, allow=bm[i:i + 1]))
+        lp = lat(lambda i: idx.search_postfilter(Q[i:i + 1], k, f, bm[i:i + 1]))
+        out["T%d" % T] = {"allowlist": {"recall_at_10": rec(ia), "latency_ms_p50": la},
+                          "overfetch_postfilter": {"overfetch": f, "recall_at_10": rec(ip),
+                                                   "latency_ms_p50": lp}}
+        log("filter study T=%d: allowlist R@10 %.3f %.3f ms; post-filter (x%d) R@10 %.3f %.3f ms"
+            % (T, rec(ia), la, f, rec(ip), lp))
+        del idx
+    del G, X
+    torch.cuda.empty_cache()
+    return out
+
+
 def bit_sweep(tq, rot, X, Qrot, k, n, d, stream):
     """Encode throughput (rotation GEMM + quantise + pack) and single-query
     search throughput at each bit width."""
@@ -326,6 +382,7 @@ def main() -> int:
         log("recall@%d %.4f  single-query latency %.3f ms" % (k, rec, extra["single_query_latency_ms_p50"]))
         extra["batched_mfma"] = batched_path(tq, idx, Qrot, k, ids, scores, ex_ids, nr)
         extra["filtered_T100"] = filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev)
+        extra["filter_study_100k"] = filter_study(tq, synth, cb, rot, d, k, dev, stream)
     if args.sweep:
         extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
     del X
