@@ -14,7 +14,8 @@ follows:
 * codebook   -- analytic Lloyd-Max boundaries/centroids, section II-B step 3.
 * rotation   -- the seeded random orthogonal matrix, section II-B step 2.
 * encode     -- normalise / rotate / quantise / pack / length-renormalise,
-                section II-B steps 1-5 (sequential float64 arithmetic in C).
+                section II-B steps 1-5 (sequential float64 arithmetic in C);
+                the optional TQ+ calibration of section II-B.
 * search     -- query rotation, scoring, allowlist filter and top-k,
                 sections II-B step 5 and III-B; exact ground truth and
                 Recall@k as in section IV-A; Hit@k and MRR@20 as in
@@ -24,7 +25,8 @@ follows:
 from .marginal import density, tail_prob, cell_mass, cell_first_moment, mse_per_coord
 from .codebook import lloyd_max, Codebook
 from .rotation import splitmix64, uniforms53, gaussians, haar_rotation
-from .encode import encode, pack_codes, unpack_codes, code_bytes_per_vector
+from .encode import (encode, pack_codes, unpack_codes, code_bytes_per_vector, tqplus_fit,
+                     encode_tqplus)
 from .search import (rotate_queries, scores_for_ids, search, exact_search,
                      recall_at_k, hit_at_k, mrr_at_k, allowed_mask, postfilter_search)
 
@@ -32,7 +34,7 @@ __all__ = [
     "density", "tail_prob", "cell_mass", "cell_first_moment", "mse_per_coord",
     "lloyd_max", "Codebook",
     "splitmix64", "uniforms53", "gaussians", "haar_rotation",
-    "encode", "pack_codes", "unpack_codes", "code_bytes_per_vector",
+    "encode", "pack_codes", "unpack_codes", "code_bytes_per_vector", "tqplus_fit", "encode_tqplus",
     "rotate_queries", "scores_for_ids", "search", "exact_search",
     "recall_at_k", "hit_at_k", "mrr_at_k", "allowed_mask", "postfilter_search",
 ]

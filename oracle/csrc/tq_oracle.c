@@ -129,3 +129,118 @@ int tqo_scales(const uint8_t *codes, const double *norms, int64_t n, int32_t d,
     }
     return 0;
 }
+
+/* TQ+ calibration (section II-B): per-coordinate shift mu_j and spread
+ * kappa_j (float32, as stored by an index) move the thresholds of coordinate
+ * j to a_jt = fl64(mu_j + fl64(kappa_j t_t)); coordinate j of a vector of
+ * norm n gets code #{t : fl64(a_jt n) <= S_j}, S_j the sequential float64
+ * dot product of tqo_encode.  mu = 0, kappa = 1 is tqo_encode. */
+int tqo_encode_plus(const float *X, int64_t n, int32_t d, const float *R,
+                    const double *bounds, int32_t L, const float *mu,
+                    const float *kappa, uint8_t *codes, double *norm_out)
+{
+    if (!X || !R || !bounds || !mu || !kappa || !codes || n < 0 || d <= 0 || L < 2 || L > 256)
+        return -1;
+    double *A = (double *)malloc(sizeof(double) * (size_t)d * (size_t)(L - 1));
+    double *RT = (double *)malloc(sizeof(double) * (size_t)d * (size_t)d);
+    if (!A || !RT) {
+        free(A);
+        free(RT);
+        return -1;
+    }
+    for (int32_t j = 0; j < d; ++j)
+        for (int32_t t = 0; t < L - 1; ++t) {
+            double p = (double)kappa[j] * bounds[t];
+            double a = (double)mu[j] + p;
+            A[(size_t)j * (L - 1) + t] = a;
+        }
+    for (int32_t j = 0; j < d; ++j)
+        for (int32_t k = 0; k < d; ++k)
+            RT[(size_t)k * d + j] = (double)R[(size_t)j * d + k];
+    int status = 0;
+#pragma omp parallel
+    {
+        double *S = (double *)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            const float *x = X + (size_t)i * d;
+            uint8_t *c = codes + (size_t)i * d;
+            int finite = 1;
+            double n2 = 0.0;
+            for (int32_t k = 0; k < d; ++k) {
+                double xk = (double)x[k];
+                if (!isfinite(xk)) finite = 0;
+                double sq = xk * xk;
+                n2 = n2 + sq;
+            }
+            if (!finite) {
+#pragma omp critical
+                status = -2;
+                continue;
+            }
+            double nrm = sqrt(n2);
+            if (norm_out) norm_out[i] = nrm;
+            if (nrm == 0.0) {
+                memset(c, L / 2, (size_t)d);
+                continue;
+            }
+            for (int32_t j = 0; j < d; ++j) S[j] = 0.0;
+            for (int32_t k = 0; k < d; ++k) {
+                const double xk = (double)x[k];
+                const double *col = RT + (size_t)k * d;
+                for (int32_t j = 0; j < d; ++j) {
+                    double prod = col[j] * xk;
+                    S[j] = S[j] + prod;
+                }
+            }
+            for (int32_t j = 0; j < d; ++j) {
+                int cnt = 0;
+                const double *a = A + (size_t)j * (L - 1);
+                for (int32_t t = 0; t < L - 1; ++t) {
+                    double thr = a[t] * nrm;
+                    cnt += (thr <= S[j]);
+                }
+                c[j] = (uint8_t)cnt;
+            }
+        }
+        free(S);
+    }
+    free(A);
+    free(RT);
+    return status;
+}
+
+/* TQ+ scales: the reconstruction of coordinate j is
+ * yhat_j = fl64(mu_j + fl64(kappa_j c[code_j])) and s = n / sqrt(sum_j
+ * fl64(yhat_j^2)) (sequential over j, float32 result); mu = 0, kappa = 1 is
+ * tqo_scales. */
+int tqo_scales_plus(const uint8_t *codes, const double *norms, int64_t n, int32_t d,
+                    const double *cents, int32_t L, const float *mu, const float *kappa,
+                    float *scale_out)
+{
+    if (!codes || !norms || !cents || !mu || !kappa || !scale_out || n < 0 || d <= 0 || L < 2)
+        return -1;
+    double *Y2 = (double *)malloc(sizeof(double) * (size_t)d * (size_t)L);
+    if (!Y2) return -1;
+    for (int32_t j = 0; j < d; ++j)
+        for (int32_t c = 0; c < L; ++c) {
+            double p = (double)kappa[j] * cents[c];
+            double y = (double)mu[j] + p;
+            double y2 = y * y;
+            Y2[(size_t)j * L + c] = y2;
+        }
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const uint8_t *c = codes + (size_t)i * d;
+        if (norms[i] == 0.0) {
+            scale_out[i] = 0.0f;
+            continue;
+        }
+        double h2 = 0.0;
+        for (int32_t j = 0; j < d; ++j) h2 = h2 + Y2[(size_t)j * L + c[j]];
+        double s = norms[i] / sqrt(h2);
+        scale_out[i] = (float)s;
+    }
+    free(Y2);
+    return 0;
+}

@@ -36,6 +36,12 @@ def _load():
         lib.tqo_scales.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P,
                                    ctypes.c_int32, P]
         lib.tqo_scales.restype = ctypes.c_int
+        lib.tqo_encode_plus.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P, ctypes.c_int32,
+                                        P, P, P, P]
+        lib.tqo_encode_plus.restype = ctypes.c_int
+        lib.tqo_scales_plus.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P, ctypes.c_int32,
+                                        P, P, P]
+        lib.tqo_scales_plus.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -81,6 +87,55 @@ def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook, return_rotated: bool = 
         raise RuntimeError("tqo_scales failed (%d)" % st)
     if return_rotated:
         return codes, norms, scales, rot
+    return codes, norms, scales
+
+
+def tqplus_fit(X: np.ndarray, R32: np.ndarray):
+    """TQ+ calibration (section II-B): per-coordinate first and second
+    moments of the rotated, L2-normalised rows of the first batch X.  Returns
+    (mu, kappa) in float64: mu_j the mean of y_j = (R x / ||x||)_j and
+    kappa_j = sigma_j sqrt(d), sigma_j the population standard deviation --
+    the map z_j = (y_j - mu_j) / kappa_j gives the batch mean 0 and variance
+    1/d per coordinate, the first two moments of the canonical marginal."""
+    X = np.asarray(X, dtype=np.float32).astype(np.float64)
+    R = np.asarray(R32, dtype=np.float32).astype(np.float64)
+    d = X.shape[1]
+    Y = (X @ R.T) / np.linalg.norm(X, axis=1, keepdims=True)
+    mu = Y.mean(axis=0)
+    sigma = np.sqrt(((Y - mu) ** 2).mean(axis=0))
+    return mu, sigma * np.sqrt(d)
+
+
+def encode_tqplus(X: np.ndarray, R32: np.ndarray, cb: Codebook, mu32: np.ndarray,
+                  kappa32: np.ndarray):
+    """Encode with TQ+ calibration (section II-B) given as float32 mu, kappa
+    (as an index stores them): thresholds a_jt = mu_j + kappa_j t_t per
+    coordinate, reconstruction yhat_j = mu_j + kappa_j c[code_j] for the
+    scale.  Returns (codes uint8 [n, d], norms float64 [n], scales float32 [n])."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    R32 = np.ascontiguousarray(R32, dtype=np.float32)
+    n, d = X.shape
+    mu = np.ascontiguousarray(mu32, dtype=np.float32)
+    kappa = np.ascontiguousarray(kappa32, dtype=np.float32)
+    if R32.shape != (d, d) or cb.d != d or mu.shape != (d,) or kappa.shape != (d,):
+        raise ValueError("shape mismatch")
+    L = cb.levels
+    bounds = np.ascontiguousarray(cb.bounds, dtype=np.float64)
+    cents = np.ascontiguousarray(cb.cents, dtype=np.float64)
+    codes = np.empty((n, d), dtype=np.uint8)
+    norms = np.empty(n, dtype=np.float64)
+    scales = np.empty(n, dtype=np.float32)
+    lib = _load()
+    st = lib.tqo_encode_plus(X.ctypes.data, n, d, R32.ctypes.data, bounds.ctypes.data, L,
+                             mu.ctypes.data, kappa.ctypes.data, codes.ctypes.data, norms.ctypes.data)
+    if st == -2:
+        raise ValueError("non-finite input")
+    if st != 0:
+        raise RuntimeError("tqo_encode_plus failed (%d)" % st)
+    st = lib.tqo_scales_plus(codes.ctypes.data, norms.ctypes.data, n, d, cents.ctypes.data, L,
+                             mu.ctypes.data, kappa.ctypes.data, scales.ctypes.data)
+    if st != 0:
+        raise RuntimeError("tqo_scales_plus failed (%d)" % st)
     return codes, norms, scales
 
 

@@ -40,11 +40,23 @@ def allowed_mask(tenants, allow_row) -> np.ndarray:
     return ((words[w] >> (t & 63).astype(np.uint64)) & np.uint64(1)).astype(bool)
 
 
+def _reconstruct(codes, cents, calib):
+    """Rotated-domain reconstruction of coded rows: c[code_j], or with TQ+
+    calibration (mu, kappa) (section II-B) mu_j + kappa_j c[code_j]."""
+    xhat = np.asarray(cents, dtype=np.float64)[codes]
+    if calib is not None:
+        mu = np.asarray(calib[0], dtype=np.float32).astype(np.float64)
+        kappa = np.asarray(calib[1], dtype=np.float32).astype(np.float64)
+        xhat = mu + kappa * xhat
+    return xhat
+
+
 def scores_for_ids(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
-                   qrot: np.ndarray, ids) -> np.ndarray:
-    """score_i for the given vector ids against one rotated query (float64)."""
+                   qrot: np.ndarray, ids, calib=None) -> np.ndarray:
+    """score_i for the given vector ids against one rotated query (float64);
+    calib: TQ+ (mu, kappa) or None."""
     ids = np.asarray(ids, dtype=np.int64)
-    xhat = np.asarray(cents, dtype=np.float64)[codes[ids]]
+    xhat = _reconstruct(codes[ids], cents, calib)
     return np.asarray(scales, dtype=np.float64)[ids] * (xhat @ qrot)
 
 
@@ -64,13 +76,14 @@ def _pad(ids, sc, k):
 
 def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
            R32: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,
-           chunk: int = 65536, masks=None):
+           chunk: int = 65536, masks=None, calib=None):
     """Top-k over TurboQuant codes for every query.  Returns (ids int64 [nq,k],
     scores float64 [nq,k]).  The eligible vectors of query b are those whose
     tenant the allowlist row allow[b] admits (section III-B) and, when masks
     is given, those with masks[b][i] true: a per-query set of allowed
     positions (slot-level allowlists, and the vectors of an id-map index not
-    deleted, section III-A)."""
+    deleted, section III-A).  calib: TQ+ calibration (mu, kappa), section
+    II-B, or None."""
     if k <= 0:
         raise ValueError("k must be positive")
     qrot = rotate_queries(R32, Q)
@@ -80,7 +93,7 @@ def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
     sc_all = np.empty((nq, n), dtype=np.float64)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
-        xhat = cents[codes[s:e]]                         # [m, d]
+        xhat = _reconstruct(codes[s:e], cents, calib)    # [m, d]
         sc_all[:, s:e] = (xhat @ qrot.T).T * np.asarray(scales[s:e], dtype=np.float64)[None, :]
     ids_out = np.empty((nq, k), dtype=np.int64)
     sc_out = np.empty((nq, k), dtype=np.float64)
@@ -170,12 +183,12 @@ def mrr_at_k(approx_ids: np.ndarray, exact_ids: np.ndarray, k: int = 20) -> floa
 
 def postfilter_search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
                       R32: np.ndarray, Q: np.ndarray, k: int, overfetch: int, tenants,
-                      allow, masks=None):
+                      allow, masks=None, calib=None):
     """The over-fetch post-filter baseline of section V-C: the unfiltered top
     k * overfetch of each query (over the vectors in masks, if given), then,
     in that order, the first k whose tenant the query's allowlist admits.
     Returns (ids int64 [nq,k], scores float64 [nq,k]), padded with (-1, -inf)."""
-    ids, sc = search(codes, scales, cents, R32, Q, k * overfetch, masks=masks)
+    ids, sc = search(codes, scales, cents, R32, Q, k * overfetch, masks=masks, calib=calib)
     out_i = np.full((ids.shape[0], k), -1, dtype=np.int64)
     out_s = np.full((ids.shape[0], k), -np.inf, dtype=np.float64)
     for b in range(ids.shape[0]):

@@ -15,7 +15,7 @@ def score_tol(ref, qnorm):
 
 
 def check_topk(gpu_ids, gpu_scores, codes, scales, cents, qrot, qnorms, k,
-               ref_ids, ref_scores, allowed=None, n=None):
+               ref_ids, ref_scores, allowed=None, n=None, calib=None):
     """Validity of GPU top-k lists against the oracle (see module docstring of
     tests/test_gpu_search.py).  `allowed` is a list of boolean masks (or None);
     `ref_*` are the oracle's own lists.  Returns the number of id lists that
@@ -39,7 +39,7 @@ def check_topk(gpu_ids, gpu_scores, codes, scales, cents, qrot, qnorms, k,
             assert np.all(allowed[b][v]), "disallowed id returned"
         if nv == 0:
             continue
-        ref = oracle.scores_for_ids(codes, scales, cents, qrot[b], v)
+        ref = oracle.scores_for_ids(codes, scales, cents, qrot[b], v, calib=calib)
         tol = score_tol(ref, qnorms[b])
         err = np.abs(gpu_scores[b][:nv] - ref)
         assert np.all(err <= tol), (b, float((err / tol).max()))
