@@ -164,12 +164,47 @@ tq_status tq_index_export(const tq_index *idx, uint8_t *codes_dev,
 tq_status tq_index_info(const tq_index *idx, int32_t *d, int32_t *bits,
                         int32_t *n_tenants, int64_t *n, int32_t *idmap);
 
+/* ------------------------------------------------------ TQ+ calibration ---
+ * TQ+ (section II-B): a per-coordinate affine calibration for embeddings
+ * whose rotated coordinates do not follow the sphere-coordinate law the
+ * codebook was built for.  With y = R x / ||x|| (float64 from float32 R and
+ * x), mu_j is the mean of y_j over a first batch of m rows and kappa_j =
+ * sigma_j sqrt(d), sigma_j the population standard deviation (both stored
+ * float32), so that z_j = (y_j - mu_j) / kappa_j has mean 0 and variance
+ * 1/d over the batch.  Coordinates are then coded against per-coordinate
+ * thresholds and reconstructed affinely; for a vector with n_x = ||x||:
+ *   a_ij   = fl64(mu_j + fl64(kappa_j t_i))                (float64)
+ *   code_j = number of i with fl64(a_ij * n_x) <= (R x)_j
+ *   yhat_j = fl64(mu_j + fl64(kappa_j c[code_j]))
+ *   scale  = n_x / sqrt(sum_j fl64(yhat_j^2))   (sequential over j; 0 if n_x = 0)
+ * and a search scores scale * sum_j q'_j (mu_j + kappa_j c[code_j]).  The
+ * identity calibration (mu = 0, kappa = 1) gives plain TurboQuant.
+ *
+ * calibrate(): fits mu and kappa to X_dev [m][d] float32 (m >= 1; sums in
+ * float64 on the device) and installs them.  Only on an index with no
+ * vectors (TQ_EINVAL otherwise, or for a row of zero or non-finite norm,
+ * reported after synchronising `stream`).  Vectors added afterwards -- by
+ * tq_index_add / tq_index_add_ids -- are coded as above; codes given to
+ * tq_index_add_codes are taken to be calibrated codes.
+ * set_calibration(): installs host mu [d], kappa [d] (finite, kappa >= 0)
+ * on an index with no vectors.
+ * calibration(): copies the installed values to mu_host, kappa_host (either
+ * may be NULL) and sets *calibrated to 1, or sets it to 0 and copies nothing.
+ * A calibrated index is searched by the scans only: TQ_PATH_MFMA is
+ * TQ_EUNSUPPORTED on it. */
+tq_status tq_index_calibrate(tq_index *idx, const float *X_dev, int64_t m, void *stream);
+tq_status tq_index_set_calibration(tq_index *idx, const float *mu_host, const float *kappa_host);
+tq_status tq_index_calibration(const tq_index *idx, float *mu_host, float *kappa_host,
+                               int32_t *calibrated);
+
 /* Persistence (section III-A: both index types persist to disk).
  * save() writes the index to `path` (created or truncated): a 48-byte header
- * (magic "TQINDEX1", format version 1, flags 0, d, bits, rotation seed, n,
+ * (magic "TQINDEX1", format version 1, flags, d, bits, rotation seed, n,
  * n_tenants), the canonical codes [n][d*bits/8], the scales [n] float32 and
- * the tenant ids [n] uint16, all little-endian, then a 64-bit FNV-1a hash of
- * every preceding byte.  The content is read back from the device with
+ * the tenant ids [n] uint16, then the optional sections the flags announce
+ * (bit 0: an id-map index's ids and live masks, see below; bit 1: TQ+
+ * calibration, mu [d] then kappa [d] float32), all little-endian, then a
+ * 64-bit FNV-1a hash of every preceding byte.  The content is read back from the device with
  * blocking copies, and host memory of the file's size is used.  A file that
  * cannot be created or written is TQ_EINVAL. */
 tq_status tq_index_save(const tq_index *idx, const char *path);

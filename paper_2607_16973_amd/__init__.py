@@ -201,6 +201,31 @@ class Index:
     def reserve(self, capacity: int) -> None:
         check(lib.tq_index_reserve(self._h, capacity))
 
+    def calibrate(self, X) -> None:
+        """TQ+ calibration (section II-B) fitted to the rows of X (cuda
+        float32 [m, d]) before the first vector is added (tq_index_calibrate)."""
+        torch = _torch()
+        check(lib.tq_index_calibrate(self._h, _dev_ptr(X, torch.float32, "X", 2), X.shape[0],
+                                     _stream(X.device)))
+
+    def set_calibration(self, mu, kappa) -> None:
+        """Installs a given TQ+ calibration (host float32 [d] each)."""
+        mu = np.ascontiguousarray(mu, dtype=np.float32)
+        kappa = np.ascontiguousarray(kappa, dtype=np.float32)
+        if mu.shape != (self.d,) or kappa.shape != (self.d,):
+            raise ValueError("mu and kappa must have shape (d,)")
+        check(lib.tq_index_set_calibration(self._h, mu.ctypes.data_as(ctypes.c_void_p),
+                                           kappa.ctypes.data_as(ctypes.c_void_p)))
+
+    def calibration(self):
+        """The installed TQ+ (mu, kappa) as float32 arrays, or None."""
+        mu = np.empty(self.d, dtype=np.float32)
+        kappa = np.empty(self.d, dtype=np.float32)
+        has = ctypes.c_int32()
+        check(lib.tq_index_calibration(self._h, mu.ctypes.data_as(ctypes.c_void_p),
+                                       kappa.ctypes.data_as(ctypes.c_void_p), ctypes.byref(has)))
+        return (mu, kappa) if has.value else None
+
     def add(self, X, tenants=None) -> None:
         torch = _torch()
         check(lib.tq_index_add(self._h, _dev_ptr(X, torch.float32, "X", 2),
@@ -215,8 +240,10 @@ class Index:
                                      codes.shape[0], _stream(codes.device)))
 
     def export(self, device="cuda"):
+        """Every slot's (codes, scales, tenants), canonical layout; deleted
+        slots of an id-map index included."""
         torch = _torch()
-        n = len(self)
+        n = self.n_slots
         codes = torch.empty((n, self.d * self.bits // 8), dtype=torch.uint8, device=device)
         scales = torch.empty((n,), dtype=torch.float32, device=device)
         tenants = torch.empty((n,), dtype=torch.int16, device=device)

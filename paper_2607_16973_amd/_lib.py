@@ -54,6 +54,9 @@ def _load():
         "tq_index_size": ([P, P], ctypes.c_int),
         "tq_index_export": ([P, P, P, P, P], ctypes.c_int),
         "tq_index_info": ([P, P, P, P, P, P], ctypes.c_int),
+        "tq_index_calibrate": ([P, P, I64, P], ctypes.c_int),
+        "tq_index_set_calibration": ([P, P, P], ctypes.c_int),
+        "tq_index_calibration": ([P, P, P, P], ctypes.c_int),
         "tq_idmap_create": ([P, P, I32, P], ctypes.c_int),
         "tq_index_add_ids": ([P, P, P, P, I64, P], ctypes.c_int),
         "tq_index_add_codes_ids": ([P, P, P, P, P, I64, P], ctypes.c_int),
@@ -83,7 +86,8 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_index_reserve", "tq_index_add", "tq_index_add_codes", "tq_index_size",
             "tq_index_export", "tq_index_info", "tq_index_save", "tq_index_load",
             "tq_idmap_create", "tq_index_add_ids", "tq_index_add_codes_ids", "tq_index_remove_ids",
-            "tq_index_slots", "tq_slot_allowlist",
+            "tq_index_slots", "tq_slot_allowlist", "tq_index_calibrate",
+            "tq_index_set_calibration", "tq_index_calibration",
             "tq_index_free", "tq_search", "tq_search_postfilter", "tq_search_workspace_size",
             "tq_search_ex", "tq_last_search_fallbacks")
 

@@ -150,6 +150,13 @@ struct tq_index {
     uint64_t *live = nullptr;      // cap/64
     std::unordered_map<uint64_t, int64_t> slot_of;
     int64_t n_deleted = 0;
+    // TQ+ calibration (section II-B): mu and kappa per coordinate (host and
+    // device float32) and the encoder's float64 tables derived from them.
+    bool calibrated = false;
+    std::vector<float> mu_h, kappa_h;
+    float *mu = nullptr, *kappa = nullptr;   // [d] each
+    double *athr = nullptr;                  // [levels-1][d]: mu_j + kappa_j t_i
+    double *ysq = nullptr;                   // [d][levels]: (mu_j + kappa_j c_c)^2
 };
 
 namespace {
@@ -169,6 +176,13 @@ void index_release(tq_index *x) {
     if (x->status) (void)hipFree(x->status);
     if (x->ext) (void)hipFree(x->ext);
     if (x->live) (void)hipFree(x->live);
+    if (x->mu) (void)hipFree(x->mu);
+    if (x->kappa) (void)hipFree(x->kappa);
+    if (x->athr) (void)hipFree(x->athr);
+    if (x->ysq) (void)hipFree(x->ysq);
+    x->mu = x->kappa = nullptr;
+    x->athr = x->ysq = nullptr;
+    x->calibrated = false;
     x->ext = nullptr;
     x->live = nullptr;
     x->codes = nullptr;
@@ -458,7 +472,12 @@ static tq_status add_vectors(tq_index *idx, const float *X_dev, const uint16_t *
     out.blocked = idx->codes;
     out.blocked_scales = idx->scales;
     out.base = idx->n;
-    e = encode_rows(X_dev, n, idx->d, R, idx->cbdev, out, ws.p, idx->status, s);
+    CalibDev cal;
+    if (idx->calibrated) {
+        cal.athr = idx->athr;
+        cal.ysq = idx->ysq;
+    }
+    e = encode_rows(X_dev, n, idx->d, R, idx->cbdev, out, ws.p, idx->status, s, cal);
     if (e != hipSuccess) return hip_fail(e, "encode");
     int h = 0;
     st = read_status(idx->status, s, &h);
@@ -503,6 +522,101 @@ tq_status tq_idmap_create(const tq_codebook *cb, const tq_rotation *rot, int32_t
     tq_status st = tq_index_create(cb, rot, n_tenants, out);
     if (st == TQ_OK) (*out)->idmap = true;
     return st;
+}
+
+}  // extern "C"
+
+// Installs a TQ+ calibration (host mu, kappa; checked finite, kappa >= 0):
+// the device copies and the encoder's tables, thresholds a_ij =
+// fl64(mu_j + fl64(kappa_j t_i)) and squared reconstructions
+// fl64(fl64(mu_j + fl64(kappa_j c_c))^2), each operation rounded on its own.
+static tq_status install_calibration(tq_index *x, const float *mu, const float *kappa) {
+    const int d = x->d, L = 1 << x->bits;
+    for (int j = 0; j < d; ++j)
+        if (!std::isfinite(mu[j]) || !std::isfinite(kappa[j]) || kappa[j] < 0.f)
+            return fail(TQ_EINVAL, "calibration values must be finite, kappa >= 0");
+    tq_status st = index_device_init(x);
+    if (st != TQ_OK) return st;
+    std::vector<double> athr((size_t)(L - 1) * d), ysq((size_t)d * L);
+    for (int i = 0; i < L - 1; ++i)
+        for (int j = 0; j < d; ++j) {
+            const double p = (double)kappa[j] * x->cb.bounds[i];
+            const double a = (double)mu[j] + p;
+            athr[(size_t)i * d + j] = a;
+        }
+    for (int j = 0; j < d; ++j)
+        for (int c = 0; c < L; ++c) {
+            const double p = (double)kappa[j] * x->cb.cents[c];
+            const double y = (double)mu[j] + p;
+            const double y2 = y * y;
+            ysq[(size_t)j * L + c] = y2;
+        }
+    if (!x->mu) {
+        hipError_t e = hipMalloc(&x->mu, sizeof(float) * d);
+        if (e == hipSuccess) e = hipMalloc(&x->kappa, sizeof(float) * d);
+        if (e == hipSuccess) e = hipMalloc(&x->athr, sizeof(double) * athr.size());
+        if (e == hipSuccess) e = hipMalloc(&x->ysq, sizeof(double) * ysq.size());
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc(calibration)");
+    }
+    hipError_t e = hipMemcpy(x->mu, mu, sizeof(float) * d, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(x->kappa, kappa, sizeof(float) * d, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(x->athr, athr.data(), sizeof(double) * athr.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(x->ysq, ysq.data(), sizeof(double) * ysq.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "calibration upload");
+    x->mu_h.assign(mu, mu + d);
+    x->kappa_h.assign(kappa, kappa + d);
+    x->calibrated = true;
+    return TQ_OK;
+}
+
+extern "C" {
+
+tq_status tq_index_calibrate(tq_index *idx, const float *X_dev, int64_t m, void *stream) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (idx->n != 0) return fail(TQ_EINVAL, "calibration must precede the first vector");
+    if (m < 1) return fail(TQ_EINVAL, "calibration needs at least one vector");
+    if (!X_dev) return fail(TQ_EINVAL, "NULL device pointer");
+    tq_status st = index_device_init(idx);
+    if (st != TQ_OK) return st;
+    const float *R = nullptr;
+    st = rotation_dev(&idx->rot, &R);
+    if (st != TQ_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int d = idx->d;
+    const size_t wb = (calib_workspace_bytes(d) + 255) & ~(size_t)255;
+    AsyncBuf ws;
+    hipError_t e = ws.alloc(wb + 2 * sizeof(float) * d, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync(calibration workspace)");
+    float *mu_d = reinterpret_cast<float *>(static_cast<uint8_t *>(ws.p) + wb);
+    float *kappa_d = mu_d + d;
+    e = hipMemsetAsync(idx->status, 0, sizeof(int), s);
+    if (e == hipSuccess) e = calib_fit(X_dev, m, d, R, ws.p, idx->status, mu_d, kappa_d, s);
+    if (e != hipSuccess) return hip_fail(e, "calibration");
+    std::vector<float> mu((size_t)d), kappa((size_t)d);
+    e = hipMemcpyAsync(mu.data(), mu_d, sizeof(float) * d, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(kappa.data(), kappa_d, sizeof(float) * d, hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "calibration read-back");
+    int h = 0;
+    st = read_status(idx->status, s, &h);   // synchronises the stream
+    if (st != TQ_OK) return st;
+    if (h & 1) return fail(TQ_EINVAL, "calibration batch has a zero or non-finite row");
+    return install_calibration(idx, mu.data(), kappa.data());
+}
+
+tq_status tq_index_set_calibration(tq_index *idx, const float *mu_host, const float *kappa_host) {
+    if (!idx || !mu_host || !kappa_host) return fail(TQ_EINVAL, "NULL argument");
+    if (idx->n != 0) return fail(TQ_EINVAL, "calibration must precede the first vector");
+    return install_calibration(idx, mu_host, kappa_host);
+}
+
+tq_status tq_index_calibration(const tq_index *idx, float *mu_host, float *kappa_host,
+                               int32_t *calibrated) {
+    if (!idx) return fail(TQ_EINVAL, "NULL index");
+    if (calibrated) *calibrated = idx->calibrated ? 1 : 0;
+    if (!idx->calibrated) return TQ_OK;
+    if (mu_host) std::memcpy(mu_host, idx->mu_h.data(), sizeof(float) * idx->d);
+    if (kappa_host) std::memcpy(kappa_host, idx->kappa_h.data(), sizeof(float) * idx->d);
+    return TQ_OK;
 }
 
 }  // extern "C"
@@ -687,16 +801,17 @@ namespace {
 // File layout (little-endian): FileHeader, then the canonical codes
 // [n][d*bits/8], the scales [n] float32 and the tenant ids [n] uint16; for
 // an id-map index (flag 1) the external ids [n] uint64 and the live-slot
-// masks [ceil(n/64)] uint64; then a 64-bit FNV-1a hash of every preceding
-// byte.
+// masks [ceil(n/64)] uint64; for a TQ+ calibrated index (flag 2) mu [d] and
+// kappa [d] float32; then a 64-bit FNV-1a hash of every preceding byte.
 constexpr char kFileMagic[8] = {'T', 'Q', 'I', 'N', 'D', 'E', 'X', '1'};
 constexpr uint32_t kFileVersion = 1;
 constexpr uint32_t kFileIds = 1;
+constexpr uint32_t kFileCalib = 2;
 
 struct FileHeader {
     char magic[8];
     uint32_t version;
-    uint32_t flags;          // kFileIds: id-map sections present
+    uint32_t flags;          // kFileIds / kFileCalib: optional sections present
     int32_t d, bits;
     uint64_t seed;           // rotation seed
     int64_t n;
@@ -756,7 +871,7 @@ tq_status tq_index_save(const tq_index *idx, const char *path) {
     FileHeader h{};
     std::memcpy(h.magic, kFileMagic, 8);
     h.version = kFileVersion;
-    h.flags = idx->idmap ? kFileIds : 0;
+    h.flags = (idx->idmap ? kFileIds : 0) | (idx->calibrated ? kFileCalib : 0);
     h.d = idx->d;
     h.bits = idx->bits;
     h.seed = idx->rot.seed;
@@ -776,6 +891,10 @@ tq_status tq_index_save(const tq_index *idx, const char *path) {
     put(ten.data(), ten.size() * 2);
     put(ext.data(), ext.size() * 8);
     put(live.data(), live.size() * 8);
+    if (idx->calibrated) {
+        put(idx->mu_h.data(), idx->mu_h.size() * 4);
+        put(idx->kappa_h.data(), idx->kappa_h.size() * 4);
+    }
     const uint64_t sum = fnv.h;
     if (ok && fwrite(&sum, 1, 8, fc.f) != 8) ok = false;
     const int rc = fclose(fc.f);
@@ -801,9 +920,10 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
     get(&h, sizeof h);
     if (!ok || std::memcmp(h.magic, kFileMagic, 8) != 0)
         return fail(TQ_EINVAL, std::string(path) + " is not an index file");
-    if (h.version != kFileVersion || (h.flags & ~kFileIds) != 0)
+    if (h.version != kFileVersion || (h.flags & ~(kFileIds | kFileCalib)) != 0)
         return fail(TQ_EUNSUPPORTED, "index file version or sections not supported");
     const bool ids = (h.flags & kFileIds) != 0;
+    const bool calib = (h.flags & kFileCalib) != 0;
     if (h.d != cb->t.d || h.bits != cb->t.bits)
         return fail(TQ_EINVAL, "index file d/bits differ from the codebook's");
     if (h.d != rot->d || h.seed != rot->seed)
@@ -817,7 +937,12 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
     std::vector<float> scales;
     std::vector<uint16_t> ten;
     std::vector<uint64_t> ext, live;
+    std::vector<float> mu, kappa;
     try {
+        if (calib) {
+            mu.resize((size_t)h.d);
+            kappa.resize((size_t)h.d);
+        }
         codes.resize((size_t)n * cbytes);
         scales.resize((size_t)n);
         ten.resize((size_t)n);
@@ -833,6 +958,8 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
     get(ten.data(), ten.size() * 2);
     get(ext.data(), ext.size() * 8);
     get(live.data(), live.size() * 8);
+    get(mu.data(), mu.size() * 4);
+    get(kappa.data(), kappa.size() * 4);
     uint64_t sum = 0;
     if (!ok || fread(&sum, 1, 8, fc.f) != 8) return fail(TQ_EINVAL, std::string(path) + " is truncated");
     if (sum != fnv.h) return fail(TQ_EINVAL, std::string(path) + " fails its checksum");
@@ -858,6 +985,13 @@ tq_status tq_index_load(const char *path, const tq_codebook *cb, const tq_rotati
     tq_status st = ids ? tq_idmap_create(cb, rot, h.n_tenants, &x)
                        : tq_index_create(cb, rot, h.n_tenants, &x);
     if (st != TQ_OK) return st;
+    if (calib) {
+        st = install_calibration(x, mu.data(), kappa.data());
+        if (st != TQ_OK) {
+            tq_index_free(x);
+            return st;
+        }
+    }
     if (n > 0) {
         st = index_grow(x, n, nullptr);
         DevBuf c, sc, t;
@@ -938,9 +1072,25 @@ static bool use_mfma(const ScanShape &sh, int k, int base) {
     return base == TQ_PATH_MFMA && mfma_search_supported(sh, k);
 }
 
-static size_t search_bytes(const ScanShape &sh, int64_t nq, int k, int base) {
-    return use_mfma(sh, k, base) ? mfma_search_workspace_bytes(sh, nq, k, scan_grid())
-                                 : lut_search_workspace_bytes(sh, nq, k, scan_grid());
+// Workspace of a search; a calibrated index adds the queries' constant
+// terms at the end (calib_offset).
+static size_t calib_offset(const ScanShape &sh, int64_t nq, int k) {
+    return (lut_search_workspace_bytes(sh, nq, k, scan_grid()) + 255) & ~(size_t)255;
+}
+
+static size_t search_bytes(const ScanShape &sh, int64_t nq, int k, int base, bool calibrated) {
+    if (use_mfma(sh, k, base)) return mfma_search_workspace_bytes(sh, nq, k, scan_grid());
+    if (calibrated) return calib_offset(sh, nq, k) + (size_t)nq * sizeof(float);
+    return lut_search_workspace_bytes(sh, nq, k, scan_grid());
+}
+
+// With TQ+ calibration the scans take kappa * q' (written over the rotated
+// queries at the start of the workspace) and the constant terms.
+static tq_status prepare_calibrated(const tq_index *x, const float *Qrot, int64_t nq, float *qout,
+                                    float *qconst, hipStream_t s) {
+    hipError_t e = calib_queries(Qrot, nq, x->d, x->mu, x->kappa, qout, qconst, s);
+    if (e != hipSuccess) return hip_fail(e, "query calibration");
+    return TQ_OK;
 }
 
 // max |float16(c)| and max |float16(c) - c| over the float32 centroids
@@ -967,9 +1117,11 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
     if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
         return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
                                      "k <= 64 and at most 4096 tenants");
+    if (base == TQ_PATH_MFMA && idx->calibrated)
+        return fail(TQ_EUNSUPPORTED, "matrix-core path does not take a TQ+ calibrated index");
     tq_status st = device_ready();
     if (st != TQ_OK) return st;
-    *bytes_out = search_bytes(shape_of(idx), nq, k, base);
+    *bytes_out = search_bytes(shape_of(idx), nq, k, base, idx->calibrated);
     return TQ_OK;
 }
 
@@ -1005,8 +1157,10 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (base == TQ_PATH_MFMA && (filter.live || filter.slot_allow))
         return fail(TQ_EUNSUPPORTED, "matrix-core path takes tenant allowlists only "
                                      "(no deleted slots, no slot allowlists)");
+    if (base == TQ_PATH_MFMA && idx->calibrated)
+        return fail(TQ_EUNSUPPORTED, "matrix-core path does not take a TQ+ calibrated index");
     const int grid = scan_grid();
-    const size_t need = search_bytes(sh, nq, k, base);
+    const size_t need = search_bytes(sh, nq, k, base, idx->calibrated);
     if (workspace_bytes < need)
         return fail(TQ_EINVAL, "workspace too small: need " + std::to_string(need) + " bytes");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1031,6 +1185,15 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
         if (e != hipSuccess) return hip_fail(e, "query rotation");
         Qrot = qr;
     }
+    float *qconst = nullptr;
+    if (idx->calibrated) {
+        uint8_t *w8 = static_cast<uint8_t *>(workspace_dev);
+        qconst = reinterpret_cast<float *>(w8 + calib_offset(sh, nq, k));
+        float *qr = static_cast<float *>(workspace_dev);
+        st = prepare_calibrated(idx, Qrot, nq, qr, qconst, s);
+        if (st != TQ_OK) return st;
+        Qrot = qr;
+    }
     if (use_mfma(sh, k, base)) {
         int n_fallback = 0;
         float cmax16 = 0.f, dmax = 0.f;
@@ -1047,7 +1210,7 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     }
     hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev,
                               Qrot, nq, k, filter, grid, workspace_dev, workspace_bytes, ids_dev,
-                              scores_dev, s);
+                              scores_dev, s, qconst);
     if (e != hipSuccess) return hip_fail(e, "scan");
     if (idx->idmap && (e = map_ids(ids_dev, nq * k, idx->ext, s)) != hipSuccess)
         return hip_fail(e, "id mapping");
@@ -1081,7 +1244,8 @@ tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev, int64_t 
     }
     const ScanShape sh = shape_of(idx);
     const int grid = scan_grid();
-    const size_t sbytes = (lut_search_workspace_bytes(sh, nq, kk, grid) + 255) & ~(size_t)255;
+    const size_t sbytes =
+        (search_bytes(sh, nq, kk, TQ_PATH_LUT, idx->calibrated) + 255) & ~(size_t)255;
     const size_t tbytes = (size_t)nq * kk * (sizeof(int64_t) + sizeof(float));
     AsyncBuf ws;
     hipError_t e = ws.alloc(sbytes + tbytes, s);
@@ -1095,11 +1259,17 @@ tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev, int64_t 
     float *qr = reinterpret_cast<float *>(w8);
     e = rotate_rows_f32(Q_dev, nq, idx->d, R, qr, s);
     if (e != hipSuccess) return hip_fail(e, "query rotation");
+    float *qconst = nullptr;
+    if (idx->calibrated) {
+        qconst = reinterpret_cast<float *>(w8 + calib_offset(sh, nq, kk));
+        st = prepare_calibrated(idx, qr, nq, qr, qconst, s);
+        if (st != TQ_OK) return st;
+    }
     // the unfiltered top k * overfetch (deleted vectors excluded) ...
     SearchFilter f;
     if (idx->idmap && idx->n_deleted > 0) f.live = idx->live;
     e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev, qr, nq, kk,
-                   f, grid, w8, sbytes, ids_tmp, sc_tmp, s);
+                   f, grid, w8, sbytes, ids_tmp, sc_tmp, s, qconst);
     if (e != hipSuccess) return hip_fail(e, "scan");
     // ... then the first k whose tenant is allowed
     e = postfilter(ids_tmp, sc_tmp, nq, kk, idx->tenants, allow_dev, idx->W, k, ids_dev, scores_dev, s);

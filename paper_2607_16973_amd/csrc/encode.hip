@@ -22,6 +22,10 @@
 //  3. pack: per row, scale = n / sqrt(sum_j fl64(c_code_j^2)) (sequential
 //     float64 over j) and the codes are written in the canonical bitstream
 //     and/or the index's blocked layout.
+// With TQ+ calibration (section II-B) coordinate j is coded against its own
+// thresholds fl64(a_ij n), a_ij = fl64(mu_j + fl64(kappa_j t_i)), and the
+// scale uses yhat_j = fl64(mu_j + fl64(kappa_j c_code_j)); both tables are
+// computed on the host in float64 and passed in (CalibDev).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -44,6 +48,9 @@ constexpr double kTauAbs = 1e-30;
 
 struct QuantArgs {
     const double *bounds;   // device copy of the thresholds t_i (levels-1)
+    // TQ+ calibration: per-coordinate thresholds a_ij = mu_j + kappa_j t_i,
+    // [levels-1][d] (null: the shared t_i)
+    const double *athr;
     int levels;
     uint8_t *codes_tmp;     // [rows][d] unpacked codes of this chunk
     double *norms;          // [rows] exact row norms (written by column tile 0)
@@ -218,10 +225,14 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                     if (nrm == 0.0) {
                         code = L / 2;
                     } else {
+                        // threshold i of this coordinate, before scaling by n
+                        auto thr = [&](int i) {
+                            return qa.athr ? qa.athr[(int64_t)i * d + col] : qa.bounds[i];
+                        };
                         int c = 0;
                         for (int step = L / 2; step >= 1; step >>= 1) {
                             if (c + step <= L - 1) {
-                                const double t = qa.bounds[c + step - 1] * nrm;
+                                const double t = thr(c + step - 1) * nrm;
                                 if (t <= y) c += step;
                             }
                         }
@@ -229,8 +240,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                         if (!std::isfinite(y)) {
                             flag = true;
                         } else {
-                            if (c > 0 && y - qa.bounds[c - 1] * nrm <= tau) flag = true;
-                            if (c < L - 1 && qa.bounds[c] * nrm - y <= tau) flag = true;
+                            if (c > 0 && y - thr(c - 1) * nrm <= tau) flag = true;
+                            if (c < L - 1 && thr(c) * nrm - y <= tau) flag = true;
                         }
                     }
                     qa.codes_tmp[gr * d + col] = (uint8_t)code;
@@ -262,7 +273,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
 // and unfused multiply-adds agree).
 __global__ __launch_bounds__(256) void fixup_kernel(
     const float *__restrict__ X, const float *__restrict__ R, int d,
-    const double *__restrict__ bounds, int levels, const double *__restrict__ norms,
+    const double *__restrict__ bounds, const double *__restrict__ athr, int levels,
+    const double *__restrict__ norms,
     const uint32_t *__restrict__ flags, const unsigned int *__restrict__ flag_count,
     uint8_t *__restrict__ codes_tmp) {
     const unsigned int cnt = *flag_count;
@@ -286,7 +298,7 @@ __global__ __launch_bounds__(256) void fixup_kernel(
         const double nrm = norms[row];
         int c = 0;
         for (int t = 0; t < levels - 1; ++t) {
-            const double th = bounds[t] * nrm;
+            const double th = (athr ? athr[(int64_t)t * d + j] : bounds[t]) * nrm;
             c += (th <= S) ? 1 : 0;
         }
         codes_tmp[row * d + j] = (uint8_t)c;
@@ -298,7 +310,8 @@ constexpr int PACK_ROWS = 32;   // PACK_ROWS * d bytes of LDS (<= 64 KiB at d = 
 
 __global__ __launch_bounds__(256) void pack_kernel(
     const uint8_t *__restrict__ codes_tmp, int64_t m, int d, int bits,
-    const double *__restrict__ cent_sq, const double *__restrict__ norms,
+    const double *__restrict__ cent_sq, const double *__restrict__ ysq,
+    const double *__restrict__ norms,
     uint8_t *__restrict__ canon, float *__restrict__ scales,
     uint8_t *__restrict__ blocked, float *__restrict__ blocked_scales, int64_t base,
     int chunks) {
@@ -317,8 +330,14 @@ __global__ __launch_bounds__(256) void pack_kernel(
     // scale: one thread per row, j in order
     if (tid < rows) {
         const uint8_t *c = cs + tid * d;
+        // sum_j fl64(yhat_j^2): c[code]^2, or with TQ+ the calibrated
+        // reconstruction's square, per coordinate ([d][levels])
+        const int L = 1 << bits;
         double h2 = 0.0;
-        for (int j = 0; j < d; ++j) h2 = h2 + cent_sq[c[j]];
+        if (ysq)
+            for (int j = 0; j < d; ++j) h2 = h2 + ysq[(int64_t)j * L + c[j]];
+        else
+            for (int j = 0; j < d; ++j) h2 = h2 + cent_sq[c[j]];
         const double nrm = norms[r0 + tid];
         const float s = (nrm == 0.0) ? 0.0f : (float)(nrm / std::sqrt(h2));
         if (scales) scales[r0 + tid] = s;
@@ -390,7 +409,7 @@ size_t encode_workspace_bytes(int d) {
 
 hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                        const CodebookDev &cb, const EncodeOut &out, void *ws,
-                       int *status_dev, hipStream_t stream) {
+                       int *status_dev, hipStream_t stream, const CalibDev &calib) {
     const size_t rows = kEncodeChunkRows;
     uint8_t *p = static_cast<uint8_t *>(ws);
     uint8_t *codes_tmp = p;
@@ -419,19 +438,19 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
         if (e != hipSuccess) return e;
         const int nrt = (int)((m + BM - 1) / BM);
         const int groups = (nrt + 7) / 8;
-        QuantArgs qa{bounds, cb.levels, codes_tmp, norms, flags, flag_count, status_dev};
+        QuantArgs qa{bounds, calib.athr, cb.levels, codes_tmp, norms, flags, flag_count, status_dev};
         F32Args fa{nullptr};
         hipLaunchKernelGGL((rot_gemm<true>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
                            stream, X + r0 * d, m, R, d, nrt, qa, fa);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(fixup_kernel, dim3(1024), dim3(256), 0, stream, X + r0 * d, R, d,
-                           bounds, cb.levels, norms, flags, flag_count, codes_tmp);
+                           bounds, calib.athr, cb.levels, norms, flags, flag_count, codes_tmp);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);
         hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * d, stream,
-                           codes_tmp, m, d, cb.bits, cent_sq, norms,
+                           codes_tmp, m, d, cb.bits, cent_sq, calib.ysq, norms,
                            out.canonical ? out.canonical + r0 * (int64_t)(d * cb.bits / 8) : nullptr,
                            out.scales ? out.scales + r0 : nullptr, out.blocked,
                            out.blocked_scales, out.base + r0, chunks);

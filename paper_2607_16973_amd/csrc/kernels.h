@@ -34,13 +34,35 @@ struct EncodeOut {
 // Encodes X [n][d] (float32, row-major) with R [d][d] on `stream`.
 // `ws` must hold encode_workspace_bytes(d); `status_dev` is an int32 that the
 // kernels set non-zero on a non-finite input.
+// TQ+ calibration tables on the device (null: plain TurboQuant):
+// athr [(levels-1)][d] per-coordinate thresholds mu_j + kappa_j t_i and ysq
+// [d][levels] squares of the reconstructions mu_j + kappa_j c_c (float64).
+struct CalibDev {
+    const double *athr = nullptr;
+    const double *ysq = nullptr;
+};
+
 hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                        const CodebookDev &cb, const EncodeOut &out, void *ws,
-                       int *status_dev, hipStream_t stream);
+                       int *status_dev, hipStream_t stream,
+                       const CalibDev &calib = CalibDev());
 
 // Y = X R^T in float32 (query rotation), X [m][d], Y [m][d].
 hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R,
                            float *Y, hipStream_t stream);
+
+// ------------------------------------------------------------- TQ+ (calib.hip)
+// Fits mu [d] and kappa [d] (float32, device) to the m >= 1 rows of X:
+// moments of the rotated, normalised rows.  `ws` holds
+// calib_workspace_bytes(d); *status_dev gets bit 0 set when a row has a zero
+// or non-finite norm.
+size_t calib_workspace_bytes(int d);
+hipError_t calib_fit(const float *X, int64_t m, int d, const float *R, void *ws, int *status_dev,
+                     float *mu, float *kappa, hipStream_t stream);
+// Qout = kappa * Qin per row (Qout may be Qin) and qconst [nq] = sum_j mu_j
+// Qin_j: the query form the scans take for a calibrated index.
+hipError_t calib_queries(const float *Qin, int64_t nq, int d, const float *mu, const float *kappa,
+                         float *Qout, float *qconst, hipStream_t stream);
 
 // --------------------------------------------------------------- layout
 // Blocked code store: vector v lives in block v/64, lane v%64; chunk c (16 B)
@@ -112,11 +134,14 @@ struct SearchFilter {
     bool any() const { return allow || live || slot_allow; }
 };
 
+// qconst: [nq] constant terms of TQ+ calibrated scores (Qrot then holds
+// kappa * q'), or null.
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries,
                       const float *cents32, const float *Qrot, int64_t nq, int k,
                       const SearchFilter &filter, int grid, void *ws, size_t ws_bytes,
-                      int64_t *ids, float *scores, hipStream_t stream);
+                      int64_t *ids, float *scores, hipStream_t stream,
+                      const float *qconst = nullptr);
 
 // Batched search of a tile of queries on the matrix cores with exact
 // rescoring (b = 4, chunks % 8 == 0, d <= 1536, k <= 64, at most 4096

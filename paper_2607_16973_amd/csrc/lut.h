@@ -9,6 +9,10 @@
 // |entry| <= 2^sh max|c| sum_j |q'_j| + rows/2 < 2^31.  The integer sums are
 // then exact and independent of summation order.  A vector's score is
 // s * (float)sum * 2^-sh, computed the same way wherever it is needed.
+// With TQ+ calibration (section II-B) the reconstruction is mu_j + kappa_j c,
+// so the table is built from q''_j = kappa_j q'_j and every entry of row 0
+// also holds round(2^sh C), C = sum_j mu_j q'_j: each code hits row 0 once,
+// so every sum carries C exactly once.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -91,10 +95,11 @@ __device__ inline void nibble_abs_sum(float *red, const float (&qv)[2][4]) {
 //
 // Entries are rounded from float32 products: each is within 1/2 unit of
 // 2^sh c q' plus 2^-23 of its magnitude, so the summed error stays below
-// 2^-23 B + rows/2 units, B = max|c| sum_j |q'_j| -- far inside the score
-// tolerance.
+// 2^-23 B + rows/2 + 1 units, B = max|c| sum_j |q'_j| + |C| -- far inside the
+// score tolerance.  C is the query's constant term (0 without calibration).
 __device__ inline int build_nibble_table(float *lds, const float *red, const float *cents,
-                                         const TableShape &p, const float (&qv)[2][4]) {
+                                         const TableShape &p, const float (&qv)[2][4],
+                                         float C = 0.f) {
     const int tid = threadIdx.x;
     const int rows = p.lut_words >> 4;
     const int L = 1 << p.bits;
@@ -107,13 +112,14 @@ __device__ inline int build_nibble_table(float *lds, const float *red, const flo
     for (int w = 0; w < kTableWaves; ++w) tot += (double)red[w];
     const double cmax = fmax(fabs((double)cl[0]), fabs((double)cl[L - 1]));
     // bound with margin for the float32 partial sums and products
-    const double B = cmax * tot * (1.0 + 1e-5);
+    const double B = (cmax * tot + fabs((double)C)) * (1.0 + 1e-5);
     int sh = 0;
     if (B > 0.0) {
         sh = (int)floor(log2((2147483647.0 - 2.0 * p.d) / B));
         sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
     }
     const float scale = ldexpf(1.0f, sh);
+    const int c0 = (int)rintf(C * scale);
     int *T = reinterpret_cast<int *>(lds);
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
@@ -134,6 +140,9 @@ __device__ inline int build_nibble_table(float *lds, const float *red, const flo
                     e[c] = (int)rintf(fmaf(cl[c & 1], q0, cl[(c >> 1) & 1] * q1) +
                                       fmaf(cl[(c >> 2) & 1], q2, cl[c >> 3] * q3));
             }
+            if (r == 0)
+#pragma unroll
+                for (int c = 0; c < 16; ++c) e[c] += c0;
             int4 *row = reinterpret_cast<int4 *>(T + r * 16);
 #pragma unroll
             for (int c4 = 0; c4 < 4; ++c4)

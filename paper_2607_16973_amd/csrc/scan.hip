@@ -48,7 +48,8 @@ struct ScanParams {
     const uint64_t *allow;      // [nq][W] tenant allowlists, or null: every tenant
     const uint64_t *live;       // [nblk] live-slot masks (bit v: slot 64b+v not deleted), or null
     const uint64_t *slot_allow; // [nq][nblk] allowed-slot masks (instead of allow), or null
-    const float *qrot;          // [nq][d]
+    const float *qrot;          // [nq][d] (with TQ+ calibration: kappa_j q'_j)
+    const float *qconst;        // [nq] TQ+ constant term sum_j mu_j q'_j, or null
     const float *cents;         // [levels]
     float *cand_s;              // [nq][G][k]
     int *cand_i;
@@ -65,6 +66,11 @@ __device__ inline uint64_t block_mask(const ScanParams &p, int qi, int64_t b) {
     uint64_t m = p.live ? p.live[b] : ~0ull;
     if (p.slot_allow) m &= p.slot_allow[(int64_t)qi * p.nblk + b];
     return m;
+}
+
+// Constant term of query qi's scores (TQ+ calibration), 0 without.
+__device__ inline float qconst_of(const ScanParams &p, int qi) {
+    return p.qconst ? p.qconst[qi] : 0.f;
 }
 
 __device__ inline TableShape table_shape(const ScanParams &p) {
@@ -114,16 +120,19 @@ __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__
 }
 
 // Builds the table for one query; returns the fixed-point exponent sh
-// (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.
+// (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.  C is the query's
+// constant term: part of the NIBBLE table, the starting value of the float
+// sums otherwise.
 template <int MODE>
-__device__ int build_table(float *lds, float *red, const ScanParams &p, const float *__restrict__ q) {
+__device__ int build_table(float *lds, float *red, const ScanParams &p, const float *__restrict__ q,
+                           float C) {
     const int tid = threadIdx.x;
     if constexpr (MODE == NIBBLE) {
         float qv[2][4];
         load_nibble_query(table_shape(p), q, qv);
         nibble_abs_sum(red, qv);
         __syncthreads();
-        return build_nibble_table(lds, red, p.cents, table_shape(p), qv);
+        return build_nibble_table(lds, red, p.cents, table_shape(p), qv, C);
     } else if constexpr (MODE == TRIBIT) {
         for (int e = tid; e < p.lut_words; e += SCAN_THREADS) {
             const int j = e >> 3, c = e & 7;
@@ -291,7 +300,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
 
     if (tid == 0) misc[2] = 0;
     for (int qi = 0; qi < p.nq; ++qi) {
-        const int sh = build_table<MODE>(lds, red, p, p.qrot + (int64_t)qi * p.d);
+        const float cq = qconst_of(p, qi);
+        const int sh = build_table<MODE>(lds, red, p, p.qrot + (int64_t)qi * p.d, cq);
         if (p.allow)
             for (int w = tid; w < p.W; w += SCAN_THREADS) allow_s[w] = p.allow[(int64_t)qi * p.W + w];
         if (tid == 0) misc[0] = fkey(-INFINITY);
@@ -350,6 +360,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                 const int ten = p.allow ? (int)p.tenants[vid] : 0;
                 const uint64_t bm = filtered ? block_mask(p, qi, b) : ~0ull;
                 acc_t acc = 0;
+                if constexpr (MODE != NIBBLE) acc = cq;
                 for (int c0 = 0; c0 < CH; c0 += PF) {
 #pragma unroll
                     for (int i = 0; i < PF; ++i) {
@@ -465,7 +476,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
     load_nibble_query(table_shape(p), p.qrot, qv);
     nibble_abs_sum(red, qv);
     __syncthreads();
-    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
     __syncthreads();
 
     // this wave's current and next work items, and the ring holding the
@@ -564,7 +575,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         } else {
             tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
-        if (more) sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+        if (more) sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
         if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
         __syncthreads();   // table ready; survivor count read by every wave
         if (tid == 0) misc[2] = 0;
@@ -630,7 +641,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
     load_nibble_query(table_shape(p), p.qrot, qv);
     nibble_abs_sum(red, qv);
     __syncthreads();
-    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
     __syncthreads();
     for (int qi = 0; qi < p.nq; ++qi) {
         WaveTopK<S> top;
@@ -753,7 +764,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
             tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
         if (more) {
-            sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv);
+            sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
             if (p.allow)
                 for (int w = tid; w < W; w += SCAN_THREADS)
                     allow_s[w] = p.allow[(int64_t)(qi + 1) * W + w];
@@ -1123,7 +1134,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
                       const uint16_t *tenants, const uint64_t *summaries, const float *cents32,
                       const float *Qrot, int64_t nq, int k, const SearchFilter &filter, int grid,
                       void *ws, size_t ws_bytes, int64_t *ids, float *scores,
-                      hipStream_t stream) {
+                      hipStream_t stream, const float *qconst) {
     const uint64_t *allow = filter.allow;
     const int64_t qc = query_chunk(s, nq, k, grid);
     uint8_t *p8 = static_cast<uint8_t *>(ws);
@@ -1150,6 +1161,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
             p.live = filter.live;
             p.slot_allow = filter.slot_allow ? filter.slot_allow + q0 * s.nblk : nullptr;
             p.qrot = Qrot + q0 * s.d;
+            p.qconst = qconst ? qconst + q0 : nullptr;
             p.cents = cents32;
             p.cand_s = all;
             p.n = s.n;
@@ -1191,6 +1203,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.live = filter.live;
         p.slot_allow = filter.slot_allow ? filter.slot_allow + q0 * s.nblk : nullptr;
         p.qrot = Qrot + q0 * s.d;
+        p.qconst = qconst ? qconst + q0 : nullptr;
         p.cents = cents32;
         p.cand_s = cand_s;
         p.cand_i = cand_i;

@@ -20,6 +20,11 @@ row range can be regenerated alone and chunks are generated in parallel):
                   100K corpus: rows [0, 100000), queries rows [100000, 101000)
                   999K corpus: rows [0, 999000), queries rows [999000, 1000000)
                   1M corpus:   999K corpus + rows [1000000, 1001000), same queries
+* shifted    -- the small recipe plus one offset shared by every row:
+                row = shift g + mu_z + 0.3 eps, g ~ N(0, I_d), L2-normalised
+                (rows then lie in a cone around g, as text embeddings with a
+                common component do; the rotated coordinates have non-zero
+                means).  Corpus seed 46, queries as for 'small' (seed 47).
 * tenants    -- Zipf(s=1.1) over T tenants, i.i.d. per vector by inverse CDF
                 (random positions), seed 44.  Equal uniform partitions are also
                 available (T equal-size contiguous-id groups, shuffled).
@@ -76,6 +81,21 @@ def isotropic_mixture(n: int = 10_000, d: int = 1536, n_clusters: int = 100,
         z = r.integers(0, n_clusters, size=c1 - c0)
         eps = r.standard_normal((c1 - c0, d), dtype=np.float32)
         _normalise_rows_into(out[c0:c1], centres[z] + np.float32(sigma) * eps)
+    return out
+
+
+def shifted_mixture(n: int = 10_000, d: int = 1536, shift: float = 1.5, n_clusters: int = 100,
+                    sigma: float = 0.3, seed: int = 46) -> np.ndarray:
+    rng = _rng(seed, _TAG_CENTRES)
+    centres = rng.standard_normal((n_clusters, d), dtype=np.float32)
+    g = rng.standard_normal(d, dtype=np.float32) * np.float32(shift)
+    out = np.empty((n, d), dtype=np.float32)
+    for c0 in range(0, n, CHUNK):
+        c1 = min(n, c0 + CHUNK)
+        r = _rng(seed, _TAG_ROWS, c0 // CHUNK)
+        z = r.integers(0, n_clusters, size=c1 - c0)
+        eps = r.standard_normal((c1 - c0, d), dtype=np.float32)
+        _normalise_rows_into(out[c0:c1], g[None, :] + centres[z] + np.float32(sigma) * eps)
     return out
 
 

@@ -86,7 +86,34 @@ def test_empty_idmap_index_file(parts, tmp_path):
     back = tq.Index.load(cb, rot, path)
     assert isinstance(back, tq.IdMapIndex) and len(back) == 0
     body = bytearray(data[:-8])
-    body[12:16] = struct.pack("<I", 3)                      # an undefined section flag
+    body[12:16] = struct.pack("<I", 5)                      # an undefined section flag
     bad = tmp_path / "bad.tq"
     bad.write_bytes(bytes(body) + struct.pack("<Q", fnv1a64(bytes(body))))
     _expect("TQ_EUNSUPPORTED", cb, rot, bad, "sections")
+
+
+def _with_calibration(data: bytes, mu, kappa) -> bytes:
+    """An empty index file with the TQ+ calibration section (flag 2) added."""
+    body = bytearray(data[:-8])
+    flags = struct.unpack("<I", body[12:16])[0]
+    body[12:16] = struct.pack("<I", flags | 2)
+    body += struct.pack("<%df" % len(mu), *mu) + struct.pack("<%df" % len(kappa), *kappa)
+    return bytes(body) + struct.pack("<Q", fnv1a64(bytes(body)))
+
+
+def test_calibration_section_checked_before_device_work(parts, tmp_path):
+    """A calibration section (mu [d], kappa [d] float32 after the other
+    sections) must be whole and hold finite values with kappa >= 0; the
+    values are checked before the index touches a device."""
+    cb, rot = parts
+    good = tmp_path / "plain.tq"
+    tq.Index(cb, rot, n_tenants=2).save(good)
+    data = good.read_bytes()
+    bad = tmp_path / "bad.tq"
+    full = _with_calibration(data, [0.0] * 256, [1.0] * 256)
+    bad.write_bytes(full[:-8 - 4 * 256] + full[-8:])          # kappa missing
+    _expect("TQ_EINVAL", cb, rot, bad, "")
+    bad.write_bytes(_with_calibration(data, [0.0] * 256, [1.0] * 255 + [-1.0]))
+    _expect("TQ_EINVAL", cb, rot, bad, "kappa")
+    bad.write_bytes(_with_calibration(data, [float("nan")] + [0.0] * 255, [1.0] * 256))
+    _expect("TQ_EINVAL", cb, rot, bad, "finite")
