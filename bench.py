@@ -183,6 +183,60 @@ def filter_study(tq, synth, cb, rot, d, k, dev, stream):
     return out
 
 
+def tqplus_study(tq, synth, cb, rot, X, Qrot, k, n, d, dev, stream):
+    """TQ+ calibration (section II-B).  Throughput: the 1M corpus indexed
+    with a calibration fitted on its first 100,000 rows -- fit, encode and
+    single-query scan rates (the scan reads the same bytes as the plain
+    one).  Quality: on 100K rows lying in a cone around a shared offset
+    (synth.shifted_mixture; the rotated coordinates have non-zero means),
+    Recall@10 against exact float32 search, plain and calibrated on the
+    first 10,000 rows."""
+    import numpy as np
+    import torch
+    out = {}
+    ic = tq.Index(cb, rot, n_tenants=1)
+    ic.reserve(n)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record(stream)
+    ic.calibrate(X[:100_000])
+    ev[1].record(stream)
+    ic.add(X)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    t_fit = ev[0].elapsed_time(ev[1]) / 1e3
+    t_enc = ev[1].elapsed_time(ev[2]) / 1e3
+    nq = Qrot.shape[0]
+    t = timed(lambda: ic.search(Qrot, k, path="lut", prerotated=True), reps=3)
+    bpq = n * (d * 4 // 8 + 4)
+    out["n1m"] = {"fit_rows": 100_000, "fit_ms": t_fit * 1e3, "encode_vectors_per_s": n / t_enc,
+                  "queries_per_s": nq / t, "achieved_GBps": bpq * nq / t / 1e9}
+    log("TQ+ 1M: fit %.1f ms (100K rows), encode %.3g vectors/s, search %.0f queries/s, %.0f GB/s"
+        % (t_fit * 1e3, n / t_enc, nq / t, bpq * nq / t / 1e9))
+    del ic
+    torch.cuda.empty_cache()
+    Xs_np = synth.shifted_mixture(100_000, d)
+    Qs_np = synth.isotropic_queries(Xs_np, 1000, seed=47)
+    Xs = torch.from_numpy(Xs_np).to(dev)
+    Qs = torch.from_numpy(Qs_np).to(dev)
+    exact = torch.topk(Qs @ Xs.T, k, dim=1).indices.cpu().numpy()
+
+    def rec(ids):
+        return float(np.mean([len(set(a.tolist()) & set(b.tolist())) / k
+                              for a, b in zip(ids.cpu().numpy(), exact)]))
+    plain = tq.Index(cb, rot)
+    plain.add(Xs)
+    cal = tq.Index(cb, rot)
+    cal.calibrate(Xs[:10_000])
+    cal.add(Xs)
+    rp, rc = rec(plain.search(Qs, k)[0]), rec(cal.search(Qs, k)[0])
+    out["shifted_cone_100k"] = {"queries": 1000, "fit_rows": 10_000, "recall_at_10_plain": rp,
+                                "recall_at_10_tqplus": rc}
+    log("TQ+ shifted cone 100K: R@10 plain %.3f, calibrated %.3f" % (rp, rc))
+    del plain, cal, Xs
+    torch.cuda.empty_cache()
+    return out
+
+
 def bit_sweep(tq, rot, X, Qrot, k, n, d, stream):
     """Encode throughput (rotation GEMM + quantise + pack) and single-query
     search throughput at each bit width."""
@@ -383,6 +437,7 @@ def main() -> int:
         extra["batched_mfma"] = batched_path(tq, idx, Qrot, k, ids, scores, ex_ids, nr)
         extra["filtered_T100"] = filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev)
         extra["filter_study_100k"] = filter_study(tq, synth, cb, rot, d, k, dev, stream)
+        extra["tqplus"] = tqplus_study(tq, synth, cb, rot, X, Qrot, k, n, d, dev, stream)
     if args.sweep:
         extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
     del X
