@@ -90,9 +90,22 @@ def batched_path(tq, idx, Qrot, k, lut_ids, lut_scores, ex_ids, nr):
     got = bi[:nr].cpu().numpy()
     rec = float(np.mean([len(set(a) & set(b)) / k for a, b in zip(got, ex_ids)]))
     log("batched path: %.0f queries/s, %d fallbacks, same scores as LUT: %s" % (nq / t, fb, same))
-    return {"queries_per_s": nq / t, "ms_per_step": t * 1e3, "queries_per_step": nq,
-            "certificate_fallbacks": fb, "same_scores_as_single_query_path": same,
-            "recall_at_k_vs_exact_fp32": rec}
+    out = {"queries_per_s": nq / t, "ms_per_step": t * 1e3, "queries_per_step": nq,
+           "certificate_fallbacks": fb, "same_scores_as_single_query_path": same,
+           "recall_at_k_vs_exact_fp32": rec}
+    # calls of B = 32, 256 and all queries at k = 10 and 100 (one call: rotation
+    # excluded, selection, rescoring and any single-query re-runs included)
+    by_call = {}
+    for b in (32, 256, nq):
+        qb = Qrot[:b].contiguous()
+        for kk in (10, 100):
+            tb = timed(lambda: idx.search(qb, kk, path="mfma", prerotated=True))
+            by_call["B%d_k%d" % (b, kk)] = {"queries_per_s": b / tb, "ms_per_call": tb * 1e3,
+                                            "certificate_fallbacks": tq.last_search_fallbacks()}
+            log("batched B=%d k=%d: %.0f queries/s, %.3f ms per call, %d fallbacks"
+                % (b, kk, b / tb, tb * 1e3, tq.last_search_fallbacks()))
+    out["by_call"] = by_call
+    return out
 
 
 def filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev, T=100):

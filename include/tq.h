@@ -320,13 +320,14 @@ tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev,
  *  TQ_PATH_LUT   one pass over the code store per query, with the query's
  *                lookup table in LDS.
  *  TQ_PATH_MFMA  one pass per tile of 32 queries: approximate float16 scores
- *                on the matrix cores select 256 candidates per query, which
- *                are rescored exactly (the same scores as TQ_PATH_LUT).  A
+ *                on the matrix cores select 256 candidates per query (512
+ *                for k > 64), which are rescored exactly (the same scores as
+ *                TQ_PATH_LUT).  A
  *                per-query certificate -- a rigorous bound on the
  *                approximation error -- proves that the exact top k lies
  *                among the candidates; queries without one are re-run on the
  *                LUT path (see tq_last_search_fallbacks).  Needs 4-bit codes,
- *                d % 256 == 0, d <= 1536, k <= 64 and n_tenants <= 4096,
+ *                d % 256 == 0, d <= 1536, k <= 256 and n_tenants <= 4096,
  *                else TQ_EUNSUPPORTED.  Synchronises `stream` once per call, to
  *                read the certificates on the host. */
 typedef enum {

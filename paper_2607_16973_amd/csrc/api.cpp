@@ -1116,7 +1116,7 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
         return fail(TQ_EINVAL, "unknown path");
     if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
         return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
-                                     "k <= 64 and at most 4096 tenants");
+                                     "k <= 256 and at most 4096 tenants");
     if (base == TQ_PATH_MFMA && idx->calibrated)
         return fail(TQ_EUNSUPPORTED, "matrix-core path does not take a TQ+ calibrated index");
     tq_status st = device_ready();
@@ -1146,7 +1146,7 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     const ScanShape sh = shape_of(idx);
     if (base == TQ_PATH_MFMA && !mfma_search_supported(sh, k))
         return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
-                                     "k <= 64 and at most 4096 tenants");
+                                     "k <= 256 and at most 4096 tenants");
     if (slot_allow && !allow_dev) return fail(TQ_EINVAL, "slot allowlist flag without an allowlist");
     SearchFilter filter;
     if (slot_allow)

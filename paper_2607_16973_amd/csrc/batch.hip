@@ -8,16 +8,26 @@
 //     of 64 vectors (32 coordinates each) is turned into float16 centroid
 //     values and multiplied with the query tile on v_mfma_f32_16x16x32_f16;
 //     after a block's last chunk the approximate scores s_v <c_hat, q'> are
-//     written, scaled to a float16 range, as a [query][vector] matrix.
-//  3. select_kernel + select_merge_kernel: the 64 best approximate scores of
-//     every query (allowed vectors only).
-//  4. rescore_kernel: the exact score of each of the 64 candidates with the
+//     written, scaled to a float16 range, as a [query][vector] matrix, and
+//     each query's largest score in the block as a [query][block] matrix.
+//  3. Selection of at most KC candidates per query (KC = 256, or 512 for
+//     k > 64) with a bound amin on the approximate score of every other
+//     vector.  Unfiltered: block_select_kernel.  The R-th largest block
+//     maximum (R = KC - 32) is a score of R distinct vectors, so at least R
+//     vectors reach it, and every vector that does lies in a block whose
+//     maximum reaches it: a radix selection over the block maxima lists
+//     those blocks, and their vectors that reach it are the candidates
+//     (about R when vectors sit at random positions; if more than KC, a
+//     radix selection over the listed scores keeps the KC best).  Filtered
+//     (the block maxima ignore the allowlist): select_kernel +
+//     select_merge_kernel, the KC best allowed scores.
+//  4. rescore_kernel: the exact score of each candidate with the
 //     single-query scan's integer table (bit-identical scores), the top k of
 //     them, and a certificate: with E a rigorous bound on |approximate -
-//     exact| for every vector, a vector outside the 64 scores at most
-//     (64th approximate) + E; if that is below the k-th exact score the top
-//     k is proven, otherwise the query is flagged and the caller re-runs it
-//     on the single-query scan.
+//     exact| for every vector, a vector outside the candidates scores at
+//     most amin + E; if that is below the k-th exact score the top k is
+//     proven, otherwise the query is flagged and the caller re-runs it on
+//     the single-query scan.
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -37,8 +47,17 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
-constexpr int kCand = 256;         // candidates per query kept for exact rescoring
-constexpr int kCandS = kCand / 64;  // 64-entry slots of a candidate list
+constexpr int kCandMax = 512;      // candidates per query kept for exact rescoring (KC <= this)
+constexpr int kMaxBatchK = 256;    // largest k of the batched path
+constexpr int BS_THREADS = 1024;   // block_select_kernel
+constexpr int BS_WAVES = BS_THREADS / 64;
+constexpr int kListMaxB = 8192;    // blocks a query's selection may list
+constexpr int kHistCopies = 4;     // histogram copies (lane & 3), against atomic conflicts
+constexpr int kHistStride = 257;   // words between copies: copies in different banks
+// Selection outcome per query.
+constexpr int kSelBound = 0;       // candidates + a bound amin on every other vector
+constexpr int kSelOverflow = 1;    // no usable candidates: the query is not certified
+constexpr int kSelAll = 2;         // every vector is a candidate
 constexpr int MF_THREADS = 768;    // 12 waves: three per SIMD, 168 registers each
 constexpr int MF_RING = 8;         // chunk loads in flight per wave
 constexpr int kTableBytes = 256 * 32 * 4;   // byte table, 32 replicas
@@ -147,6 +166,7 @@ struct ScoreParams {
     const QInfo *info;         // [nqt]
     const float *cents;        // 16 levels
     _Float16 *out;             // [kTile][npad] approximate scores / norm
+    _Float16 *bmax;            // [kTile][nblk] per-block maximum of out (vectors < n)
     int64_t n, nblk, npad;
     int d, chunks, nqt;
 };
@@ -302,18 +322,39 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
             chunk(c0 + 7, rb7);
         }
         // lane holds vectors 16m + qrow, queries 16t + 4*kq + r
+        float mx[2][4];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx[t][r] = -INFINITY;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int64_t v = blk * 64 + 16 * m + qrow;
+            const bool vin = v < p.n;
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int q = 16 * t + 4 * kq + r;
-                    if (q < p.nqt)
-                        p.out[(int64_t)q * p.npad + v] = (_Float16)(acc[t][m][r] * scl[m] * qf[t][r]);
+                    const _Float16 h = (_Float16)(acc[t][m][r] * scl[m] * qf[t][r]);
+                    if (q < p.nqt) p.out[(int64_t)q * p.npad + v] = h;
+                    mx[t][r] = fmaxf(mx[t][r], vin ? (float)h : -INFINITY);
                 }
         }
+        // block maxima: the 16 lanes of a DPP row hold the block's 64 vectors
+        // of the same queries
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float x = mx[t][r];
+                x = fmaxf(x, dpp_f<kDppRowRor8>(x));
+                x = fmaxf(x, dpp_f<kDppRowRor4>(x));
+                x = fmaxf(x, dpp_f<kDppRowRor2>(x));
+                x = fmaxf(x, dpp_f<kDppRowRor1>(x));
+                const int q = 16 * t + 4 * kq + r;
+                if (qrow == 0 && q < p.nqt) p.bmax[(int64_t)q * p.nblk + blk] = (_Float16)x;
+            }
         if (nxt >= nbw) break;
         cur = nxt;
         nxt = __builtin_amdgcn_readfirstlane(ticket);
@@ -326,21 +367,23 @@ struct SelectParams {
     const _Float16 *approx;    // [nqt][npad]
     const uint16_t *tenants;
     const uint64_t *allow;     // [nqt][W] or null
-    float *cand_s;             // [nqt][SEL_GROUPS][kCand]
+    float *cand_s;             // [nqt][SEL_GROUPS][KC]
     int *cand_i;
     int *gbound;               // [nqt * kBoundStride] order keys
     int64_t n, npad;
     int W;
 };
 
-// The kCand best allowed approximate scores of one query over 1/SEL_GROUPS
-// of the vectors; each lane reads 8 consecutive scores per load.  A wave
+// The KC = 64 S best allowed approximate scores of one query over
+// 1/SEL_GROUPS of the vectors; each lane reads 8 consecutive scores per load.  A wave
 // keeps its best kCand in registers; scores that pass its current bound are
 // first appended to a per-wave LDS buffer, and the buffer is sorted into
 // the list only when 64 have gathered -- a sort per 64 real candidates
 // rather than per 64 scores read.
+template <int S>
 __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     constexpr int NW = SEL_THREADS / 64;
+    constexpr int kCand = 64 * S, kCandS = S;
     __shared__ float st_s[NW * kCand];
     __shared__ int st_i[NW * kCand];
     __shared__ float buf_s[NW * kBuf];
@@ -435,11 +478,16 @@ __global__ __launch_bounds__(SEL_THREADS) void select_kernel(SelectParams p) {
     }
 }
 
-// The kCand best of the SEL_GROUPS lists of each query, sorted.
+// The KC = 64 S best of the SEL_GROUPS lists of each query: their ids, the
+// approximate score of the KC-th, and the selection state (every allowed
+// vector a candidate when fewer than KC).
+template <int S>
 __global__ __launch_bounds__(256) void select_merge_kernel(const float *__restrict__ cs,
                                                            const int *__restrict__ ci,
-                                                           float *__restrict__ top_s,
-                                                           int *__restrict__ top_i) {
+                                                           int *__restrict__ top_i,
+                                                           float *__restrict__ amin,
+                                                           int *__restrict__ state) {
+    constexpr int kCand = 64 * S, kCandS = S;
     __shared__ float st_s[4 * kCand];
     __shared__ int st_i[4 * kCand];
     const int q = blockIdx.x;
@@ -480,11 +528,281 @@ __global__ __launch_bounds__(256) void select_merge_kernel(const float *__restri
             merge_lists<kCandS>(ls, li, os, oi, lane);
         }
 #pragma unroll
-        for (int a = 0; a < kCandS; ++a) {
-            top_s[(int64_t)q * kCand + a * 64 + lane] = ls[a];
-            top_i[(int64_t)q * kCand + a * 64 + lane] = li[a];
+        for (int a = 0; a < kCandS; ++a) top_i[(int64_t)q * kCand + a * 64 + lane] = li[a];
+        const bool full = __shfl(li[kCandS - 1], 63, 64) != INT_MAX;
+        if (lane == 63) {
+            amin[q] = ls[kCandS - 1];
+            state[q] = full ? kSelBound : kSelAll;
         }
     }
+}
+
+// ------------------------------------------- selection by block maxima
+// Order-preserving map of float16 bit patterns onto 16-bit keys.
+__device__ inline uint32_t hkey(uint32_t h) { return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u); }
+__device__ inline float hkey_value(uint32_t key) {
+    const uint32_t h = (key & 0x8000u) ? (key & 0x7FFFu) : (~key & 0xFFFFu);
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+// Run by one whole wave once the histogram copies of a digit (256 bins) are
+// complete: the digit d with (#keys whose digit > d) < K <= (#keys whose
+// digit >= d), for 1 <= K <= #keys; out[0] = d, out[1] = #keys whose digit
+// > d.  Lane l holds bins 4l .. 4l+3.
+__device__ inline void find_digit(const int *hist, int K, int *out) {
+    const int lane = threadIdx.x & 63;
+    int c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        int v = 0;
+#pragma unroll
+        for (int h = 0; h < kHistCopies; ++h) v += hist[h * kHistStride + 4 * lane + j];
+        c[j] = v;
+    }
+    const int s = (c[0] + c[1]) + (c[2] + c[3]);
+    int S = s;   // keys in the bins of lanes >= this one
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_down(S, o, 64);
+        if (lane + o < 64) S += t;
+    }
+    const uint64_t ge = __ballot(S >= K);
+    const int L = 63 - __builtin_clzll(ge);
+    if (lane == L) {
+        int above = S - s;
+        int d = 4 * lane;
+        for (int j = 3; j >= 0; --j) {
+            if (above + c[j] >= K) {
+                d = 4 * lane + j;
+                break;
+            }
+            above += c[j];
+        }
+        out[0] = d;
+        out[1] = above;
+    }
+}
+
+struct BlockSelParams {
+    const uint16_t *approx;    // [nqt][npad] float16 bit patterns
+    const uint16_t *bmax;      // [nqt][nblk]
+    int *top_i;                // [nqt][KC] candidate ids (INT_MAX: none)
+    float *amin;               // [nqt] bound on the approximate score of non-candidates
+    int *state;                // [nqt] kSel*
+    int64_t n, nblk, npad;
+    int KC;
+};
+
+// One workgroup per query (unfiltered), as described at the top of the
+// file.  Keys are the float16 bit patterns mapped by hkey; a radix
+// selection takes the high byte, then the low byte, with LDS histograms.
+__global__ __launch_bounds__(BS_THREADS) void block_select_kernel(BlockSelParams p) {
+    __shared__ int hist[kHistCopies * kHistStride];
+    __shared__ int list[kListMaxB];
+    __shared__ int sh[8];
+    const int q = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int KC = p.KC, R = KC - 32;
+    const uint16_t *bm = p.bmax + (int64_t)q * p.nblk;
+    const uint16_t *row = p.approx + (int64_t)q * p.npad;
+    int *out_i = p.top_i + (int64_t)q * KC;
+    int *hc = hist + (lane & 3) * kHistStride;
+    auto clear_hist = [&]() {
+        for (int i = tid; i < kHistCopies * kHistStride; i += BS_THREADS) hist[i] = 0;
+    };
+    // Visitors of the keys: block maxima (thread t: blocks t + 1024 u) and
+    // the scores of the listed blocks (wave w: listed blocks w + 16 u, lane =
+    // vector).  Up to BB block keys per thread and LB listed-block keys per
+    // lane stay in registers across the passes (one round of loads); beyond
+    // that the keys are loaded again, in rounds of RB, for every pass.
+    // A round's loads are unconditional, from clamped indices, and all
+    // issued before any is used (the empty asm keeps the compiler from
+    // moving a load under the branch that uses it, where it would be waited
+    // for on the spot and a round would run one load at a time).
+    constexpr int BB = 16, LB = 40, RB = 8;
+    const bool breg = p.nblk <= (int64_t)BB * BS_THREADS;
+    // keys of blocks b0 + tid + 1024 u (0 past the end) into key[0..U)
+    auto load_blocks = [&](int64_t b0, auto &key) {
+        constexpr int U = sizeof(key) / sizeof(key[0]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t b = b0 + tid + (int64_t)u * BS_THREADS;
+            key[u] = bm[b < p.nblk ? b : p.nblk - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) asm volatile("" : "+v"(key[u]));
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t b = b0 + tid + (int64_t)u * BS_THREADS;
+            key[u] = b < p.nblk ? hkey(key[u]) : 0u;
+        }
+    };
+    // keys of vectors vv[u] (0 past the end) into key[0..U)
+    auto load_vectors = [&](const int64_t *vv, auto &key) {
+        constexpr int U = sizeof(key) / sizeof(key[0]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) key[u] = row[vv[u] < p.n ? vv[u] : p.n - 1];
+#pragma unroll
+        for (int u = 0; u < U; ++u) asm volatile("" : "+v"(key[u]));
+#pragma unroll
+        for (int u = 0; u < U; ++u) key[u] = vv[u] < p.n ? hkey(key[u]) : 0u;
+    };
+    uint32_t bk[BB];
+    if (breg) load_blocks(0, bk);
+    auto each_block = [&](auto fn) {
+        if (breg) {
+#pragma unroll
+            for (int u = 0; u < BB; ++u) {
+                const int64_t b = tid + (int64_t)u * BS_THREADS;
+                if (b < p.nblk) fn(b, bk[u]);
+            }
+            return;
+        }
+        for (int64_t b0 = 0; b0 < p.nblk; b0 += (int64_t)RB * BS_THREADS) {
+            uint32_t key[RB];
+            load_blocks(b0, key);
+#pragma unroll
+            for (int u = 0; u < RB; ++u) {
+                const int64_t b = b0 + tid + (int64_t)u * BS_THREADS;
+                if (b < p.nblk) fn(b, key[u]);
+            }
+        }
+    };
+    uint32_t lk[LB];
+    bool lreg = false;
+    int nu = 0;   // listed blocks of this wave (register keys)
+    auto load_listed = [&](int nl) {
+        lreg = nl <= LB * BS_WAVES;
+        if (!lreg) return;
+        nu = nl > wave ? (nl - wave + BS_WAVES - 1) / BS_WAVES : 0;
+        int64_t vv[LB];
+#pragma unroll
+        for (int u = 0; u < LB; ++u)
+            vv[u] = u < nu ? (int64_t)list[wave + u * BS_WAVES] * 64 + lane : p.n;
+        load_vectors(vv, lk);
+    };
+    auto each_listed = [&](int nl, auto fn) {
+        if (lreg) {
+#pragma unroll
+            for (int u = 0; u < LB; ++u) {
+                if (u >= nu) break;
+                const int64_t v = (int64_t)list[wave + u * BS_WAVES] * 64 + lane;
+                if (v < p.n) fn(v, lk[u]);
+            }
+            return;
+        }
+        for (int j0 = 0; j0 < nl; j0 += RB * BS_WAVES) {
+            uint32_t key[RB];
+            int64_t vv[RB];
+#pragma unroll
+            for (int u = 0; u < RB; ++u) {
+                const int j = j0 + wave + u * BS_WAVES;
+                vv[u] = j < nl ? (int64_t)list[j] * 64 + lane : p.n;
+            }
+            load_vectors(vv, key);
+#pragma unroll
+            for (int u = 0; u < RB; ++u) {
+                const int j = j0 + wave + u * BS_WAVES;
+                const int64_t v = j < nl ? (int64_t)list[j] * 64 + lane : p.n;
+                if (v < p.n) fn(v, key[u]);
+            }
+        }
+    };
+    // radix selection: the K-th largest key (1 <= K <= #keys) of a visitor;
+    // returns it and the number of keys above it
+    auto kth = [&](auto each, int K, int &above) -> uint32_t {
+        clear_hist();
+        __syncthreads();
+        each([&](int64_t, uint32_t key) { atomicAdd(&hc[key >> 8], 1); });
+        __syncthreads();
+        if (wave == 0) find_digit(hist, K, sh);
+        __syncthreads();
+        const int hi = sh[0], a1 = sh[1];
+        clear_hist();
+        __syncthreads();
+        each([&](int64_t, uint32_t key) {
+            if ((int)(key >> 8) == hi) atomicAdd(&hc[key & 255u], 1);
+        });
+        __syncthreads();
+        if (wave == 0) find_digit(hist, K - a1, sh);
+        __syncthreads();
+        above = a1 + sh[1];
+        const uint32_t t = ((uint32_t)hi << 8) | (uint32_t)sh[0];
+        __syncthreads();   // sh is read before it is written again
+        return t;
+    };
+    auto finish = [&](float am, int st) {
+        if (tid == 0) {
+            p.amin[q] = am;
+            p.state[q] = st;
+        }
+    };
+    // theta_a: the R-th largest block key (0, every block, when nblk <= R)
+    const bool all_blocks = p.nblk <= R;
+    uint32_t tha = 0;
+    if (!all_blocks) {
+        int above;
+        tha = kth(each_block, R, above);
+    }
+    if (tid == 0) {
+        sh[2] = 0;
+        sh[3] = 0;
+        sh[4] = 0;
+        sh[5] = 0;
+    }
+    __syncthreads();
+    each_block([&](int64_t b, uint32_t key) {
+        if (key >= tha) {
+            const int pos = atomicAdd(&sh[2], 1);
+            if (pos < kListMaxB) list[pos] = (int)b;
+        }
+    });
+    __syncthreads();
+    const int nl = sh[2];
+    if (nl > kListMaxB) {
+        // too many blocks tie at the threshold: no candidates
+        for (int i = tid; i < KC; i += BS_THREADS) out_i[i] = INT_MAX;
+        finish(INFINITY, kSelOverflow);
+        return;
+    }
+    load_listed(nl);
+    if (all_blocks && p.n <= KC) {
+        // every block listed and at most KC vectors: all are candidates
+        each_listed(nl, [&](int64_t v, uint32_t) { out_i[atomicAdd(&sh[3], 1)] = (int)v; });
+        __syncthreads();
+        for (int i = sh[3] + tid; i < KC; i += BS_THREADS) out_i[i] = INT_MAX;
+        finish(-INFINITY, kSelAll);
+        return;
+    }
+    if (!all_blocks) {
+        // the vectors that reach theta_a (at least R)
+        each_listed(nl, [&](int64_t v, uint32_t key) {
+            if (key >= tha) {
+                const int pos = atomicAdd(&sh[3], 1);
+                if (pos < KC) out_i[pos] = (int)v;
+            }
+        });
+        __syncthreads();
+        const int c = sh[3];
+        if (c <= KC) {
+            for (int i = c + tid; i < KC; i += BS_THREADS) out_i[i] = INT_MAX;
+            finish(hkey_value(tha), kSelBound);
+            return;
+        }
+    }
+    // the KC best scores of the listed blocks
+    int n_gt;
+    const uint32_t thb = kth([&](auto fn) { each_listed(nl, fn); }, KC, n_gt);
+    const int need_eq = KC - n_gt;   // keys equal to theta_b to take (>= 1)
+    each_listed(nl, [&](int64_t v, uint32_t key) {
+        if (key > thb) {
+            out_i[atomicAdd(&sh[4], 1)] = (int)v;
+        } else if (key == thb) {
+            const int e = atomicAdd(&sh[5], 1);
+            if (e < need_eq) out_i[n_gt + e] = (int)v;
+        }
+    });
+    finish(hkey_value(thb), kSelBound);
 }
 
 // ------------------------------------------------------- exact rescoring
@@ -493,93 +811,130 @@ struct RescoreParams {
     const float *scales;
     const float *qrot;         // [nqt][d] float32 rotated queries
     const float *cents;
+    const int *top_i;          // [nqt][KC] candidates (INT_MAX: none)
+    const float *amin;         // [nqt] bound on the approximate score of non-candidates
+    const int *state;          // [nqt] kSel*
     const QInfo *info;
-    const float *top_s;        // [nqt][kCand] approximate, sorted
-    const int *top_i;
     int64_t *ids;              // [nqt][k]
     float *scores;
     int *flags;                // [nqt]: 1 = not certified
     int d, bits, chunks, lut_words, k;
 };
 
+// One workgroup per query, KC = 64 S candidate slots.
+//  1. The query's integer table (as the single-query scan builds it).
+//  2. Lane = candidate: wave w takes the 64 candidates of run w % S and the
+//     (w / S)-th of 16 / S slices of the chunks, so all lanes read the same
+//     table rows (as in the scan); partial integer sums meet in LDS (exact,
+//     order-free): bit-identical to the single-query scan's scores.
+//  3. Waves 0..S-1 sort their 64 exact scores; an entry's rank is its lane
+//     plus, in every other sorted run, the number of entries ahead of it
+//     (binary search); ranks below k are written.
+//  4. Certificate: a vector outside the candidates has a stored score at
+//     most amin, so its exact score is at most amin + 2^-11 |amin| +
+//     2^-25 norm + err; if that is below the k-th exact score it cannot
+//     enter the top k.
+template <int S>
 __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p) {
+    constexpr int KC = 64 * S;
+    constexpr int SL = kTableWaves / S;    // chunk slices
     extern __shared__ __attribute__((aligned(16))) float lds[];
     float *red = lds + p.lut_words;         // 16
-    float *ex_s = red + 16;                 // kCand exact scores
-    int *ex_i = reinterpret_cast<int *>(ex_s + kCand);
+    int *sums = reinterpret_cast<int *>(red + 16);   // [KC]
+    float *run_s = reinterpret_cast<float *>(sums + KC);
+    int *run_i = reinterpret_cast<int *>(run_s + KC);
+    int *sh = run_i + KC;                   // [0] valid count, [1] k-th exact score
     const int q = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int run = wave % S, slice = wave / S;
+    const int c0 = p.chunks * slice / SL, c1 = p.chunks * (slice + 1) / SL;
     const TableShape ts{p.d, p.bits, p.lut_words};
+    for (int i = tid; i < KC; i += kTableThreads) sums[i] = 0;
+    if (tid == 0) {
+        sh[0] = 0;
+        sh[1] = __float_as_int(-INFINITY);
+    }
+    // this lane's candidate and its first chunk loads, in flight while the
+    // table is built
+    // (unconditional loads from clamped addresses: a load under a branch is
+    // waited for on the spot)
+    const int v = p.top_i[(int64_t)q * KC + run * 64 + lane];
+    const bool valid = v != INT_MAX;
+    const int vc = valid ? v : 0;
+    const uint4 *src = p.codes + ((int64_t)(vc >> 6) * p.chunks) * 64 + (vc & 63);
+    const float scl = p.scales[vc];
+    constexpr int RING = 4;
+    uint4 w[RING];
+#pragma unroll
+    for (int r = 0; r < RING; ++r) w[r] = src[(int64_t)(c0 + r < c1 ? c0 + r : c0) * 64];
     float qv[2][4];
     load_nibble_query(ts, p.qrot + (int64_t)q * p.d, qv);
     nibble_abs_sum(red, qv);
     __syncthreads();
-    const int sh = build_nibble_table(lds, red, p.cents, ts, qv);
+    const int shx = build_nibble_table(lds, red, p.cents, ts, qv);
     __syncthreads();
     const char *lut = reinterpret_cast<const char *>(lds);
-    // each wave scores kCand / 16 candidates, 4 at a time: their chunk loads
-    // are issued together
-    constexpr int PER = kCand / kTableWaves, GRP = 4;
-    for (int j0 = 0; j0 < PER; j0 += GRP) {
-        int v[GRP];
-        uint4 w[GRP];
+    int acc = 0;
+    for (int c = c0; c < c1; c += RING) {
 #pragma unroll
-        for (int t = 0; t < GRP; ++t) {
-            v[t] = p.top_i[(int64_t)q * kCand + wave * PER + j0 + t];
-            w[t] = make_uint4(0, 0, 0, 0);
-            if (v[t] != INT_MAX && lane < p.chunks)
-                w[t] = p.codes[((int64_t)(v[t] >> 6) * p.chunks + lane) * 64 + (v[t] & 63)];
-        }
-#pragma unroll
-        for (int t = 0; t < GRP; ++t) {
-            const bool valid = v[t] != INT_MAX;
-            int part = (valid && lane < p.chunks) ? nib_chunk(lut + lane * 2048, w[t]) : 0;
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-            if (lane == 0) {
-                const int j = wave * PER + j0 + t;
-                ex_s[j] = valid ? ldexpf((float)part * p.scales[v[t]], -sh) : -INFINITY;
-                ex_i[j] = valid ? v[t] : INT_MAX;
+        for (int r = 0; r < RING; ++r) {
+            if (c + r < c1) {
+                acc += nib_chunk(lut + (c + r) * 2048, w[r]);
+                const int nc = c + r + RING;
+                w[r] = src[(int64_t)(nc < c1 ? nc : c0) * 64];
             }
         }
     }
+    if (valid) atomicAdd(&sums[run * 64 + lane], acc);
     __syncthreads();
-    if (wave == 0) {
-        // exact scores sorted into one list of kCand
-        float ls[kCandS];
-        int li[kCandS];
-#pragma unroll
-        for (int a = 0; a < kCandS; ++a) {
-            ls[a] = -INFINITY;
-            li[a] = INT_MAX;
+    float s_ = -INFINITY;
+    int i_ = INT_MAX;
+    if (wave < S) {
+        if (valid) {
+            s_ = ldexpf((float)sums[run * 64 + lane] * scl, -shx);
+            i_ = v;
         }
+        wave_sort64(s_, i_, lane);
+        run_s[wave * 64 + lane] = s_;
+        run_i[wave * 64 + lane] = i_;
+        const int c = __popcll(__ballot(i_ != INT_MAX));
+        if (lane == 0 && c) atomicAdd(&sh[0], c);
+    }
+    __syncthreads();
+    if (wave < S && i_ != INT_MAX) {
+        int rank = lane;
+        for (int b = 0; b < S; ++b) {
+            if (b == wave) continue;
+            const float *rs = run_s + b * 64;
+            const int *ri = run_i + b * 64;
+            int pos = 0;   // entries of run b ahead of this one
 #pragma unroll
-        for (int a = 0; a < kCandS; ++a) {
-            float s = ex_s[a * 64 + lane];
-            int i = ex_i[a * 64 + lane];
-            wave_sort64(s, i, lane);
-            merge_sorted64<kCandS>(ls, li, s, i, lane);
+            for (int step = 64; step >= 1; step >>= 1)
+                if (pos + step <= 64 && better(rs[pos + step - 1], ri[pos + step - 1], s_, i_))
+                    pos += step;
+            rank += pos;
         }
-        if (lane < p.k) {
-            const bool empty = !(ls[0] > -INFINITY);
-            p.ids[(int64_t)q * p.k + lane] = empty ? -1 : (int64_t)li[0];
-            p.scores[(int64_t)q * p.k + lane] = empty ? -INFINITY : ls[0];
+        if (rank < p.k) {
+            p.ids[(int64_t)q * p.k + rank] = (int64_t)i_;
+            p.scores[(int64_t)q * p.k + rank] = s_;
+            if (rank == p.k - 1) sh[1] = __float_as_int(s_);
         }
-        // Certificate: a vector outside the candidates has a stored score at
-        // most the last candidate's, so its exact score is at most
-        // amin + 2^-11 |amin| + 2^-25 norm + err; below the k-th exact
-        // score it cannot enter the top k.
-        int nvalid = 0;
-#pragma unroll
-        for (int a = 0; a < kCandS; ++a)
-            nvalid += __popcll(__ballot(p.top_i[(int64_t)q * kCand + a * 64 + lane] != INT_MAX));
-        const float ek = __shfl(ls[0], p.k - 1, 64);
+    }
+    __syncthreads();
+    const int nv = sh[0];
+    for (int r = nv + tid; r < p.k; r += kTableThreads) {
+        p.ids[(int64_t)q * p.k + r] = -1;
+        p.scores[(int64_t)q * p.k + r] = -INFINITY;
+    }
+    if (tid == 0) {
+        const float ek = __int_as_float(sh[1]);
         const QInfo qi = p.info[q];
-        const double amin = (double)p.top_s[(int64_t)q * kCand + kCand - 1] * qi.norm;
+        const double amin = (double)p.amin[q] * qi.norm;
         const double reach = amin + ldexp(1.0, -11) * fabs(amin) + ldexp(1.0, -25) * qi.norm +
                              (double)qi.err;
-        const bool cert = nvalid < kCand || reach < (double)ek;
-        if (lane == 0) p.flags[q] = cert ? 0 : 1;
+        const int st = p.state[q];
+        const bool cert = st == kSelAll || (st == kSelBound && reach < (double)ek);
+        p.flags[q] = cert ? 0 : 1;
     }
 }
 
@@ -638,8 +993,8 @@ __global__ void scale_max_kernel(const float *__restrict__ s, int64_t n, int *sm
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 struct BatchLayout {
-    size_t q16, info, approx, cand_s, cand_i, top_s, top_i, gbound, flags, rows, qc, allow_c, ids_c,
-        scores_c, lut, total;
+    size_t q16, info, approx, bmax, cand_s, cand_i, top_i, amin, state, gbound, flags, rows, qc,
+        allow_c, ids_c, scores_c, lut, total;
 };
 
 // Row length of the approximate-score matrix: whole 512-vector select units.
@@ -655,14 +1010,18 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
     o += align256(kTile * sizeof(QInfo));
     L.approx = o;
     o += align256((size_t)kTile * npad * 2);
+    L.bmax = o;
+    o += align256((size_t)kTile * s.nblk * 2);
     L.cand_s = o;
-    o += align256((size_t)kTile * SEL_GROUPS * kCand * 4);
+    o += align256((size_t)kTile * SEL_GROUPS * kCandMax * 4);
     L.cand_i = o;
-    o += align256((size_t)kTile * SEL_GROUPS * kCand * 4);
-    L.top_s = o;
-    o += align256((size_t)kTile * kCand * 4);
+    o += align256((size_t)kTile * SEL_GROUPS * kCandMax * 4);
     L.top_i = o;
-    o += align256((size_t)kTile * kCand * 4);
+    o += align256((size_t)kTile * kCandMax * 4);
+    L.amin = o;
+    o += align256((size_t)kTile * 4);
+    L.state = o;
+    o += align256((size_t)kTile * 4);
     L.gbound = o;
     o += align256(kTile * kBoundStride * 4);
     L.flags = o;
@@ -691,7 +1050,7 @@ size_t score_lds_bytes(int d) {
 }
 
 bool mfma_search_supported(const ScanShape &s, int k) {
-    return s.bits == 4 && s.chunks % 8 == 0 && k <= 64 && s.W <= 64 &&
+    return s.bits == 4 && s.chunks % 8 == 0 && k <= kMaxBatchK && s.W <= 64 &&
            score_lds_bytes(s.d) <= 160 * 1024;
 }
 
@@ -719,21 +1078,28 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     _Float16 *q16 = reinterpret_cast<_Float16 *>(w8 + L.q16);
     QInfo *info = reinterpret_cast<QInfo *>(w8 + L.info);
     _Float16 *approx = reinterpret_cast<_Float16 *>(w8 + L.approx);
+    _Float16 *bmax = reinterpret_cast<_Float16 *>(w8 + L.bmax);
     float *cand_s = reinterpret_cast<float *>(w8 + L.cand_s);
     int *cand_i = reinterpret_cast<int *>(w8 + L.cand_i);
-    float *top_s = reinterpret_cast<float *>(w8 + L.top_s);
     int *top_i = reinterpret_cast<int *>(w8 + L.top_i);
+    float *amin = reinterpret_cast<float *>(w8 + L.amin);
+    int *state = reinterpret_cast<int *>(w8 + L.state);
     int *gbound = reinterpret_cast<int *>(w8 + L.gbound);
     int *flags = reinterpret_cast<int *>(w8 + L.flags);
     const int64_t npad = approx_row(s);
     const size_t lds_scores = score_lds_bytes(s.d);
-    const size_t lds_rescore = (size_t)s.chunks * 2048 + (16 + 2 * kCand) * 4;
+    const int KC = k <= 64 ? 256 : kCandMax;   // candidates per query
+    // table, 16 floats, integer sums and sorted (score, id) runs, two counters
+    const size_t lds_rescore = (size_t)s.chunks * 2048 + 16 * 4 + (size_t)KC * 12 + 16;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)mfma_scores_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)rescore_kernel,
+            e = hipFuncSetAttribute((const void *)rescore_kernel<4>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)rescore_kernel<8>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -749,6 +1115,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         sp.info = info;
         sp.cents = cents32;
         sp.out = approx;
+        sp.bmax = bmax;
         sp.n = s.n;
         sp.nblk = s.nblk;
         sp.npad = npad;
@@ -756,28 +1123,52 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         sp.chunks = s.chunks;
         sp.nqt = nqt;
         hipLaunchKernelGGL(mfma_scores_kernel, dim3(grid), dim3(MF_THREADS), lds_scores, stream, sp);
-        hipLaunchKernelGGL(fill_order_keys, dim3(1), dim3(64), 0, stream, gbound, nqt);
-        SelectParams sl{};
-        sl.approx = approx;
-        sl.tenants = tenants;
-        sl.allow = allow ? allow + q0 * s.W : nullptr;
-        sl.cand_s = cand_s;
-        sl.cand_i = cand_i;
-        sl.gbound = gbound;
-        sl.n = s.n;
-        sl.npad = npad;
-        sl.W = s.W;
-        hipLaunchKernelGGL(select_kernel, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0, stream, sl);
-        hipLaunchKernelGGL(select_merge_kernel, dim3(nqt), dim3(256), 0, stream, cand_s, cand_i,
-                           top_s, top_i);
+        if (allow) {
+            // the block maxima ignore the allowlist: select over every allowed score
+            hipLaunchKernelGGL(fill_order_keys, dim3(1), dim3(64), 0, stream, gbound, nqt);
+            SelectParams sl{};
+            sl.approx = approx;
+            sl.tenants = tenants;
+            sl.allow = allow + q0 * s.W;
+            sl.cand_s = cand_s;
+            sl.cand_i = cand_i;
+            sl.gbound = gbound;
+            sl.n = s.n;
+            sl.npad = npad;
+            sl.W = s.W;
+            if (KC == 256) {
+                hipLaunchKernelGGL(select_kernel<4>, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0,
+                                   stream, sl);
+                hipLaunchKernelGGL(select_merge_kernel<4>, dim3(nqt), dim3(256), 0, stream, cand_s,
+                                   cand_i, top_i, amin, state);
+            } else {
+                hipLaunchKernelGGL(select_kernel<8>, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0,
+                                   stream, sl);
+                hipLaunchKernelGGL(select_merge_kernel<8>, dim3(nqt), dim3(256), 0, stream, cand_s,
+                                   cand_i, top_i, amin, state);
+            }
+        } else {
+            BlockSelParams bp{};
+            bp.approx = reinterpret_cast<const uint16_t *>(approx);
+            bp.bmax = reinterpret_cast<const uint16_t *>(bmax);
+            bp.top_i = top_i;
+            bp.amin = amin;
+            bp.state = state;
+            bp.n = s.n;
+            bp.nblk = s.nblk;
+            bp.npad = npad;
+            bp.KC = KC;
+            hipLaunchKernelGGL(block_select_kernel, dim3(nqt), dim3(BS_THREADS), 0, stream, bp);
+        }
         RescoreParams rp{};
         rp.codes = reinterpret_cast<const uint4 *>(blocked);
         rp.scales = scales;
         rp.qrot = Qrot + q0 * s.d;
         rp.cents = cents32;
-        rp.info = info;
-        rp.top_s = top_s;
         rp.top_i = top_i;
+        rp.amin = amin;
+        rp.state = state;
+        rp.info = info;
         rp.ids = ids + q0 * k;
         rp.scores = scores + q0 * k;
         rp.flags = flags + q0;
@@ -786,7 +1177,10 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         rp.chunks = s.chunks;
         rp.lut_words = s.chunks * 512;
         rp.k = k;
-        hipLaunchKernelGGL(rescore_kernel, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
+        if (KC == 256)
+            hipLaunchKernelGGL(rescore_kernel<4>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
+        else
+            hipLaunchKernelGGL(rescore_kernel<8>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -32,6 +32,9 @@ constexpr int kDppXor3 = 0x1B;        // quad_perm [3,2,1,0]
 constexpr int kDppRowShl4 = 0x104;    // lane i <- lane i+4 within the row
 constexpr int kDppRowShr4 = 0x114;    // lane i <- lane i-4 within the row
 constexpr int kDppRowRor8 = 0x128;    // lane i <- lane (i+8) mod 16 == i ^ 8
+constexpr int kDppRowRor4 = 0x124;    // lane i <- lane (i+4) mod 16 within the row
+constexpr int kDppRowRor2 = 0x122;    // lane i <- lane (i+2) mod 16
+constexpr int kDppRowRor1 = 0x121;    // lane i <- lane (i+1) mod 16
 constexpr int kDppRowMirror = 0x140;  // lane i <- lane 15-i == i ^ 15
 constexpr int kDppHalfMirror = 0x141; // lane i <- lane 7-i within 8 == i ^ 7
 
