@@ -33,6 +33,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 #include <vector>
 
 #include "kernels.h"
@@ -48,6 +49,7 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
 constexpr int kCandMax = 512;      // candidates per query kept for exact rescoring (KC <= this)
+constexpr int kCandMin = 64;
 constexpr int kMaxBatchK = 256;    // largest k of the batched path
 constexpr int BS_THREADS = 1024;   // block_select_kernel
 constexpr int BS_WAVES = BS_THREADS / 64;
@@ -838,9 +840,10 @@ template <int S>
 __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p) {
     constexpr int KC = 64 * S;
     constexpr int SL = kTableWaves / S;    // chunk slices
+    constexpr int CB = 12;                 // chunk loads of a lane in flight at once
     extern __shared__ __attribute__((aligned(16))) float lds[];
     float *red = lds + p.lut_words;         // 16
-    int *sums = reinterpret_cast<int *>(red + 16);   // [KC]
+    int *sums = reinterpret_cast<int *>(red + 16);   // [KC]: integer sums, then ranks
     float *run_s = reinterpret_cast<float *>(sums + KC);
     int *run_i = reinterpret_cast<int *>(run_s + KC);
     int *sh = run_i + KC;                   // [0] valid count, [1] k-th exact score
@@ -854,39 +857,44 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
         sh[0] = 0;
         sh[1] = __float_as_int(-INFINITY);
     }
-    // this lane's candidate and its first chunk loads, in flight while the
-    // table is built
-    // (unconditional loads from clamped addresses: a load under a branch is
-    // waited for on the spot)
+    // Loads in the order they are needed (completion is in order): the
+    // query's coordinates, this lane's candidate, the certificate inputs,
+    // then the candidate's chunks, in flight while the table is built.
+    // Every load is unconditional, from a clamped address.
+    float qv[2][4];
+    load_nibble_query(ts, p.qrot + (int64_t)q * p.d, qv);
     const int v = p.top_i[(int64_t)q * KC + run * 64 + lane];
+    const QInfo qi = p.info[q];
+    const float amin_s = p.amin[q];
+    const int st = p.state[q];
     const bool valid = v != INT_MAX;
     const int vc = valid ? v : 0;
     const uint4 *src = p.codes + ((int64_t)(vc >> 6) * p.chunks) * 64 + (vc & 63);
     const float scl = p.scales[vc];
-    constexpr int RING = 4;
-    uint4 w[RING];
+    uint4 w[CB];
+    auto load_chunks = [&](int cb) {
 #pragma unroll
-    for (int r = 0; r < RING; ++r) w[r] = src[(int64_t)(c0 + r < c1 ? c0 + r : c0) * 64];
-    float qv[2][4];
-    load_nibble_query(ts, p.qrot + (int64_t)q * p.d, qv);
+        for (int r = 0; r < CB; ++r) {
+            const int c = cb + r < c1 ? cb + r : c0;
+            w[r] = src[(int64_t)c * 64];
+        }
+    };
+    load_chunks(c0);
     nibble_abs_sum(red, qv);
     __syncthreads();
     const int shx = build_nibble_table(lds, red, p.cents, ts, qv);
     __syncthreads();
     const char *lut = reinterpret_cast<const char *>(lds);
     int acc = 0;
-    for (int c = c0; c < c1; c += RING) {
+    for (int cb = c0; cb < c1; cb += CB) {
+        if (cb > c0) load_chunks(cb);
 #pragma unroll
-        for (int r = 0; r < RING; ++r) {
-            if (c + r < c1) {
-                acc += nib_chunk(lut + (c + r) * 2048, w[r]);
-                const int nc = c + r + RING;
-                w[r] = src[(int64_t)(nc < c1 ? nc : c0) * 64];
-            }
-        }
+        for (int r = 0; r < CB; ++r)
+            if (cb + r < c1) acc += nib_chunk(lut + (cb + r) * 2048, w[r]);
     }
     if (valid) atomicAdd(&sums[run * 64 + lane], acc);
     __syncthreads();
+    // waves 0..S-1: sort their runs of 64 exact scores
     float s_ = -INFINITY;
     int i_ = INT_MAX;
     if (wave < S) {
@@ -901,23 +909,39 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
         if (lane == 0 && c) atomicAdd(&sh[0], c);
     }
     __syncthreads();
-    if (wave < S && i_ != INT_MAX) {
-        int rank = lane;
-        for (int b = 0; b < S; ++b) {
-            if (b == wave) continue;
-            const float *rs = run_s + b * 64;
-            const int *ri = run_i + b * 64;
-            int pos = 0;   // entries of run b ahead of this one
+    // rank of entry e = its place in its run + the entries ahead of it in
+    // each other run (binary search); thread t searches for entry t % KC in
+    // the runs (run(e) + 1 + t / KC + g * (1024 / KC)) % S
+    for (int e = tid; e < KC; e += kTableThreads) sums[e] = e & 63;
+    __syncthreads();
+    {
+        const int e = tid % KC, er = e >> 6;
+        const float es = run_s[e];
+        const int ei = run_i[e];
+        int add = 0;
+        if (ei != INT_MAX) {
+            for (int o = 1 + tid / KC; o < S; o += kTableThreads / KC) {
+                const int b = (er + o) % S;
+                const float *rs = run_s + b * 64;
+                const int *ri = run_i + b * 64;
+                int pos = 0;
 #pragma unroll
-            for (int step = 64; step >= 1; step >>= 1)
-                if (pos + step <= 64 && better(rs[pos + step - 1], ri[pos + step - 1], s_, i_))
-                    pos += step;
-            rank += pos;
+                for (int step = 64; step >= 1; step >>= 1)
+                    if (pos + step <= 64 && better(rs[pos + step - 1], ri[pos + step - 1], es, ei))
+                        pos += step;
+                add += pos;
+            }
         }
-        if (rank < p.k) {
-            p.ids[(int64_t)q * p.k + rank] = (int64_t)i_;
-            p.scores[(int64_t)q * p.k + rank] = s_;
-            if (rank == p.k - 1) sh[1] = __float_as_int(s_);
+        if (add) atomicAdd(&sums[e], add);
+    }
+    __syncthreads();
+    for (int e = tid; e < KC; e += kTableThreads) {
+        const int ei = run_i[e];
+        const int rank = sums[e];
+        if (ei != INT_MAX && rank < p.k) {
+            p.ids[(int64_t)q * p.k + rank] = (int64_t)ei;
+            p.scores[(int64_t)q * p.k + rank] = run_s[e];
+            if (rank == p.k - 1) sh[1] = __float_as_int(run_s[e]);
         }
     }
     __syncthreads();
@@ -928,11 +952,9 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
     }
     if (tid == 0) {
         const float ek = __int_as_float(sh[1]);
-        const QInfo qi = p.info[q];
-        const double amin = (double)p.amin[q] * qi.norm;
+        const double amin = (double)amin_s * qi.norm;
         const double reach = amin + ldexp(1.0, -11) * fabs(amin) + ldexp(1.0, -25) * qi.norm +
                              (double)qi.err;
-        const int st = p.state[q];
         const bool cert = st == kSelAll || (st == kSelBound && reach < (double)ek);
         p.flags[q] = cert ? 0 : 1;
     }
@@ -991,6 +1013,26 @@ __global__ void scale_max_kernel(const float *__restrict__ s, int64_t n, int *sm
 }
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Candidate slots for a given k: eight per result, 64 to 512 (the
+// certificate needs the KC-th approximate score, plus the error bound, to
+// fall below the k-th exact one; candidates are cheap next to a re-run).
+int batch_candidates(int k) {
+    int kc = kCandMin;
+    while (kc < 8 * k && kc < kCandMax) kc *= 2;
+    return kc;
+}
+
+// Calls fn with std::integral_constant<int, KC / 64>.
+template <class Fn>
+void with_slots(int KC, Fn fn) {
+    switch (KC) {
+    case 64: fn(std::integral_constant<int, 1>()); break;
+    case 128: fn(std::integral_constant<int, 2>()); break;
+    case 256: fn(std::integral_constant<int, 4>()); break;
+    default: fn(std::integral_constant<int, 8>()); break;
+    }
+}
 
 struct BatchLayout {
     size_t q16, info, approx, bmax, cand_s, cand_i, top_i, amin, state, gbound, flags, rows, qc,
@@ -1088,19 +1130,18 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     int *flags = reinterpret_cast<int *>(w8 + L.flags);
     const int64_t npad = approx_row(s);
     const size_t lds_scores = score_lds_bytes(s.d);
-    const int KC = k <= 64 ? 256 : kCandMax;   // candidates per query
+    const int KC = batch_candidates(k);   // candidates per query
     // table, 16 floats, integer sums and sorted (score, id) runs, two counters
     const size_t lds_rescore = (size_t)s.chunks * 2048 + 16 * 4 + (size_t)KC * 12 + 16;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)mfma_scores_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)rescore_kernel<4>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)rescore_kernel<8>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        for (int S = 1; S <= 8 && e == hipSuccess; S *= 2)
+            with_slots(64 * S, [&](auto sc) {
+                e = hipFuncSetAttribute((const void *)rescore_kernel<decltype(sc)::value>,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            });
         if (e != hipSuccess) return e;
         attr_set = true;
     }
@@ -1136,17 +1177,13 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
             sl.n = s.n;
             sl.npad = npad;
             sl.W = s.W;
-            if (KC == 256) {
-                hipLaunchKernelGGL(select_kernel<4>, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0,
+            with_slots(KC, [&](auto sc) {
+                constexpr int S = decltype(sc)::value;
+                hipLaunchKernelGGL(select_kernel<S>, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0,
                                    stream, sl);
-                hipLaunchKernelGGL(select_merge_kernel<4>, dim3(nqt), dim3(256), 0, stream, cand_s,
+                hipLaunchKernelGGL(select_merge_kernel<S>, dim3(nqt), dim3(256), 0, stream, cand_s,
                                    cand_i, top_i, amin, state);
-            } else {
-                hipLaunchKernelGGL(select_kernel<8>, dim3(SEL_GROUPS, nqt), dim3(SEL_THREADS), 0,
-                                   stream, sl);
-                hipLaunchKernelGGL(select_merge_kernel<8>, dim3(nqt), dim3(256), 0, stream, cand_s,
-                                   cand_i, top_i, amin, state);
-            }
+            });
         } else {
             BlockSelParams bp{};
             bp.approx = reinterpret_cast<const uint16_t *>(approx);
@@ -1177,10 +1214,11 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         rp.chunks = s.chunks;
         rp.lut_words = s.chunks * 512;
         rp.k = k;
-        if (KC == 256)
-            hipLaunchKernelGGL(rescore_kernel<4>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
-        else
-            hipLaunchKernelGGL(rescore_kernel<8>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream, rp);
+        with_slots(KC, [&](auto sc) {
+            constexpr int S = decltype(sc)::value;
+            hipLaunchKernelGGL(rescore_kernel<S>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream,
+                               rp);
+        });
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
