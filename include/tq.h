@@ -327,7 +327,7 @@ tq_status tq_search_postfilter(const tq_index *idx, const float *Q_dev,
  *                approximation error -- proves that the exact top k lies
  *                among the candidates; queries without one are re-run on the
  *                LUT path (see tq_last_search_fallbacks).  Needs 4-bit codes,
- *                d % 256 == 0, d <= 1536, k <= 256 and n_tenants <= 4096,
+ *                d % 256 == 0, d <= 1792, k <= 256 and n_tenants <= 4096,
  *                else TQ_EUNSUPPORTED.  Synchronises `stream` once per call, to
  *                read the certificates on the host. */
 typedef enum {

@@ -1115,7 +1115,7 @@ tq_status tq_search_workspace_size(const tq_index *idx, int64_t nq, int32_t k, i
     if (base != TQ_PATH_AUTO && base != TQ_PATH_LUT && base != TQ_PATH_MFMA)
         return fail(TQ_EINVAL, "unknown path");
     if (base == TQ_PATH_MFMA && !mfma_search_supported(shape_of(idx), k))
-        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1792, "
                                      "k <= 256 and at most 4096 tenants");
     if (base == TQ_PATH_MFMA && idx->calibrated)
         return fail(TQ_EUNSUPPORTED, "matrix-core path does not take a TQ+ calibrated index");
@@ -1145,7 +1145,7 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     if (st != TQ_OK) return st;
     const ScanShape sh = shape_of(idx);
     if (base == TQ_PATH_MFMA && !mfma_search_supported(sh, k))
-        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1536, "
+        return fail(TQ_EUNSUPPORTED, "matrix-core path needs 4-bit codes, d % 256 == 0, d <= 1792, "
                                      "k <= 256 and at most 4096 tenants");
     if (slot_allow && !allow_dev) return fail(TQ_EINVAL, "slot allowlist flag without an allowlist");
     SearchFilter filter;

@@ -63,7 +63,6 @@ constexpr int kSelAll = 2;         // every vector is a candidate
 constexpr int MF_THREADS = 768;    // 12 waves: three per SIMD, 168 registers each
 constexpr int MF_RING = 8;         // chunk loads in flight per wave
 constexpr int kTableBytes = 256 * 32 * 4;   // byte table, 32 replicas
-constexpr int MF_WAVES = MF_THREADS / 64;
 constexpr int SEL_THREADS = 256;
 constexpr int SEL_GROUPS = 32;     // select workgroups per query
 constexpr int kBoundStride = 32;  // ints between the global bounds of two queries
@@ -198,10 +197,11 @@ __device__ inline half8 dequant8(uint32_t w, uint32_t lb) {
 // tile (32 rows of d float16, rows padded by 16 bytes so the 16 rows read by
 // one instruction fall in distinct banks) stay in LDS.  Waves claim the workgroup's
 // 64-vector blocks one at a time from an LDS counter (one ahead, so the ring
-// of MF_RING chunk loads runs on into the next block).  For a chunk, lane 16q+i
-// has loaded the 4 words of vector 16q+i; written to the wave's LDS slot and
-// read back as word q of vectors i, 16+i, 32+i, 48+i (bank-conflict free),
-// they are the B operands (k = 8q..8q+7, column i) of the four 16-vector
+// of MF_RING chunk loads runs on into the next block).  For a chunk, lane 16m+i
+// (row m of 16 lanes) has loaded the 4 words of vector 16m+i; a 4 x 4
+// transpose across the rows (two v_permlane32_swap, then two
+// v_permlane16_swap) leaves word q of vectors i, 16+i, 32+i, 48+i in lane
+// 16q+i: the B operands (k = 8q..8q+7, column i) of the four 16-vector
 // MFMAs.
 __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -209,8 +209,6 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
     uint32_t *T = reinterpret_cast<uint32_t *>(smem);          // byte table x 32, at 0
     _Float16 *Qs = reinterpret_cast<_Float16 *>(smem + kTableBytes);   // [kTile][ld]
     int *ctr = reinterpret_cast<int *>(smem + kTableBytes + (size_t)kTile * ld * 2);
-    // per-wave staging slot of one chunk (64 lanes x 16 bytes)
-    char *stg = smem + kTableBytes + (size_t)kTile * ld * 2 + 16 + (threadIdx.x >> 6) * 1024;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -292,17 +290,19 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
             for (int m = 0; m < 4; ++m) acc[t][m] = float4v{0.f, 0.f, 0.f, 0.f};
         // one chunk; the ring index is a compile-time constant at every call
         auto chunk = [&](const int c, uint4 &slot) {
-            // the chunk goes through the wave's staging slot and comes back
-            // transposed (LDS runs a wave's operations in order)
-            *reinterpret_cast<uint4 *>(stg + lane * 16) = slot;
+            // W_q (row m) = word q of vector 16m+i.  permlane32_swap(a, b)
+            // exchanges a's rows 2, 3 with b's rows 0, 1; permlane16_swap(a, b)
+            // exchanges a's rows 1, 3 with b's rows 0, 2.  After both levels
+            // r[m] (row q) = W_q (row m).
+            const auto s02 = __builtin_amdgcn_permlane32_swap(slot.x, slot.z, false, false);
+            const auto s13 = __builtin_amdgcn_permlane32_swap(slot.y, slot.w, false, false);
+            const auto t01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+            const auto t23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+            const uint32_t r[4] = {t01[0], t01[1], t23[0], t23[1]};
             // refill MF_RING chunks ahead: this block, then the next one
             const int nc = c + MF_RING;
             slot = load_stream((nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64) + lane);
             __builtin_amdgcn_sched_barrier(kKeepVmemB);
-            uint32_t r[4];
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-                r[m] = *reinterpret_cast<const uint32_t *>(stg + (16 * m + qrow) * 16 + kq * 4);
             const half8 a0 = *reinterpret_cast<const half8 *>(qa0 + c * 32);
             const half8 a1 = *reinterpret_cast<const half8 *>(qa1 + c * 32);
 #pragma unroll
@@ -1086,9 +1086,9 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
 
 }  // namespace
 
-// LDS of the score kernel: replicated byte table, query tile, staging.
+// LDS of the score kernel: replicated byte table, query tile, counter.
 size_t score_lds_bytes(int d) {
-    return kTableBytes + (size_t)kTile * (d + 8) * 2 + 16 + MF_WAVES * 1024;
+    return kTableBytes + (size_t)kTile * (d + 8) * 2 + 16;
 }
 
 bool mfma_search_supported(const ScanShape &s, int k) {

@@ -144,7 +144,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
                       const float *qconst = nullptr);
 
 // Batched search of a tile of queries on the matrix cores with exact
-// rescoring (b = 4, chunks % 8 == 0, d <= 1536, k <= 256, at most 4096
+// rescoring (b = 4, chunks % 8 == 0, d <= 1792, k <= 256, at most 4096
 // tenants).
 // cmax16 = max |float16(c_l)|, dmax = max |float16(c_l) - c_l| over the
 // float32 centroids cents32.

@@ -170,6 +170,23 @@ def test_certificate_failure_falls_back(env):
     assert np.array_equal(ids.cpu().numpy()[0], np.arange(10))   # ties: lowest ids
 
 
+def test_largest_dimension():
+    """d = 1792, the largest dimension whose query tile fits in LDS, against
+    the single-query path and the oracle."""
+    d = 1792
+    X = synth.isotropic_mixture(3000, d, seed=50)
+    Q = synth.isotropic_queries(X, 16, seed=51)
+    cb, rot = tq.Codebook(d, 4), tq.Rotation(d, 7)
+    idx = tq.Index(cb, rot, n_tenants=1)
+    idx.add(torch.from_numpy(X).cuda())
+    Qd = torch.from_numpy(Q).cuda()
+    ids, sc = idx.search(Qd, 10, path="mfma")
+    same_as_lut(idx, Qd, 10, ids, sc)
+    R32 = oracle.haar_rotation(d, 7)[1]
+    check_topk_sampled(ids.cpu().numpy(), sc.cpu().numpy(), X, R32, oracle.lloyd_max(d, 4), Q, 10,
+                       np.arange(X.shape[0]))
+
+
 def test_unsupported_shapes_rejected(env):
     with pytest.raises(tq.TQError, match="TQ_EUNSUPPORTED"):
         env.idx.search(env.Qd, 257, path="mfma")
