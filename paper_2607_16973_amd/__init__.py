@@ -18,7 +18,7 @@ import numpy as np
 
 from ._lib import FLAG_PREROTATED, FLAG_SLOT_ALLOW, PATHS, TQError, check, lib
 
-__all__ = ["Codebook", "Rotation", "Index", "TQError", "rotate_quantize",
+__all__ = ["Codebook", "Rotation", "Index", "IdMapIndex", "TQError", "rotate_quantize",
            "rotate_queries", "version", "last_search_fallbacks"]
 
 
@@ -40,6 +40,13 @@ def _torch():
 def _stream(device=None):
     torch = _torch()
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _shape(t, shape, name):
+    """Raises ValueError unless tensor t has this shape.  The library takes
+    raw device pointers and cannot check the size of what they point to."""
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
 
 
 def _dev_ptr(t, dtype, name, ndim=None):
@@ -111,6 +118,9 @@ def rotate_quantize(cb: Codebook, rot: Rotation, X, codes=None, scales=None):
     [n, d*bits/8], scales float32 [n]).  Synchronises the current stream."""
     torch = _torch()
     n = X.shape[0]
+    _shape(X, (n, cb.d), "X")
+    _shape(codes, (n, cb.d * cb.bits // 8), "codes")
+    _shape(scales, (n,), "scales")
     if codes is None:
         codes = torch.empty((n, cb.d * cb.bits // 8), dtype=torch.uint8, device=X.device)
     if scales is None:
@@ -124,6 +134,8 @@ def rotate_quantize(cb: Codebook, rot: Rotation, X, codes=None, scales=None):
 def rotate_queries(rot: Rotation, Q, out=None):
     """q' = R q for every row of Q (cuda float32 [nq, d])."""
     torch = _torch()
+    _shape(Q, (Q.shape[0], rot.d), "Q")
+    _shape(out, tuple(Q.shape), "out")
     if out is None:
         out = torch.empty_like(Q)
     check(lib.tq_rotate_queries(rot._h, _dev_ptr(Q, torch.float32, "Q", 2), Q.shape[0],
@@ -205,6 +217,7 @@ class Index:
         """TQ+ calibration (section II-B) fitted to the rows of X (cuda
         float32 [m, d]) before the first vector is added (tq_index_calibrate)."""
         torch = _torch()
+        _shape(X, (X.shape[0], self.d), "X")
         check(lib.tq_index_calibrate(self._h, _dev_ptr(X, torch.float32, "X", 2), X.shape[0],
                                      _stream(X.device)))
 
@@ -226,14 +239,22 @@ class Index:
                                        kappa.ctypes.data_as(ctypes.c_void_p), ctypes.byref(has)))
         return (mu, kappa) if has.value else None
 
+    def _check_rows(self, n, X=None, codes=None, scales=None, tenants=None):
+        _shape(X, (n, self.d), "X")
+        _shape(codes, (n, self.d * self.bits // 8), "codes")
+        _shape(scales, (n,), "scales")
+        _shape(tenants, (n,), "tenants")
+
     def add(self, X, tenants=None) -> None:
         torch = _torch()
+        self._check_rows(X.shape[0], X=X, tenants=tenants)
         check(lib.tq_index_add(self._h, _dev_ptr(X, torch.float32, "X", 2),
                                _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
                                X.shape[0], _stream(X.device)))
 
     def add_codes(self, codes, scales, tenants=None) -> None:
         torch = _torch()
+        self._check_rows(codes.shape[0], codes=codes, scales=scales, tenants=tenants)
         check(lib.tq_index_add_codes(self._h, _dev_ptr(codes, torch.uint8, "codes", 2),
                                      _dev_ptr(scales, torch.float32, "scales", 1),
                                      _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
@@ -267,19 +288,21 @@ class Index:
         returns its external ids (uint64 bit patterns)."""
         torch = _torch()
         nq = Q.shape[0]
+        _shape(Q, (nq, self.d), "Q")
+        _shape(ids, (nq, k), "ids")
+        _shape(scores, (nq, k), "scores")
         flags = FLAG_PREROTATED if prerotated else 0
         if slot_allow is not None:
             if allow is not None:
                 raise ValueError("give allow or slot_allow, not both")
-            if tuple(slot_allow.shape) != (nq, (self.n_slots + 63) // 64):
-                raise ValueError("slot_allow must have shape (nq, %d)" % ((self.n_slots + 63) // 64))
+            _shape(slot_allow, (nq, (self.n_slots + 63) // 64), "slot_allow")
             allow, flags = slot_allow, flags | FLAG_SLOT_ALLOW
+        else:
+            _shape(allow, (nq, self.words), "allow")
         if ids is None:
             ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
         if scores is None:
             scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
-        elif allow is not None and tuple(allow.shape) != (nq, self.words):
-            raise ValueError("allow must have shape (nq, %d)" % self.words)
         need = self.workspace_bytes(nq, k, path)
         if workspace is None:
             if self._ws is None or self._ws.numel() < need:
@@ -289,7 +312,8 @@ class Index:
                                _dev_ptr(allow, torch.int64, "allow") if allow is not None else None,
                                PATHS[path] | flags,
                                ctypes.c_void_p(workspace.data_ptr()),
-                               workspace.numel(), _dev_ptr(ids, torch.int64, "ids"),
+                               workspace.numel() * workspace.element_size(),
+                               _dev_ptr(ids, torch.int64, "ids"),
                                _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
         return ids, scores
 
@@ -299,8 +323,8 @@ class Index:
         (cuda int64 [nq, words])."""
         torch = _torch()
         nq = Q.shape[0]
-        if tuple(allow.shape) != (nq, self.words):
-            raise ValueError("allow must have shape (nq, %d)" % self.words)
+        _shape(Q, (nq, self.d), "Q")
+        _shape(allow, (nq, self.words), "allow")
         ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
         scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
         check(lib.tq_search_postfilter(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k, overfetch,
@@ -313,6 +337,8 @@ class Index:
         """tq_search: the library allocates its own stream-ordered workspace."""
         torch = _torch()
         nq = Q.shape[0]
+        _shape(Q, (nq, self.d), "Q")
+        _shape(allow, (nq, self.words), "allow")
         ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
         scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
         check(lib.tq_search(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k,
@@ -344,6 +370,7 @@ class IdMapIndex(Index):
         ids = np.ascontiguousarray(ids, dtype=np.uint64)
         if ids.shape != (X.shape[0],):
             raise ValueError("ids must have shape (n,)")
+        self._check_rows(X.shape[0], X=X, tenants=tenants)
         check(lib.tq_index_add_ids(self._h, _dev_ptr(X, torch.float32, "X", 2),
                                    ids.ctypes.data_as(ctypes.c_void_p),
                                    _dev_ptr(tenants, torch.int16, "tenants") if tenants is not None else None,
@@ -354,6 +381,7 @@ class IdMapIndex(Index):
         ids = np.ascontiguousarray(ids, dtype=np.uint64)
         if ids.shape != (codes.shape[0],):
             raise ValueError("ids must have shape (n,)")
+        self._check_rows(codes.shape[0], codes=codes, scales=scales, tenants=tenants)
         check(lib.tq_index_add_codes_ids(self._h, _dev_ptr(codes, torch.uint8, "codes", 2),
                                          _dev_ptr(scales, torch.float32, "scales", 1),
                                          ids.ctypes.data_as(ctypes.c_void_p),
