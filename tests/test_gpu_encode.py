@@ -80,6 +80,27 @@ def test_codes_bit_exact(small, rot_pair, bits):
     assert ulps.max() <= 1, ulps.max()
 
 
+@pytest.mark.parametrize("d,bits", [(64, 4), (192, 2), (2048, 4), (2048, 8), (128, 3)])
+def test_codes_bit_exact_other_dimensions(d, bits):
+    """Rotation tiles of 128 output columns clipped (d = 64) or ragged
+    (d = 192), the largest d, and 3-bit packing at its smallest d."""
+    print("rotate_quantize d=%d bits=%d" % (d, bits), flush=True)
+    rng = np.random.default_rng(d * 10 + bits)
+    X = rng.standard_normal((1000, d)).astype(np.float32)
+    X[7] *= np.float32(1e-20)
+    rot = tq.Rotation(d, 5)
+    R32 = rot.matrix()
+    codes, scales = tq.rotate_quantize(tq.Codebook(d, bits), rot, torch.from_numpy(X).cuda())
+    ocb = oracle.lloyd_max(d, bits)
+    c_or, n_or, s_or, S = oracle.encode(X, R32, ocb, return_rotated=True)
+    c_gpu = oracle.unpack_codes(codes.cpu().numpy(), d, bits)
+    nm = classify_mismatch(c_gpu, c_or, S, n_or, ocb.bounds)
+    assert nm <= 1e-6 * c_or.size + 2
+    s = scales.cpu().numpy()
+    ulps = np.abs(s.view(np.int32).astype(np.int64) - s_or.view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1, ulps.max()
+
+
 def test_codes_special_rows(rot_pair):
     """Zero rows, tiny and huge norms, exact-zero coordinates, a ragged count."""
     rot, R32 = rot_pair

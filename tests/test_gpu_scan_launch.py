@@ -51,8 +51,14 @@ def test_top64_of_k64_and_k65_agree(env):
     assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
 
 
-# (d, b): code chunks per vector d*b/128, eight-chunk groups chunks/8
-@pytest.mark.parametrize("d,bits", [(256, 4), (1024, 4), (1280, 4), (512, 2), (1024, 1)])
+# (d, b): code chunks per vector d*b/128, eight-chunk groups chunks/8.  The
+# edges: the smallest d (64); chunk counts that are not a multiple of 8
+# (d = 192 at b = 4, d = 64 at b = 2 and 8); the largest d (2048), whose
+# 4-bit table no longer fits beside the split scan's other LDS regions; the
+# 3-bit layout at its smallest d (128).
+@pytest.mark.parametrize("d,bits", [(256, 4), (1024, 4), (1280, 4), (512, 2), (1024, 1),
+                                    (64, 4), (192, 4), (2048, 4), (2048, 8), (128, 3),
+                                    (64, 2), (64, 8), (2048, 1)])
 def test_other_dimensions(d, bits):
     print("scan d=%d b=%d" % (d, bits), flush=True)
     rng = np.random.default_rng(d + bits)
