@@ -190,6 +190,11 @@ def test_largest_dimension():
 def test_unsupported_shapes_rejected(env):
     with pytest.raises(tq.TQError, match="TQ_EUNSUPPORTED"):
         env.idx.search(env.Qd, 257, path="mfma")
+    many = tq.Index(env.cb, env.rot, n_tenants=4097)   # 65 allowlist words
+    many.add_codes(torch.from_numpy(oracle.pack_codes(env.codes[:100], 4)).cuda(),
+                   torch.from_numpy(env.scales[:100]).cuda())
+    with pytest.raises(tq.TQError, match="TQ_EUNSUPPORTED"):
+        many.search(env.Qd, 10, path="mfma")
     cb2 = tq.Codebook(D, 2)
     idx = tq.Index(cb2, env.rot, n_tenants=1)
     idx.add(env.Xd[:100].contiguous())

@@ -91,7 +91,7 @@ def test_add_codes_path_and_ragged_sizes(env):
 
 
 @pytest.mark.parametrize("T,mode", [(10, "selective"), (100, "selective"), (1000, "selective"),
-                                    (100, "broad")])
+                                    (100, "broad"), (65535, "broad")])
 def test_filtered_search(env, T, mode):
     print("filtered T=%d %s" % (T, mode), flush=True)
     n = env.X.shape[0]
