@@ -74,3 +74,39 @@ def test_calibration_lowers_distortion_on_shifted_data():
     i0, _ = oracle.search(c0, s0, cb.cents, R, Q, 10)
     i1, _ = oracle.search(c1, s1, cb.cents, R, Q, 10, calib=(mu32, kappa32))
     assert oracle.recall_at_k(i1, ex, 10) > oracle.recall_at_k(i0, ex, 10)
+
+
+def test_fit_hand_worked():
+    """Two unit rows under the identity rotation: per coordinate the mean is
+    (1/2, 1/2, 0, 0) and the population standard deviation (1/2, 1/2, 0, 0),
+    so kappa = sigma * sqrt(4) = (1, 1, 0, 0)."""
+    X = np.array([[2.0, 0, 0, 0], [0, 3.0, 0, 0]], dtype=np.float32)   # norms removed by the fit
+    mu, kappa = oracle.tqplus_fit(X, np.eye(4, dtype=np.float32))
+    assert np.allclose(mu, [0.5, 0.5, 0, 0], atol=1e-15)
+    assert np.allclose(kappa, [1, 1, 0, 0], atol=1e-15)
+
+
+def test_encode_hand_worked():
+    """d = 4, 1 bit (threshold 0, centroids -+4/(3 pi), the closed form of
+    E|X| for a coordinate of a uniform unit vector in R^4), identity
+    rotation, x = (3, 4, 0, 0): y = (0.6, 0.8, 0, 0).  With mu = (0.7, 0.5,
+    -0.1, 0.1) and kappa = (1, 2, 1, 0.5) the thresholds mu + kappa * 0 are
+    (0.7, 0.5, -0.1, 0.1): codes (0, 1, 1, 0), where plain TurboQuant gives
+    (1, 1, 1, 1).  Reconstruction mu + kappa c_code, scale 5 / ||yhat||, and
+    the score of q = e_0 is scale * yhat_0."""
+    cb = oracle.lloyd_max(4, 1)
+    R = np.eye(4, dtype=np.float32)
+    X = np.array([[3.0, 4.0, 0.0, 0.0]], dtype=np.float32)
+    mu = np.array([0.7, 0.5, -0.1, 0.1], dtype=np.float32)
+    kappa = np.array([1.0, 2.0, 1.0, 0.5], dtype=np.float32)
+    codes, norms, scales = oracle.encode_tqplus(X, R, cb, mu, kappa)
+    assert codes.tolist() == [[0, 1, 1, 0]]
+    assert oracle.encode(X, R, cb)[0].tolist() == [[1, 1, 1, 1]]
+    c = 4.0 / (3.0 * np.pi)
+    yhat = mu.astype(np.float64) + kappa.astype(np.float64) * np.array([-c, c, c, -c])
+    s = 5.0 / np.sqrt(np.sum(yhat ** 2))
+    assert norms[0] == 5.0
+    assert abs(scales[0] - s) <= 1e-6 * s
+    score = oracle.scores_for_ids(codes, scales, cb.cents, np.array([1.0, 0, 0, 0]), [0],
+                                  calib=(mu, kappa))
+    assert abs(score[0] - scales[0] * yhat[0]) <= 1e-12
