@@ -322,8 +322,8 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU only (the scan shards over N with one "
-              "top-k exchange per query; that multi-GPU path is not built); run with --gpus 1",
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the scan "
+              "would shard over N with one top-k exchange per query); run with --gpus 1",
               file=sys.stderr)
         return 2
 

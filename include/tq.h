@@ -42,7 +42,7 @@ typedef enum {
     TQ_EINVAL = -1,          /* bad argument (null pointer, bad size, bad id) */
     TQ_ENOMEM = -2,          /* device or host allocation failed */
     TQ_EDEVICE = -3,         /* no usable GPU, or a HIP runtime error */
-    TQ_EUNSUPPORTED = -4     /* valid request outside what this build supports */
+    TQ_EUNSUPPORTED = -4     /* valid request outside what the library supports */
 } tq_status;
 
 typedef struct tq_codebook tq_codebook;

@@ -1,6 +1,7 @@
 // Per-query lookup tables for 4-bit fields of the code stream (b in
-// {1, 2, 4}) and the integer scoring that uses them (device code, shared by
-// the single-query scan and the exact rescoring of the batched search).
+// {1, 2, 4}) and for 3-bit codes (b = 3), and the integer scoring that uses
+// them (device code, shared by the single-query scan and the exact
+// rescoring of the batched search).
 //
 // One row of 16 int32 entries per 4-bit field of the code stream (row r
 // covers coordinates r*g .. r*g+g-1, g = 4/b), holding round(2^sh * sum_t
@@ -150,6 +151,97 @@ __device__ inline int build_nibble_table(float *lds, const float *red, const flo
         }
     }
     return sh;
+}
+
+// ---------------------------------------------------------------- b = 3
+// Stored words hold ten 3-bit fields (bits 3t..3t+2: coordinate 10w + t of
+// the word's run; two pad bits), so a 16-byte chunk covers 40 coordinates.
+// The table has one row of 8 int32 entries (32 bytes) per coordinate,
+// round(2^sh c[code] q'_j), under the same fixed-point rule as the 4-bit
+// field tables; rows = chunks * 40 <= 3 * 1024 (d <= 2048), so thread t owns
+// rows t, t + 1024 and t + 2048, and rows of padding coordinates (j >= d)
+// are zero.  With TQ+ calibration row 0 also carries round(2^sh C).
+constexpr int kTriRowsPerThread = 3;
+
+__device__ inline void load_tribit_query(const TableShape &p, const float *__restrict__ q,
+                                         float (&qv)[kTriRowsPerThread]) {
+#pragma unroll
+    for (int m = 0; m < kTriRowsPerThread; ++m) {
+        const int j = threadIdx.x + m * kTableThreads;
+        qv[m] = j < p.d ? q[j] : 0.f;
+    }
+}
+
+__device__ inline void tribit_abs_sum(float *red, const float (&qv)[kTriRowsPerThread]) {
+    float part = 0.f;
+#pragma unroll
+    for (int m = 0; m < kTriRowsPerThread; ++m) part += fabsf(qv[m]);
+    part = wave_sum(part);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
+}
+
+// As build_nibble_table, for the 3-bit rows; the summed rounding error
+// stays below 2^-23 B + d/2 + 1 units.
+__device__ inline int build_tribit_table(float *lds, const float *red, const float *cents,
+                                         const TableShape &p, const float (&qv)[kTriRowsPerThread],
+                                         float C = 0.f) {
+    const int tid = threadIdx.x;
+    const int rows = p.lut_words >> 3;
+    float cl[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) cl[c] = cents[c];
+    double tot = 0.0;
+#pragma unroll
+    for (int w = 0; w < kTableWaves; ++w) tot += (double)red[w];
+    const double cmax = fmax(fabs((double)cl[0]), fabs((double)cl[7]));
+    const double B = (cmax * tot + fabs((double)C)) * (1.0 + 1e-5);
+    int sh = 0;
+    if (B > 0.0) {
+        sh = (int)floor(log2((2147483647.0 - 2.0 * p.d) / B));
+        sh = sh < 0 ? 0 : (sh > 100 ? 100 : sh);
+    }
+    const float scale = ldexpf(1.0f, sh);
+    const int c0 = (int)rintf(C * scale);
+    int *T = reinterpret_cast<int *>(lds);
+#pragma unroll
+    for (int m = 0; m < kTriRowsPerThread; ++m) {
+        const int r = tid + m * kTableThreads;
+        if (r < rows) {
+            const float q0 = qv[m] * scale;
+            int e[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) e[c] = (int)rintf(cl[c] * q0);
+            if (r == 0)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) e[c] += c0;
+            int4 *row = reinterpret_cast<int4 *>(T + r * 8);
+            row[0] = make_int4(e[0], e[1], e[2], e[3]);
+            row[1] = make_int4(e[4], e[5], e[6], e[7]);
+        }
+    }
+    return sh;
+}
+
+// Sum of the 10 table hits of one stored word; Lb is its 10 rows (320 bytes).
+// Each address is a bit-field extract and a shift-add onto Lb (the empty asm
+// keeps the compiler from re-forming them into a shift, a mask and an add).
+__device__ inline int tri10(const char *__restrict__ Lb, uint32_t w) {
+    int a = 0, b = 0;
+#pragma unroll
+    for (int t = 0; t < 10; t += 2) {
+        uint32_t f0 = __builtin_amdgcn_ubfe(w, 3 * t, 3);
+        uint32_t f1 = __builtin_amdgcn_ubfe(w, 3 * t + 3, 3);
+        asm volatile("" : "+v"(f0), "+v"(f1));
+        a += *reinterpret_cast<const int *>(Lb + t * 32 + (f0 << 2));
+        b += *reinterpret_cast<const int *>(Lb + (t + 1) * 32 + (f1 << 2));
+    }
+    return a + b;
+}
+
+// Sum of the 40 table hits of one 16-byte chunk; Lb is the chunk's 1280
+// bytes of table rows.
+__device__ inline int tri_chunk(const char *__restrict__ Lb, uint4 v) {
+    return (tri10(Lb, v.x) + tri10(Lb + 320, v.y)) + (tri10(Lb + 640, v.z) + tri10(Lb + 960, v.w));
 }
 
 }  // namespace tq

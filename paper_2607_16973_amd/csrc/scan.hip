@@ -78,19 +78,9 @@ __device__ inline TableShape table_shape(const ScanParams &p) {
 }
 
 // ---------------------------------------------------------------- tables
-// b in {1,2,4}: int32 fixed-point rows of 16 entries (lut.h).
-// b = 3: float32 rows of 8 entries c[code] q'_j per coordinate.
+// b in {1,2,4}: int32 fixed-point rows of 16 entries per 4-bit field (lut.h).
+// b = 3: int32 fixed-point rows of 8 entries per coordinate (lut.h).
 // b = 8: the 256 float32 centroids followed by q' (multiplied on the fly).
-
-__device__ inline float tri10(const float *__restrict__ L, uint32_t w) {
-    float a = 0.f, b = 0.f;
-#pragma unroll
-    for (int t = 0; t < 10; t += 2) {
-        a += L[t * 8 + ((w >> (3 * t)) & 7)];
-        b += L[(t + 1) * 8 + ((w >> (3 * t + 3)) & 7)];
-    }
-    return a + b;
-}
 
 __device__ inline float byte4(const float *__restrict__ cents, const float *__restrict__ q,
                               uint32_t w) {
@@ -101,48 +91,79 @@ __device__ inline float byte4(const float *__restrict__ cents, const float *__re
     return a + b;
 }
 
-template <int MODE> struct AccOf { typedef float type; };
-template <> struct AccOf<NIBBLE> { typedef int type; };
+// The integer-table modes: the query coordinates a thread loads ahead of
+// the build, and the bytes of table per 16-byte chunk of codes.
+template <int MODE> struct QueryRegs { float v[2][4]; };
+template <> struct QueryRegs<TRIBIT> { float v[kTriRowsPerThread]; };
+template <int MODE> constexpr int kChunkTableBytes = MODE == TRIBIT ? 1280 : 2048;
+
+template <int MODE>
+__device__ inline void load_query(const TableShape &t, const float *__restrict__ q,
+                                  QueryRegs<MODE> &r) {
+    if constexpr (MODE == TRIBIT)
+        load_tribit_query(t, q, r.v);
+    else
+        load_nibble_query(t, q, r.v);
+}
+
+template <int MODE>
+__device__ inline void query_abs_sum(float *red, const QueryRegs<MODE> &r) {
+    if constexpr (MODE == TRIBIT)
+        tribit_abs_sum(red, r.v);
+    else
+        nibble_abs_sum(red, r.v);
+}
+
+template <int MODE>
+__device__ inline int build_int_table(float *lds, const float *red, const float *cents,
+                                      const TableShape &t, const QueryRegs<MODE> &r, float C) {
+    if constexpr (MODE == TRIBIT)
+        return build_tribit_table(lds, red, cents, t, r.v, C);
+    else
+        return build_nibble_table(lds, red, cents, t, r.v, C);
+}
+
+template <int MODE>
+__device__ inline int int_chunk(const char *__restrict__ Lb, uint4 v) {
+    if constexpr (MODE == TRIBIT)
+        return tri_chunk(Lb, v);
+    else
+        return nib_chunk(Lb, v);
+}
+
+template <int MODE> struct AccOf { typedef int type; };
+template <> struct AccOf<BYTE> { typedef float type; };
 
 template <int MODE>
 __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__ lds, int c, uint4 v) {
-    if constexpr (MODE == NIBBLE) {
-        return nib_chunk(reinterpret_cast<const char *>(lds) + c * 2048, v);
-    } else if constexpr (MODE == TRIBIT) {
-        const float *L = lds + c * 40 * 8;
-        return (tri10(L, v.x) + tri10(L + 80, v.y)) + (tri10(L + 160, v.z) + tri10(L + 240, v.w));
-    } else {
+    if constexpr (MODE == BYTE) {
         const float *cents = lds;          // 256 centroids
         const float *q = lds + 256 + c * 16;
         return (byte4(cents, q, v.x) + byte4(cents, q + 4, v.y)) +
                (byte4(cents, q + 8, v.z) + byte4(cents, q + 12, v.w));
+    } else {
+        return int_chunk<MODE>(reinterpret_cast<const char *>(lds) + c * kChunkTableBytes<MODE>, v);
     }
 }
 
-// Builds the table for one query; returns the fixed-point exponent sh
-// (NIBBLE) or 0.  `red` is 16 floats of LDS scratch.  C is the query's
-// constant term: part of the NIBBLE table, the starting value of the float
-// sums otherwise.
+// Builds the table for one query; returns the fixed-point exponent sh of
+// the integer tables, or 0.  `red` is 16 floats of LDS scratch.  C is the
+// query's constant term: part of the integer tables, the starting value of
+// the float sums of b = 8.
 template <int MODE>
 __device__ int build_table(float *lds, float *red, const ScanParams &p, const float *__restrict__ q,
                            float C) {
     const int tid = threadIdx.x;
-    if constexpr (MODE == NIBBLE) {
-        float qv[2][4];
-        load_nibble_query(table_shape(p), q, qv);
-        nibble_abs_sum(red, qv);
-        __syncthreads();
-        return build_nibble_table(lds, red, p.cents, table_shape(p), qv, C);
-    } else if constexpr (MODE == TRIBIT) {
-        for (int e = tid; e < p.lut_words; e += SCAN_THREADS) {
-            const int j = e >> 3, c = e & 7;
-            lds[e] = (j < p.d) ? p.cents[c] * q[j] : 0.f;
-        }
-        return 0;
-    } else {
+    if constexpr (MODE == BYTE) {
         for (int e = tid; e < 256; e += SCAN_THREADS) lds[e] = p.cents[e];
         for (int e = tid; e < p.d; e += SCAN_THREADS) lds[256 + e] = q[e];
         return 0;
+    } else {
+        QueryRegs<MODE> qv;
+        load_query<MODE>(table_shape(p), q, qv);
+        query_abs_sum<MODE>(red, qv);
+        __syncthreads();
+        return build_int_table<MODE>(lds, red, p.cents, table_shape(p), qv, C);
     }
 }
 
@@ -360,7 +381,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                 const int ten = p.allow ? (int)p.tenants[vid] : 0;
                 const uint64_t bm = filtered ? block_mask(p, qi, b) : ~0ull;
                 acc_t acc = 0;
-                if constexpr (MODE != NIBBLE) acc = cq;
+                if constexpr (MODE == BYTE) acc = cq;
                 for (int c0 = 0; c0 < CH; c0 += PF) {
 #pragma unroll
                     for (int i = 0; i < PF; ++i) {
@@ -379,10 +400,10 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
                 bool ok = inside && ((bm >> lane) & 1ull);
                 if (ok && p.allow) ok = (allow_s[ten >> 6] >> (ten & 63)) & 1ull;
                 float sc;
-                if constexpr (MODE == NIBBLE)
-                    sc = ldexpf((float)acc * scl, -sh);
-                else
+                if constexpr (MODE == BYTE)
                     sc = acc * scl;
+                else
+                    sc = ldexpf((float)acc * scl, -sh);
                 if constexpr (ALL) {
                     if (inside) p.cand_s[(int64_t)qi * p.n + vid] = ok ? sc : -INFINITY;
                 } else {
@@ -403,7 +424,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void scan_kernel(ScanParams p) {
 // = 16 KiB of LDS.
 constexpr int kPassBlocks = 64;
 
-// Unfiltered scan for b in {1, 2, 4} with the work of a workgroup handed
+// Unfiltered scan for b in {1, 2, 3, 4} with the work of a workgroup handed
 // out in groups of 8 chunks (8 KiB of one block's codes) rather than whole
 // blocks.
 //  * Every query covers the same blocks of the workgroup, taken in passes of
@@ -422,7 +443,7 @@ constexpr int kPassBlocks = 64;
 //    top-k while the other waves stream on.
 //  * Per query there are three barriers: end of the scan, survivors
 //    collected, next table built (the survivors' sort overlaps the build).
-template <int S>
+template <int MODE, int S>
 __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
     // [0, aux): the table (and the tree-merge stage); then the fixed regions
@@ -472,11 +493,11 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         misc[2] = 0;
     }
     if (p.nq == 0) return;
-    float qv[2][4];
-    load_nibble_query(table_shape(p), p.qrot, qv);
-    nibble_abs_sum(red, qv);
+    QueryRegs<MODE> qv;
+    load_query<MODE>(table_shape(p), p.qrot, qv);
+    query_abs_sum<MODE>(red, qv);
     __syncthreads();
-    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
+    int sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
     __syncthreads();
 
     // this wave's current and next work items, and the ring holding the
@@ -525,12 +546,12 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
                 // the ticket after next is taken now and read after the
                 // group's lookups, which hide its LDS round trip
                 const int ticket = take(misc + 1);
-                const char *Lb = lut + c0 * 2048;
+                const char *Lb = lut + c0 * kChunkTableBytes<MODE>;
                 int acc = 0;
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
                     // consume buf[i], then refill it with the next group
-                    acc += nib_chunk(Lb + i * 2048, buf[i]);
+                    acc += int_chunk<MODE>(Lb + i * kChunkTableBytes<MODE>, buf[i]);
                     buf[i] = load_stream(nsrc + i * 64 + lane);
                     __builtin_amdgcn_sched_barrier(kKeepVmem);
                 }
@@ -562,8 +583,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         // sum while the others finish (red was last read by this table's build)
         const bool more = qi + 1 < p.nq;
         if (more) {
-            load_nibble_query(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
-            nibble_abs_sum(red, qv);
+            load_query<MODE>(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
+            query_abs_sum<MODE>(red, qv);
         }
         __syncthreads();   // scan done: every offer made, the bound key final
         const int64_t out = ((int64_t)qi * G + g) * p.k;
@@ -575,14 +596,14 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         } else {
             tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
-        if (more) sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
+        if (more) sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
         if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
         __syncthreads();   // table ready; survivor count read by every wave
         if (tid == 0) misc[2] = 0;
     }
 }
 
-// Filtered scan for b in {1, 2, 4}: as split_scan_kernel, over the blocks
+// Filtered scan for b in {1, 2, 3, 4}: as split_scan_kernel, over the blocks
 // whose tenant summary meets the query's allowlist only.  At the start of a
 // query the workgroup lists those of its blocks (by summary & allowlist, in
 // windows of kListMax blocks; no code byte of a skipped block is read), then
@@ -592,7 +613,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
 // fixed; the result does not depend on it.)
 constexpr int kListMax = 4096;
 
-template <int S>
+template <int MODE, int S>
 __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams p) {
     extern __shared__ __attribute__((aligned(16))) float lds[];
     const int aux = aux_words(p.lut_words, S);
@@ -637,11 +658,11 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
     if (p.nq == 0) return;
     if (p.allow)
         for (int w = tid; w < W; w += SCAN_THREADS) allow_s[w] = p.allow[w];
-    float qv[2][4];
-    load_nibble_query(table_shape(p), p.qrot, qv);
-    nibble_abs_sum(red, qv);
+    QueryRegs<MODE> qv;
+    load_query<MODE>(table_shape(p), p.qrot, qv);
+    query_abs_sum<MODE>(red, qv);
     __syncthreads();
-    int sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
+    int sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
     __syncthreads();
     for (int qi = 0; qi < p.nq; ++qi) {
         WaveTopK<S> top;
@@ -711,11 +732,11 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                         }
                         const uint4 *nsrc = nxt < ng ? group_src(nxt) : csrc;
                         const int ticket = take(ctr);
-                        const char *Lb = lut + c0 * 2048;
+                        const char *Lb = lut + c0 * kChunkTableBytes<MODE>;
                         int acc = 0;
 #pragma unroll
                         for (int i = 0; i < 8; ++i) {
-                            acc += nib_chunk(Lb + i * 2048, buf[i]);
+                            acc += int_chunk<MODE>(Lb + i * kChunkTableBytes<MODE>, buf[i]);
                             buf[i] = load_stream(nsrc + i * 64 + lane);
                             __builtin_amdgcn_sched_barrier(kKeepVmem);
                         }
@@ -750,8 +771,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
         }
         const bool more = qi + 1 < p.nq;
         if (more) {
-            load_nibble_query(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
-            nibble_abs_sum(red, qv);
+            load_query<MODE>(table_shape(p), p.qrot + (int64_t)(qi + 1) * p.d, qv);
+            query_abs_sum<MODE>(red, qv);
         }
         __syncthreads();   // scan done: every offer made, the bound key final
         const int64_t out = ((int64_t)qi * G + g) * p.k;
@@ -764,7 +785,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
             tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
         if (more) {
-            sh = build_nibble_table(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
+            sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
             if (p.allow)
                 for (int w = tid; w < W; w += SCAN_THREADS)
                     allow_s[w] = p.allow[(int64_t)(qi + 1) * W + w];
@@ -1005,10 +1026,10 @@ int lut_words_for(const ScanShape &s) {
     return s.chunks * 32 * 16;
 }
 
-// The split scans serve searches over 1-, 2- and 4-bit codes whose chunk
-// count is a multiple of their 8-chunk groups, unfiltered or filtered.
+// The split scans serve searches over 1-, 2-, 3- and 4-bit codes whose
+// chunk count is a multiple of their 8-chunk groups, unfiltered or filtered.
 bool use_split(const ScanShape &s) {
-    return (s.bits == 1 || s.bits == 2 || s.bits == 4) && s.chunks % 8 == 0;
+    return s.bits != 8 && s.chunks % 8 == 0;
 }
 
 size_t lds_bytes_for(const ScanShape &s, int S, bool split, bool filtered) {
@@ -1066,29 +1087,34 @@ hipError_t launch_scan_all(const ScanParams &p, int grid, size_t lds, hipStream_
     return launch_scan<MODE, 1, 1, true>(p, grid, lds, stream);
 }
 
-template <int S>
+template <int MODE, int S>
 hipError_t launch_split(const ScanParams &p, int grid, size_t lds, hipStream_t stream) {
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)split_scan_kernel<S>,
+        hipError_t e = hipFuncSetAttribute((const void *)split_scan_kernel<MODE, S>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)split_filtered_kernel<S>,
+            e = hipFuncSetAttribute((const void *)split_filtered_kernel<MODE, S>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     if (p.allow || p.live || p.slot_allow)
-        hipLaunchKernelGGL(split_filtered_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+        hipLaunchKernelGGL((split_filtered_kernel<MODE, S>), dim3(grid), dim3(SCAN_THREADS), lds,
+                           stream, p);
     else
-        hipLaunchKernelGGL(split_scan_kernel<S>, dim3(grid), dim3(SCAN_THREADS), lds, stream, p);
+        hipLaunchKernelGGL((split_scan_kernel<MODE, S>), dim3(grid), dim3(SCAN_THREADS), lds, stream,
+                           p);
     return hipGetLastError();
 }
 
 template <int S>
 hipError_t launch_scan_mode(const ScanParams &p, int grid, size_t lds, bool split,
                             hipStream_t stream) {
-    if (split) return launch_split<S>(p, grid, lds, stream);
+    if (split) {
+        if (p.bits == 3) return launch_split<TRIBIT, S>(p, grid, lds, stream);
+        return launch_split<NIBBLE, S>(p, grid, lds, stream);
+    }
     if (p.bits == 8) return launch_scan_pf<BYTE, S>(p, grid, lds, stream);
     if (p.bits == 3) return launch_scan_pf<TRIBIT, S>(p, grid, lds, stream);
     return launch_scan_pf<NIBBLE, S>(p, grid, lds, stream);

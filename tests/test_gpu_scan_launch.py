@@ -1,8 +1,9 @@
 """GPU parity of the single-query scan (section II-B step 5, section III-B)
 across launch shapes: many queries in one launch (the scan keeps per-query
 state across its query loop), results that must not depend on the other
-queries of a launch, four dimensions and three bit widths with 1 to 6
-eight-chunk groups per vector, and exact agreement between the top-64 lists
+queries of a launch, dimensions from 64 to 2048 at every bit width, with 1
+to 6 eight-chunk groups per vector or chunk counts outside that scheme,
+unfiltered and tenant-filtered, and exact agreement between the top-64 lists
 of k = 64 and k = 65 (wave lists of one and of two 64-entry slots; both sum
 the same integer table entries)."""
 import numpy as np
@@ -54,11 +55,14 @@ def test_top64_of_k64_and_k65_agree(env):
 # (d, b): code chunks per vector d*b/128, eight-chunk groups chunks/8.  The
 # edges: the smallest d (64); chunk counts that are not a multiple of 8
 # (d = 192 at b = 4, d = 64 at b = 2 and 8); the largest d (2048), whose
-# 4-bit table no longer fits beside the split scan's other LDS regions; the
-# 3-bit layout at its smallest d (128).
+# 4-bit table no longer fits beside the split scan's other LDS regions.
+# 3-bit codes (ten per word, chunks rounded up to a multiple of 4): d = 128
+# (4 chunks) and 2048 (52 chunks, 2080 table rows) take the block-per-wave
+# scan, d = 256 (8 chunks) and 1792 (48) the split scans.
 @pytest.mark.parametrize("d,bits", [(256, 4), (1024, 4), (1280, 4), (512, 2), (1024, 1),
                                     (64, 4), (192, 4), (2048, 4), (2048, 8), (128, 3),
-                                    (64, 2), (64, 8), (2048, 1)])
+                                    (64, 2), (64, 8), (2048, 1), (256, 3), (1792, 3),
+                                    (2048, 3)])
 def test_other_dimensions(d, bits):
     print("scan d=%d b=%d" % (d, bits), flush=True)
     rng = np.random.default_rng(d + bits)
@@ -71,9 +75,11 @@ def test_other_dimensions(d, bits):
     R32 = rot.matrix()
     ocb = oracle.lloyd_max(d, bits)
     codes, _, scales = oracle.encode(X, R32, ocb)
-    idx = tq.Index(tq.Codebook(d, bits), rot, n_tenants=1)
+    tenants = rng.integers(0, 5, n).astype(np.uint16)
+    idx = tq.Index(tq.Codebook(d, bits), rot, n_tenants=5)
     idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
-                  torch.from_numpy(scales).cuda())
+                  torch.from_numpy(scales).cuda(),
+                  torch.from_numpy(tenants.view(np.int16)).cuda())
     Qd = torch.from_numpy(Q).cuda()
     qrot = oracle.rotate_queries(R32, Q)
     qn = np.linalg.norm(Q.astype(np.float64), axis=1)
@@ -85,3 +91,11 @@ def test_other_dimensions(d, bits):
     a_i, a_s = idx.search(Qd, 64)
     b_i, b_s = idx.search(Qd, 65)
     assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
+    # one tenant of five per query
+    bm = np.zeros((nq, 1), dtype=np.uint64)
+    bm[:, 0] = np.left_shift(np.uint64(1), (np.arange(nq) % 5).astype(np.uint64))
+    ids, sc = idx.search(Qd, 10, allow=torch.from_numpy(bm.view(np.int64)).cuda())
+    ref_i, ref_s = oracle.search(codes, scales, ocb.cents, R32, Q, 10, tenants, bm)
+    masks = [oracle.allowed_mask(tenants, bm[b]) for b in range(nq)]
+    check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, qrot, qn, 10,
+               ref_i, ref_s, allowed=masks)
