@@ -80,14 +80,29 @@ __device__ inline TableShape table_shape(const ScanParams &p) {
 // ---------------------------------------------------------------- tables
 // b in {1,2,4}: int32 fixed-point rows of 16 entries per 4-bit field (lut.h).
 // b = 3: int32 fixed-point rows of 8 entries per coordinate (lut.h).
-// b = 8: the 256 float32 centroids followed by q' (multiplied on the fly).
+// b = 8: the 256 float32 centroids, each repeated 32 times, followed by q'
+// (multiplied on the fly).  Centroid e of lane l is at byte 128 e + 4 (l % 32):
+// the 32 lanes of a half-wave always read 32 different banks, whatever
+// their codes.
 
-__device__ inline float byte4(const float *__restrict__ cents, const float *__restrict__ q,
-                              uint32_t w) {
-    float a = cents[w & 255] * q[0];
-    float b = cents[(w >> 8) & 255] * q[1];
-    a = fmaf(cents[(w >> 16) & 255], q[2], a);
-    b = fmaf(cents[w >> 24], q[3], b);
+constexpr int kByteRepWords = 256 * 32;
+
+// Sum over the four codes of word w of c[code] q'_j; rep is the repeated
+// centroids, lo = 4 (lane % 32).  Each address is a bit-field extract and a
+// shift-add (the empty asm keeps the compiler from re-forming them).
+__device__ inline float byte4(const char *__restrict__ rep, const float *__restrict__ q,
+                              uint32_t w, uint32_t lo) {
+    uint32_t e0 = __builtin_amdgcn_ubfe(w, 0, 8), e1 = __builtin_amdgcn_ubfe(w, 8, 8);
+    uint32_t e2 = __builtin_amdgcn_ubfe(w, 16, 8), e3 = w >> 24;
+    asm volatile("" : "+v"(e0), "+v"(e1), "+v"(e2), "+v"(e3));
+    const float c0 = *reinterpret_cast<const float *>(rep + (e0 << 7) + lo);
+    const float c1 = *reinterpret_cast<const float *>(rep + (e1 << 7) + lo);
+    const float c2 = *reinterpret_cast<const float *>(rep + (e2 << 7) + lo);
+    const float c3 = *reinterpret_cast<const float *>(rep + (e3 << 7) + lo);
+    float a = c0 * q[0];
+    float b = c1 * q[1];
+    a = fmaf(c2, q[2], a);
+    b = fmaf(c3, q[3], b);
     return a + b;
 }
 
@@ -137,10 +152,11 @@ template <> struct AccOf<BYTE> { typedef float type; };
 template <int MODE>
 __device__ inline typename AccOf<MODE>::type chunk_sum(const float *__restrict__ lds, int c, uint4 v) {
     if constexpr (MODE == BYTE) {
-        const float *cents = lds;          // 256 centroids
-        const float *q = lds + 256 + c * 16;
-        return (byte4(cents, q, v.x) + byte4(cents, q + 4, v.y)) +
-               (byte4(cents, q + 8, v.z) + byte4(cents, q + 12, v.w));
+        const char *rep = reinterpret_cast<const char *>(lds);
+        const float *q = lds + kByteRepWords + c * 16;
+        const uint32_t lo = (threadIdx.x & 31u) << 2;
+        return (byte4(rep, q, v.x, lo) + byte4(rep, q + 4, v.y, lo)) +
+               (byte4(rep, q + 8, v.z, lo) + byte4(rep, q + 12, v.w, lo));
     } else {
         return int_chunk<MODE>(reinterpret_cast<const char *>(lds) + c * kChunkTableBytes<MODE>, v);
     }
@@ -155,8 +171,8 @@ __device__ int build_table(float *lds, float *red, const ScanParams &p, const fl
                            float C) {
     const int tid = threadIdx.x;
     if constexpr (MODE == BYTE) {
-        for (int e = tid; e < 256; e += SCAN_THREADS) lds[e] = p.cents[e];
-        for (int e = tid; e < p.d; e += SCAN_THREADS) lds[256 + e] = q[e];
+        for (int e = tid; e < kByteRepWords; e += SCAN_THREADS) lds[e] = p.cents[e >> 5];
+        for (int e = tid; e < p.d; e += SCAN_THREADS) lds[kByteRepWords + e] = q[e];
         return 0;
     } else {
         QueryRegs<MODE> qv;
@@ -1021,7 +1037,7 @@ __global__ __launch_bounds__(64) void postfilter_kernel(const int64_t *__restric
 }
 
 int lut_words_for(const ScanShape &s) {
-    if (s.bits == 8) return 256 + s.d;
+    if (s.bits == 8) return kByteRepWords + s.d;
     if (s.bits == 3) return s.chunks * 40 * 8;
     return s.chunks * 32 * 16;
 }
