@@ -80,6 +80,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_STRIDE];
     __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
     __shared__ double norm_s[BM];
+    __shared__ double bnd_s[255];   // the shared thresholds t_i (no TQ+ tables)
 
     const int ncol = (d + BN - 1) / BN;
     int rt, ct;
@@ -140,6 +141,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     bool finite = true;
 
     const int nslab = d / KB;
+    if (QUANT && !qa.athr)
+        for (int i = tid; i < qa.levels - 1; i += GEMM_THREADS) bnd_s[i] = qa.bounds[i];
     load_slab(0);
     store_slab(0);
     __syncthreads();
@@ -206,6 +209,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
         }
         __syncthreads();
         const int L = qa.levels;
+        // bit 8 ti + 2 v + tj: that coordinate is flagged
+        uint32_t fmask = 0;
 #pragma unroll
         for (int ti = 0; ti < 4; ++ti)
 #pragma unroll
@@ -227,7 +232,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                     } else {
                         // threshold i of this coordinate, before scaling by n
                         auto thr = [&](int i) {
-                            return qa.athr ? qa.athr[(int64_t)i * d + col] : qa.bounds[i];
+                            return qa.athr ? qa.athr[(int64_t)i * d + col] : bnd_s[i];
                         };
                         int c = 0;
                         for (int step = L / 2; step >= 1; step >>= 1) {
@@ -245,12 +250,33 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                         }
                     }
                     qa.codes_tmp[gr * d + col] = (uint8_t)code;
-                    if (flag) {
-                        const unsigned int slot = atomicAdd(qa.flag_count, 1u);
-                        qa.flags[slot] = ((uint32_t)gr << 11) | (uint32_t)col;
-                    }
+                    if (flag) fmask |= 1u << (ti * 8 + v * 2 + tj);
                 }
             }
+        // one slot reservation per wave: lanes take consecutive ranges in
+        // lane order (inclusive prefix sum of the per-lane counts)
+        const int cnt = __popc(fmask);
+        int incl = cnt;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int t = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += t;
+        }
+        const int total = __shfl(incl, 63, 64);
+        if (total > 0) {
+            unsigned int base = 0;
+            if (lane == 63) base = atomicAdd(qa.flag_count, (unsigned int)total);
+            base = __shfl(base, 63, 64);
+            unsigned int slot = base + (unsigned int)(incl - cnt);
+            while (fmask) {
+                const int b = __ffs(fmask) - 1;
+                fmask &= fmask - 1;
+                const int ti = b >> 3, v = (b >> 1) & 3, tj = b & 1;
+                const int64_t gr = row0 + wr * 64 + ti * 16 + g4 * 4 + v;
+                const int col = col0 + wc * 32 + tj * 16 + l16;
+                qa.flags[slot++] = ((uint32_t)gr << 11) | (uint32_t)col;
+            }
+        }
     } else {
 #pragma unroll
         for (int ti = 0; ti < 4; ++ti)
