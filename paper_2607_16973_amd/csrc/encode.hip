@@ -18,7 +18,10 @@
 //     With ||R_j|| <= 1 + 1e-6 this gives tau = 4.0e-6 * n + 1e-30.
 //  2. fixup: every flagged coordinate is recomputed as the sequential float64
 //     sum sum_{k=0}^{d-1} R[j][k] x_k (every product of two float32 values is
-//     exact in float64) and re-coded.
+//     exact in float64) and re-coded.  Flags are kept per output tile; with
+//     few flags per tile (b <= 4) one thread per flag reads its rows from
+//     memory, with many (b = 8, about 2% of coordinates) each tile stages
+//     its X and R slabs in LDS once for all of its flags.
 //  3. pack: per row, scale = n / sqrt(sum_j fl64(c_code_j^2)) (sequential
 //     float64 over j) and the codes are written in the canonical bitstream
 //     and/or the index's blocked layout.
@@ -54,8 +57,8 @@ struct QuantArgs {
     int levels;
     uint8_t *codes_tmp;     // [rows][d] unpacked codes of this chunk
     double *norms;          // [rows] exact row norms (written by column tile 0)
-    uint32_t *flags;        // flagged (row << 11 | j)
-    unsigned int *flag_count;
+    uint32_t *flags;        // per output tile, BM * BN slots: flagged (local row << 7 | local col)
+    unsigned int *tile_count;   // flags of each output tile
     int *status;            // set non-zero on a non-finite input
 };
 
@@ -81,6 +84,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
     __shared__ double norm_s[BM];
     __shared__ double bnd_s[255];   // the shared thresholds t_i (no TQ+ tables)
+    __shared__ unsigned int nflag_s;
 
     const int ncol = (d + BN - 1) / BN;
     int rt, ct;
@@ -143,6 +147,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     const int nslab = d / KB;
     if (QUANT && !qa.athr)
         for (int i = tid; i < qa.levels - 1; i += GEMM_THREADS) bnd_s[i] = qa.bounds[i];
+    if (QUANT && tid == 0) nflag_s = 0;
     load_slab(0);
     store_slab(0);
     __syncthreads();
@@ -209,8 +214,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
         }
         __syncthreads();
         const int L = qa.levels;
-        // bit 8 ti + 2 v + tj: that coordinate is flagged
-        uint32_t fmask = 0;
+        const int64_t tile = (int64_t)rt * ncol + ct;
+        uint32_t *tflags = qa.flags + tile * (BM * BN);
 #pragma unroll
         for (int ti = 0; ti < 4; ++ti)
 #pragma unroll
@@ -250,33 +255,15 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                         }
                     }
                     qa.codes_tmp[gr * d + col] = (uint8_t)code;
-                    if (flag) fmask |= 1u << (ti * 8 + v * 2 + tj);
+                    if (flag) {
+                        // a slot of this tile's list (an LDS counter)
+                        const unsigned int slot = atomicAdd(&nflag_s, 1u);
+                        tflags[slot] = ((uint32_t)lr << 7) | (uint32_t)(col - col0);
+                    }
                 }
             }
-        // one slot reservation per wave: lanes take consecutive ranges in
-        // lane order (inclusive prefix sum of the per-lane counts)
-        const int cnt = __popc(fmask);
-        int incl = cnt;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int t = __shfl_up(incl, off, 64);
-            if (lane >= off) incl += t;
-        }
-        const int total = __shfl(incl, 63, 64);
-        if (total > 0) {
-            unsigned int base = 0;
-            if (lane == 63) base = atomicAdd(qa.flag_count, (unsigned int)total);
-            base = __shfl(base, 63, 64);
-            unsigned int slot = base + (unsigned int)(incl - cnt);
-            while (fmask) {
-                const int b = __ffs(fmask) - 1;
-                fmask &= fmask - 1;
-                const int ti = b >> 3, v = (b >> 1) & 3, tj = b & 1;
-                const int64_t gr = row0 + wr * 64 + ti * 16 + g4 * 4 + v;
-                const int col = col0 + wc * 32 + tj * 16 + l16;
-                qa.flags[slot++] = ((uint32_t)gr << 11) | (uint32_t)col;
-            }
-        }
+        __syncthreads();
+        if (tid == 0) qa.tile_count[tile] = nflag_s;
     } else {
 #pragma unroll
         for (int ti = 0; ti < 4; ++ti)
@@ -294,21 +281,36 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     }
 }
 
-// Exact recomputation of flagged coordinates: the sequential float64 sum of
-// the definition (products of float32 values are exact in float64, so fused
-// and unfused multiply-adds agree).
+// The code of coordinate j of a row with norm nrm whose exact sum is S.
+__device__ inline int exact_code(double S, double nrm, int j, int d, const double *bounds,
+                                 const double *athr, int levels) {
+    int c = 0;
+    for (int t = 0; t < levels - 1; ++t) {
+        const double th = (athr ? athr[(int64_t)t * d + j] : bounds[t]) * nrm;
+        c += (th <= S) ? 1 : 0;
+    }
+    return c;
+}
+
+// Exact recomputation of flagged coordinates, one thread per flag (one
+// workgroup per output tile): the sequential float64 sum of the definition
+// (products of float32 values are exact in float64, so fused and unfused
+// multiply-adds agree).
 __global__ __launch_bounds__(256) void fixup_kernel(
-    const float *__restrict__ X, const float *__restrict__ R, int d,
+    const float *__restrict__ X, const float *__restrict__ R, int d, int ncol,
     const double *__restrict__ bounds, const double *__restrict__ athr, int levels,
     const double *__restrict__ norms,
-    const uint32_t *__restrict__ flags, const unsigned int *__restrict__ flag_count,
+    const uint32_t *__restrict__ flags, const unsigned int *__restrict__ tile_count,
     uint8_t *__restrict__ codes_tmp) {
-    const unsigned int cnt = *flag_count;
-    for (unsigned int e = blockIdx.x * blockDim.x + threadIdx.x; e < cnt;
-         e += gridDim.x * blockDim.x) {
-        const uint32_t f = flags[e];
-        const int64_t row = f >> 11;
-        const int j = f & 2047;
+    const int tile = blockIdx.x;
+    const int64_t row0 = (int64_t)(tile / ncol) * BM;
+    const int col0 = (tile % ncol) * BN;
+    const unsigned int cnt = tile_count[tile];
+    const uint32_t *tflags = flags + (int64_t)tile * (BM * BN);
+    for (unsigned int e = threadIdx.x; e < cnt; e += blockDim.x) {
+        const uint32_t f = tflags[e];
+        const int64_t row = row0 + (f >> 7);
+        const int j = col0 + (int)(f & 127);
         const f4 *xr = reinterpret_cast<const f4 *>(X + row * d);
         const f4 *rr = reinterpret_cast<const f4 *>(R + (int64_t)j * d);
         double S = 0.0;
@@ -321,13 +323,71 @@ __global__ __launch_bounds__(256) void fixup_kernel(
                 S = S + prod;
             }
         }
-        const double nrm = norms[row];
-        int c = 0;
-        for (int t = 0; t < levels - 1; ++t) {
-            const double th = (athr ? athr[(int64_t)t * d + j] : bounds[t]) * nrm;
-            c += (th <= S) ? 1 : 0;
+        codes_tmp[row * d + j] = (uint8_t)exact_code(S, norms[row], j, d, bounds, athr, levels);
+    }
+}
+
+// The same recomputation for tiles with many flags: the tile's X rows and R
+// rows pass through LDS in slabs of KB (once per 512 flags), and each
+// thread adds its flag's products in k order from there.
+__global__ __launch_bounds__(GEMM_THREADS) void fixup_tile_kernel(
+    const float *__restrict__ X, int64_t m, const float *__restrict__ R, int d, int ncol,
+    const double *__restrict__ bounds, const double *__restrict__ athr, int levels,
+    const double *__restrict__ norms,
+    const uint32_t *__restrict__ flags, const unsigned int *__restrict__ tile_count,
+    uint8_t *__restrict__ codes_tmp) {
+    __shared__ __attribute__((aligned(16))) float As[BM * LDS_STRIDE];
+    __shared__ __attribute__((aligned(16))) float Bs[BN * LDS_STRIDE];
+    const int tile = blockIdx.x;
+    const int64_t row0 = (int64_t)(tile / ncol) * BM;
+    const int col0 = (tile % ncol) * BN;
+    const unsigned int cnt = tile_count[tile];
+    if (cnt == 0) return;
+    const uint32_t *tflags = flags + (int64_t)tile * (BM * BN);
+    const int tid = threadIdx.x;
+    for (unsigned int e0 = 0; e0 < cnt; e0 += GEMM_THREADS) {
+        const unsigned int e = e0 + tid;
+        const bool active = e < cnt;
+        const uint32_t f = active ? tflags[e] : 0u;
+        const int lr = (int)(f >> 7), lc = (int)(f & 127);
+        double S = 0.0;
+        for (int k0 = 0; k0 < d; k0 += KB) {
+            __syncthreads();   // the previous slab has been read
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int q = tid + r * GEMM_THREADS;
+                const int row = q >> 3;
+                const int kq = (q & 7) * 4;
+                const int64_t gr = row0 + row;
+                const f4 a = gr < m ? *reinterpret_cast<const f4 *>(X + gr * d + k0 + kq)
+                                    : f4{0.f, 0.f, 0.f, 0.f};
+                const f4 b = col0 + row < d
+                                 ? *reinterpret_cast<const f4 *>(R + (int64_t)(col0 + row) * d + k0 + kq)
+                                 : f4{0.f, 0.f, 0.f, 0.f};
+                *reinterpret_cast<f4 *>(&As[row * LDS_STRIDE + kq]) = a;
+                *reinterpret_cast<f4 *>(&Bs[row * LDS_STRIDE + kq]) = b;
+            }
+            __syncthreads();
+            if (active) {
+                const float *xa = &As[lr * LDS_STRIDE];
+                const float *rb = &Bs[lc * LDS_STRIDE];
+#pragma unroll
+                for (int q = 0; q < KB; q += 4) {
+                    const f4 a = *reinterpret_cast<const f4 *>(rb + q);
+                    const f4 b = *reinterpret_cast<const f4 *>(xa + q);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const double prod = (double)a[c] * (double)b[c];
+                        S = S + prod;
+                    }
+                }
+            }
         }
-        codes_tmp[row * d + j] = (uint8_t)c;
+        if (active) {
+            const int64_t row = row0 + lr;
+            const int j = col0 + lc;
+            codes_tmp[row * d + j] = (uint8_t)exact_code(S, norms[row], j, d, bounds, athr, levels);
+        }
     }
 }
 
@@ -418,6 +478,11 @@ __global__ __launch_bounds__(256) void pack_kernel(
 
 }  // namespace
 
+// Output tiles of one chunk of rows.
+size_t encode_tiles(int d) {
+    return (size_t)(kEncodeChunkRows / BM) * (size_t)((d + BN - 1) / BN);
+}
+
 size_t encode_workspace_bytes(int d) {
     const size_t rows = kEncodeChunkRows;
     size_t b = 0;
@@ -425,9 +490,10 @@ size_t encode_workspace_bytes(int d) {
     b = (b + 255) & ~(size_t)255;
     b += rows * sizeof(double);               // norms
     b = (b + 255) & ~(size_t)255;
-    b += rows * (size_t)d * sizeof(uint32_t); // flags (worst case: every coordinate)
+    b += encode_tiles(d) * BM * BN * sizeof(uint32_t);   // flags (worst case: every coordinate)
     b = (b + 255) & ~(size_t)255;
-    b += 256;                                 // flag counter
+    b += encode_tiles(d) * sizeof(unsigned int);          // flags per tile
+    b = (b + 255) & ~(size_t)255;
     b += 255 * sizeof(double) + 256 * sizeof(double);   // bounds, cent_sq
     b = (b + 255) & ~(size_t)255;
     return b;
@@ -443,9 +509,9 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
     double *norms = reinterpret_cast<double *>(p);
     p += (rows * sizeof(double) + 255) & ~(size_t)255;
     uint32_t *flags = reinterpret_cast<uint32_t *>(p);
-    p += (rows * (size_t)d * sizeof(uint32_t) + 255) & ~(size_t)255;
-    unsigned int *flag_count = reinterpret_cast<unsigned int *>(p);
-    p += 256;
+    p += (encode_tiles(d) * BM * BN * sizeof(uint32_t) + 255) & ~(size_t)255;
+    unsigned int *tile_count = reinterpret_cast<unsigned int *>(p);
+    p += (encode_tiles(d) * sizeof(unsigned int) + 255) & ~(size_t)255;
     double *bounds = reinterpret_cast<double *>(p);
     double *cent_sq = bounds + 255;
 
@@ -460,18 +526,25 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
     const int ncol = (d + BN - 1) / BN;
     for (int64_t r0 = 0; r0 < n; r0 += rows) {
         const int64_t m = (n - r0) < (int64_t)rows ? (n - r0) : (int64_t)rows;
-        e = hipMemsetAsync(flag_count, 0, sizeof(unsigned int), stream);
-        if (e != hipSuccess) return e;
         const int nrt = (int)((m + BM - 1) / BM);
         const int groups = (nrt + 7) / 8;
-        QuantArgs qa{bounds, calib.athr, cb.levels, codes_tmp, norms, flags, flag_count, status_dev};
+        // every output tile of the chunk writes its flag count
+        QuantArgs qa{bounds, calib.athr, cb.levels, codes_tmp, norms, flags, tile_count, status_dev};
         F32Args fa{nullptr};
         hipLaunchKernelGGL((rot_gemm<true>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
                            stream, X + r0 * d, m, R, d, nrt, qa, fa);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(fixup_kernel, dim3(1024), dim3(256), 0, stream, X + r0 * d, R, d,
-                           bounds, calib.athr, cb.levels, norms, flags, flag_count, codes_tmp);
+        // 8-bit codes flag about 2% of coordinates (thresholds ~4e-4 apart
+        // at d = 1536): tiles then share their staged rows
+        if (cb.levels > 16)
+            hipLaunchKernelGGL(fixup_tile_kernel, dim3(nrt * ncol), dim3(GEMM_THREADS), 0, stream,
+                               X + r0 * d, m, R, d, ncol, bounds, calib.athr, cb.levels, norms,
+                               flags, tile_count, codes_tmp);
+        else
+            hipLaunchKernelGGL(fixup_kernel, dim3(nrt * ncol), dim3(256), 0, stream, X + r0 * d, R,
+                               d, ncol, bounds, calib.athr, cb.levels, norms, flags, tile_count,
+                               codes_tmp);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);

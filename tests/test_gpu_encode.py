@@ -144,3 +144,49 @@ def test_gemm_error_is_far_inside_the_proven_band(small, rot_pair):
     rel = np.abs(Y - ref).max(axis=1) / np.linalg.norm(X[:512].astype(np.float64), axis=1)
     print("max |y - S| / ||x|| = %.3e" % rel.max())
     assert rel.max() < 4e-7
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_codes_of_rows_built_on_thresholds(rot_pair, bits):
+    """Rows whose rotated coordinates sit on thresholds to float32 rounding:
+    90% of the coordinates of a random unit vector are moved to their nearest
+    threshold and the others rescaled to keep the norm at one.  Nearly every
+    coordinate then falls inside the proven band, each 128 x 128 output tile
+    carries about 15,000 flags (about 29 rounds of the 8-bit tile
+    recomputation), and the codes are decided by the exact sums."""
+    rot, R32 = rot_pair
+    print("rotate_quantize on thresholds bits=%d" % bits, flush=True)
+    ocb = oracle.lloyd_max(D, bits)
+    t = np.asarray(ocb.bounds, dtype=np.float64)
+    rng = np.random.default_rng(17 + bits)
+    n = 300
+    Y = rng.standard_normal((n, D))
+    Y /= np.linalg.norm(Y, axis=1, keepdims=True)
+    snap = rng.random((n, D)) < 0.9
+    pos = np.clip(np.searchsorted(t, Y), 1, len(t) - 1)
+    lo, hi = t[pos - 1], t[pos]
+    nearest = np.where(np.abs(Y - lo) <= np.abs(Y - hi), lo, hi)
+    Y = np.where(snap, nearest, Y)
+    on = np.where(snap, Y, 0.0)
+    free = np.where(snap, 0.0, Y)
+    rest = 1.0 - (on * on).sum(axis=1)
+    assert np.all(rest > 0)
+    Y = on + free * np.sqrt(rest / (free * free).sum(axis=1))[:, None]
+    nrm = rng.uniform(0.5, 2.0, n)
+    X = np.ascontiguousarray(((Y * nrm[:, None]) @ R32.astype(np.float64)).astype(np.float32))
+    cb = tq.Codebook(D, bits)
+    codes, scales = tq.rotate_quantize(cb, rot, torch.from_numpy(X).cuda())
+    c_or, n_or, s_or, S = oracle.encode(X, R32, ocb, return_rotated=True)
+    u = S / n_or[:, None]
+    p2 = np.clip(np.searchsorted(t, u), 1, len(t) - 1)
+    gap = np.minimum(np.abs(u - t[p2 - 1]), np.abs(u - t[p2]))
+    print("coordinates inside the band: %.3f" % (gap <= 4e-6).mean(), flush=True)
+    assert (gap <= 4e-6).mean() > 0.85
+    c_gpu = oracle.unpack_codes(codes.cpu().numpy(), D, bits)
+    nm = classify_mismatch(c_gpu, c_or, S, n_or, ocb.bounds)
+    print("bits=%d code mismatches explained by input rounding: %d of %d" % (bits, nm, c_or.size))
+    assert nm <= 1e-4 * c_or.size
+    same = np.all(c_gpu == c_or, axis=1)
+    s = scales.cpu().numpy()[same]
+    ulps = np.abs(s.view(np.int32).astype(np.int64) - s_or[same].view(np.int32).astype(np.int64))
+    assert ulps.max() <= 1
