@@ -419,7 +419,8 @@ def main() -> int:
         g = torch.empty((nr, n), dtype=torch.float32, device=dev)
         for s0 in range(0, n, 250_000):
             g[:, s0:s0 + 250_000] = Q[:nr] @ X[s0:s0 + 250_000].T
-        ex_ids = torch.topk(g, k, dim=1).indices.cpu().numpy()
+        ex_all = torch.topk(g, max(k, 100), dim=1).indices.cpu().numpy()
+        ex_ids = ex_all[:, :k]
         got = ids[:nr].cpu().numpy()
         rec = float(np.mean([len(set(a) & set(b)) / k for a, b in zip(got, ex_ids)]))
         extra["recall_at_k_vs_exact_fp32"] = rec
@@ -433,6 +434,17 @@ def main() -> int:
         hit["mrr_at_20"] = float(np.mean(np.where(ranks > 0, 1.0 / np.maximum(ranks, 1), 0.0)))
         hit["queries"] = nr
         extra["rag_metrics_vs_exact_fp32"] = hit
+        # the single-query path at k = 100: throughput and recall@100
+        i100 = torch.empty((nq, 100), dtype=torch.int64, device=dev)
+        s100 = torch.empty((nq, 100), dtype=torch.float32, device=dev)
+        ws100 = torch.empty((idx.workspace_bytes(nq, 100, "lut"),), dtype=torch.uint8, device=dev)
+        t100 = timed(lambda: idx.search(Qrot, 100, path="lut", ids=i100, scores=s100,
+                                        workspace=ws100, prerotated=True), reps=2)
+        g100 = i100[:nr].cpu().numpy()
+        rec100 = float(np.mean([len(set(a) & set(b)) / 100 for a, b in zip(g100, ex_all[:, :100])]))
+        extra["lut_k100"] = {"queries_per_s": nq / t100, "recall_at_100_vs_exact_fp32": rec100}
+        log("single-query path k=100: %.0f queries/s, recall@100 %.4f" % (nq / t100, rec100))
+        del i100, s100, ws100
         log("Hit@1 %.3f Hit@5 %.3f MRR@20 %.3f" % (hit["hit_at_1"], hit["hit_at_5"], hit["mrr_at_20"]))
         # single-query latency (one call: rotation + scan + merge)
         lat = []
