@@ -80,10 +80,13 @@ def test_codes_bit_exact(small, rot_pair, bits):
     assert ulps.max() <= 1, ulps.max()
 
 
-@pytest.mark.parametrize("d,bits", [(64, 4), (192, 2), (2048, 4), (2048, 8), (128, 3)])
+@pytest.mark.parametrize("d,bits", [(64, 4), (192, 2), (2048, 4), (2048, 8), (128, 3),
+                                    (64, 8), (192, 8)])
 def test_codes_bit_exact_other_dimensions(d, bits):
     """Rotation tiles of 128 output columns clipped (d = 64) or ragged
-    (d = 192), the largest d, and 3-bit packing at its smallest d."""
+    (d = 192), the largest d, and 3-bit packing at its smallest d; the 8-bit
+    cases take the tiled recomputation of flagged coordinates, here with
+    clipped and ragged column tiles and a ragged last row tile."""
     print("rotate_quantize d=%d bits=%d" % (d, bits), flush=True)
     rng = np.random.default_rng(d * 10 + bits)
     X = rng.standard_normal((1000, d)).astype(np.float32)
