@@ -819,13 +819,52 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
 template <int S>
 __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs,
                                                     const int *__restrict__ ci, int G, int k,
+                                                    const int *__restrict__ gbound,
                                                     int64_t *__restrict__ ids,
                                                     float *__restrict__ scores) {
     __shared__ float st_s[4 * 64 * S];
     __shared__ int st_i[4 * 64 * S];
+    __shared__ int nsurv;
     const int q = blockIdx.x;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
+    // The k best score at least the final bound gbound[q] (a proven lower
+    // bound on the k-th best score), so only entries that reach it can be in
+    // the result.  When at most 64 do, one wave sorts them; otherwise the
+    // lists are merged in full.
+    if (threadIdx.x == 0) nsurv = 0;
+    __syncthreads();
+    {
+        const float bound = unfkey(gbound[q]);
+        const int64_t base = (int64_t)q * G * k;
+        for (int e = threadIdx.x; e < G * k; e += 256) {
+            const float sc = cs[base + e];
+            const int id = ci[base + e];
+            if (id != INT_MAX && !(sc < bound)) {
+                const int pos = atomicAdd(&nsurv, 1);
+                if (pos < 64) {
+                    st_s[pos] = sc;
+                    st_i[pos] = id;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const int ns = nsurv;
+    if (ns <= 64) {
+        if (wave == 0) {
+            float sv = lane < ns ? st_s[lane] : -INFINITY;
+            int iv = lane < ns ? st_i[lane] : INT_MAX;
+            wave_sort64(sv, iv, lane);
+            for (int r = lane; r < k; r += 64) {
+                const bool empty = r >= 64 || !(sv > -INFINITY);
+                ids[(int64_t)q * k + r] = empty ? -1 : (int64_t)iv;
+                scores[(int64_t)q * k + r] = empty ? -INFINITY : sv;
+            }
+        }
+        return;
+    }
+    __syncthreads();   // the stage is reused below
     float ls[S];
     int li[S];
 #pragma unroll
@@ -1274,13 +1313,13 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         if (e != hipSuccess) return e;
         if (S == 1)
             hipLaunchKernelGGL(merge_kernel<1>, dim3(m), dim3(256), 0, stream, cand_s, cand_i,
-                               grid, k, ids + q0 * k, scores + q0 * k);
+                               grid, k, gbound, ids + q0 * k, scores + q0 * k);
         else if (S == 2)
             hipLaunchKernelGGL(merge_kernel<2>, dim3(m), dim3(256), 0, stream, cand_s, cand_i,
-                               grid, k, ids + q0 * k, scores + q0 * k);
+                               grid, k, gbound, ids + q0 * k, scores + q0 * k);
         else
             hipLaunchKernelGGL(merge_kernel<4>, dim3(m), dim3(256), 0, stream, cand_s, cand_i,
-                               grid, k, ids + q0 * k, scores + q0 * k);
+                               grid, k, gbound, ids + q0 * k, scores + q0 * k);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
