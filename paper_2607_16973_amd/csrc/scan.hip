@@ -830,11 +830,11 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
     const int wave = threadIdx.x >> 6;
     // The k best score at least the final bound gbound[q] (a proven lower
     // bound on the k-th best score), so only entries that reach it can be in
-    // the result.  When at most 64 do, one wave sorts them; otherwise the
-    // lists are merged in full.
-    if (threadIdx.x == 0) nsurv = 0;
+    // the result.  For k <= 64, when at most 64 do, one wave sorts them;
+    // otherwise (and for larger k) the lists are merged in full.
+    if (threadIdx.x == 0) nsurv = k <= 64 ? 0 : 65;
     __syncthreads();
-    {
+    if (k <= 64) {
         const float bound = unfkey(gbound[q]);
         const int64_t base = (int64_t)q * G * k;
         for (int e = threadIdx.x; e < G * k; e += 256) {
