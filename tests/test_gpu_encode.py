@@ -59,6 +59,20 @@ def test_query_rotation(small, rot_pair):
     assert np.abs(out1[0] - ref[5]).max() < 2e-6
 
 
+@pytest.mark.parametrize("d", [1536, 64, 192, 2048])
+def test_query_rotation_does_not_depend_on_the_batch(d):
+    """Short batches (up to 64 rows) take their own kernel; every row must
+    rotate to the same bits as in a long batch."""
+    print("query rotation batches d=%d" % d, flush=True)
+    rot = tq.Rotation(d, 9)
+    rng = np.random.default_rng(d)
+    Q = torch.from_numpy(rng.standard_normal((300, d)).astype(np.float32)).cuda()
+    full = tq.rotate_queries(rot, Q)
+    for a, b in [(0, 1), (5, 6), (0, 16), (17, 81), (250, 300), (64, 127)]:
+        part = tq.rotate_queries(rot, Q[a:b].contiguous())
+        assert torch.equal(part, full[a:b]), (a, b)
+
+
 @pytest.mark.parametrize("bits", [4, 2, 8, 3, 1])
 def test_codes_bit_exact(small, rot_pair, bits):
     X, _ = small
