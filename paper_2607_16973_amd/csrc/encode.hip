@@ -84,6 +84,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
     __shared__ double norm_s[BM];
     __shared__ double bnd_s[255];   // the shared thresholds t_i (no TQ+ tables)
+    // TQ+ thresholds of this tile's columns, [levels-1][BN], for b <= 4
+    __shared__ double athr_s[QUANT ? 15 * BN : 1];
     __shared__ unsigned int nflag_s;
 
     const int ncol = (d + BN - 1) / BN;
@@ -147,6 +149,12 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     const int nslab = d / KB;
     if (QUANT && !qa.athr)
         for (int i = tid; i < qa.levels - 1; i += GEMM_THREADS) bnd_s[i] = qa.bounds[i];
+    const bool athr_lds = QUANT && qa.athr && qa.levels <= 16;
+    if (athr_lds)
+        for (int e = tid; e < (qa.levels - 1) * BN; e += GEMM_THREADS) {
+            const int i = e / BN, c = col0 + e % BN;
+            athr_s[e] = c < d ? qa.athr[(int64_t)i * d + c] : 0.0;
+        }
     if (QUANT && tid == 0) nflag_s = 0;
     load_slab(0);
     store_slab(0);
@@ -237,7 +245,9 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
                     } else {
                         // threshold i of this coordinate, before scaling by n
                         auto thr = [&](int i) {
-                            return qa.athr ? qa.athr[(int64_t)i * d + col] : bnd_s[i];
+                            if (!qa.athr) return bnd_s[i];
+                            return athr_lds ? athr_s[i * BN + (col - col0)]
+                                            : qa.athr[(int64_t)i * d + col];
                         };
                         int c = 0;
                         for (int step = L / 2; step >= 1; step >>= 1) {
