@@ -60,14 +60,6 @@ def tail_prob(x, d: int):
     return 0.5 * betaincc(0.5, (d - 1) / 2.0, x * x)
 
 
-def cdf(x, d: int):
-    """P(X <= x) for any x in [-1, 1], by symmetry of the law about 0."""
-    x = np.asarray(x, dtype=np.float64)
-    ax = np.abs(x)
-    t = tail_prob(ax, d)
-    return np.where(x >= 0, 1.0 - t, t)
-
-
 def _central_prob(x, d: int):
     """P(|X| <= x) = I_{x^2}(1/2, (d-1)/2) for x >= 0 (small and exact near 0)."""
     return betainc(0.5, (d - 1) / 2.0, x * x)
