@@ -25,16 +25,17 @@ follows:
 from .marginal import density, tail_prob, cell_mass, cell_first_moment, mse_per_coord
 from .codebook import lloyd_max, Codebook
 from .rotation import splitmix64, uniforms53, gaussians, haar_rotation
-from .encode import (encode, pack_codes, unpack_codes, code_bytes_per_vector, tqplus_fit,
-                     encode_tqplus)
-from .search import (rotate_queries, scores_for_ids, search, exact_search,
+from .encode import (encode, quantise_rotated, pack_codes, unpack_codes, code_bytes_per_vector,
+                     tqplus_fit, encode_tqplus)
+from .search import (rotate_queries, scores_for_ids, score_all, topk_from_scores, search,
+                     exact_search,
                      recall_at_k, hit_at_k, mrr_at_k, allowed_mask, postfilter_search)
 
 __all__ = [
     "density", "tail_prob", "cell_mass", "cell_first_moment", "mse_per_coord",
     "lloyd_max", "Codebook",
     "splitmix64", "uniforms53", "gaussians", "haar_rotation",
-    "encode", "pack_codes", "unpack_codes", "code_bytes_per_vector", "tqplus_fit", "encode_tqplus",
-    "rotate_queries", "scores_for_ids", "search", "exact_search",
+    "encode", "quantise_rotated", "pack_codes", "unpack_codes", "code_bytes_per_vector", "tqplus_fit", "encode_tqplus",
+    "rotate_queries", "scores_for_ids", "score_all", "topk_from_scores", "search", "exact_search",
     "recall_at_k", "hit_at_k", "mrr_at_k", "allowed_mask", "postfilter_search",
 ]

@@ -26,6 +26,17 @@
 #include <stdlib.h>
 #include <string.h>
 
+/* Step 3 for one row: code_j = #{ t : T[t] <= S_j } with T[t] = fl64(t_t * n),
+ * the thresholds already scaled by the row's norm. */
+static void quantise_row(const double *S, const double *T, int32_t d, int32_t L, uint8_t *c)
+{
+    for (int32_t j = 0; j < d; ++j) {
+        int cnt = 0;
+        for (int32_t t = 0; t < L - 1; ++t) cnt += (T[t] <= S[j]);
+        c[j] = (uint8_t)cnt;
+    }
+}
+
 /* Returns 0 on success, -1 on bad arguments, -2 on a non-finite input row
  * (its index is written to *bad_row). */
 int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
@@ -90,11 +101,7 @@ int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
             }
             if (rot_out)
                 for (int32_t j = 0; j < d; ++j) rot_out[(size_t)i * d + j] = S[j];
-            for (int32_t j = 0; j < d; ++j) {
-                int cnt = 0;
-                for (int32_t t = 0; t < L - 1; ++t) cnt += (T[t] <= S[j]);
-                c[j] = (uint8_t)cnt;
-            }
+            quantise_row(S, T, d, L, c);
         }
         free(S);
         free(T);
@@ -102,6 +109,35 @@ int tqo_encode(const float *X, int64_t n, int32_t d, const float *R,
     free(RT);
     if (status == -2 && bad_row) *bad_row = first_bad;
     return status;
+}
+
+/* Step 3 alone, for rows already rotated: S [n][d] the sequential float64
+ * sums and norms [n] the row norms of tqo_encode (rot_out, norm_out), so one
+ * rotation serves several codebooks.  A zero norm gives code L/2. */
+int tqo_quantise(const double *S, const double *norms, int64_t n, int32_t d,
+                 const double *bounds, int32_t L, uint8_t *codes)
+{
+    if (!S || !norms || !bounds || !codes || n < 0 || d <= 0 || L < 2 || L > 256)
+        return -1;
+#pragma omp parallel
+    {
+        double T[255];
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            uint8_t *c = codes + (size_t)i * d;
+            const double nrm = norms[i];
+            if (nrm == 0.0) {
+                memset(c, L / 2, (size_t)d);
+                continue;
+            }
+            for (int32_t t = 0; t < L - 1; ++t) {
+                double p = bounds[t] * nrm;
+                T[t] = p;
+            }
+            quantise_row(S + (size_t)i * d, T, d, L, c);
+        }
+    }
+    return 0;
 }
 
 /* Length-renormalisation scalar (step 5) for rows already coded. */

@@ -36,6 +36,8 @@ def _load():
         lib.tqo_scales.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P,
                                    ctypes.c_int32, P]
         lib.tqo_scales.restype = ctypes.c_int
+        lib.tqo_quantise.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P, ctypes.c_int32, P]
+        lib.tqo_quantise.restype = ctypes.c_int
         lib.tqo_encode_plus.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P, ctypes.c_int32,
                                         P, P, P, P]
         lib.tqo_encode_plus.restype = ctypes.c_int
@@ -88,6 +90,34 @@ def encode(X: np.ndarray, R32: np.ndarray, cb: Codebook, return_rotated: bool = 
     if return_rotated:
         return codes, norms, scales, rot
     return codes, norms, scales
+
+
+def quantise_rotated(S: np.ndarray, norms: np.ndarray, cb: Codebook):
+    """Steps 3 and 5 for rows already rotated by encode(..., return_rotated=True):
+    S float64 [n, d] and norms float64 [n] as it returned them, coded with the
+    codebook cb (so one rotation serves several bit widths).  Returns (codes
+    uint8 [n, d] unpacked, scales float32 [n]), equal to what encode returns
+    for the same rows with cb."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    norms = np.ascontiguousarray(norms, dtype=np.float64)
+    n, d = S.shape
+    if norms.shape != (n,) or cb.d != d:
+        raise ValueError("shape mismatch")
+    L = cb.levels
+    bounds = np.ascontiguousarray(cb.bounds, dtype=np.float64)
+    cents = np.ascontiguousarray(cb.cents, dtype=np.float64)
+    codes = np.empty((n, d), dtype=np.uint8)
+    scales = np.empty(n, dtype=np.float32)
+    lib = _load()
+    st = lib.tqo_quantise(S.ctypes.data, norms.ctypes.data, n, d, bounds.ctypes.data, L,
+                          codes.ctypes.data)
+    if st != 0:
+        raise RuntimeError("tqo_quantise failed (%d)" % st)
+    st = lib.tqo_scales(codes.ctypes.data, norms.ctypes.data, n, d, cents.ctypes.data, L,
+                        scales.ctypes.data)
+    if st != 0:
+        raise RuntimeError("tqo_scales failed (%d)" % st)
+    return codes, scales
 
 
 def tqplus_fit(X: np.ndarray, R32: np.ndarray):

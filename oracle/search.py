@@ -74,6 +74,54 @@ def _pad(ids, sc, k):
     return out_i, out_s
 
 
+def score_all(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray, qrot: np.ndarray,
+              chunk: int = 65536, calib=None) -> np.ndarray:
+    """score_i of every vector against every rotated query (section II-B step
+    5), float64 [nq, n]; qrot float64 [nq, d] from rotate_queries.  The rows
+    are dequantised a chunk at a time; calib: TQ+ (mu, kappa) or None."""
+    qrot = np.atleast_2d(np.asarray(qrot, dtype=np.float64))
+    nq = qrot.shape[0]
+    n = codes.shape[0]
+    cents = np.asarray(cents, dtype=np.float64)
+    sc_all = np.empty((nq, n), dtype=np.float64)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        xhat = _reconstruct(codes[s:e], cents, calib)    # [m, d]
+        sc_all[:, s:e] = (xhat @ qrot.T).T * np.asarray(scales[s:e], dtype=np.float64)[None, :]
+    return sc_all
+
+
+def topk_from_scores(sc_all: np.ndarray, k: int, tenants=None, allow=None, masks=None):
+    """Top-k of every query's row of scores (section III-B): the eligible
+    vectors ordered by (score descending, id ascending), the first
+    min(k, #eligible) kept and the rest padded with (-1, -inf).  A vector is
+    eligible for query b when its tenant's bit is set in allow[b] (if given)
+    and masks[b][i] is true (if given)."""
+    if k <= 0:
+        raise ValueError("k must be positive")
+    nq, n = sc_all.shape
+    ids_out = np.empty((nq, k), dtype=np.int64)
+    sc_out = np.empty((nq, k), dtype=np.float64)
+    all_ids = np.arange(n, dtype=np.int64)
+    for b in range(nq):
+        m = allowed_mask(tenants, None if allow is None else allow[b])
+        if masks is not None and masks[b] is not None:
+            mb = np.asarray(masks[b], dtype=bool)
+            m = mb if m is None else (m & mb)
+        ids = all_ids if m is None else all_ids[m]
+        sc = sc_all[b] if m is None else sc_all[b][m]
+        if sc.shape[0] > k:
+            # only vectors scoring at least the k-th largest score can be
+            # among the first k (ties at that score included); the order
+            # below then decides among them
+            kth = np.partition(sc, sc.shape[0] - k)[sc.shape[0] - k]
+            keep = sc >= kth
+            ids, sc = ids[keep], sc[keep]
+        i, s_ = _order(sc, ids, k)
+        ids_out[b], sc_out[b] = _pad(i, s_, k)
+    return ids_out, sc_out
+
+
 def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
            R32: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,
            chunk: int = 65536, masks=None, calib=None):
@@ -86,28 +134,8 @@ def search(codes: np.ndarray, scales: np.ndarray, cents: np.ndarray,
     II-B, or None."""
     if k <= 0:
         raise ValueError("k must be positive")
-    qrot = rotate_queries(R32, Q)
-    nq = qrot.shape[0]
-    n = codes.shape[0]
-    cents = np.asarray(cents, dtype=np.float64)
-    sc_all = np.empty((nq, n), dtype=np.float64)
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
-        xhat = _reconstruct(codes[s:e], cents, calib)    # [m, d]
-        sc_all[:, s:e] = (xhat @ qrot.T).T * np.asarray(scales[s:e], dtype=np.float64)[None, :]
-    ids_out = np.empty((nq, k), dtype=np.int64)
-    sc_out = np.empty((nq, k), dtype=np.float64)
-    all_ids = np.arange(n, dtype=np.int64)
-    for b in range(nq):
-        m = allowed_mask(tenants, None if allow is None else allow[b])
-        if masks is not None and masks[b] is not None:
-            mb = np.asarray(masks[b], dtype=bool)
-            m = mb if m is None else (m & mb)
-        ids = all_ids if m is None else all_ids[m]
-        sc = sc_all[b] if m is None else sc_all[b][m]
-        i, s_ = _order(sc, ids, k)
-        ids_out[b], sc_out[b] = _pad(i, s_, k)
-    return ids_out, sc_out
+    sc_all = score_all(codes, scales, cents, rotate_queries(R32, Q), chunk=chunk, calib=calib)
+    return topk_from_scores(sc_all, k, tenants, allow, masks)
 
 
 def exact_search(X: np.ndarray, Q: np.ndarray, k: int, tenants=None, allow=None,

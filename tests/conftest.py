@@ -39,16 +39,19 @@ def small_env():
     import oracle
     import paper_2607_16973_amd as tq
     import synth
+    from tests.parity import oracle_tables
     d = 1536
     s = SmallSetup()
     s.X, s.Q = synth.workload("small")
-    s.R32 = oracle.haar_rotation(d, 42)[1]
-    s.ocb = oracle.lloyd_max(d, 4)
+    s.cb = tq.Codebook(d, 4)
+    s.rot = tq.Rotation(d, 42)
+    # the oracle encodes with the library's rotation and tables (the
+    # parameters of the encode definition), so codes agree bit for bit
+    s.R32 = s.rot.matrix()
+    s.ocb = oracle_tables(s.cb)
     s.codes, s.norms, s.scales = oracle.encode(s.X, s.R32, s.ocb)
     s.qrot = oracle.rotate_queries(s.R32, s.Q)
     s.qn = np.linalg.norm(s.Q.astype(np.float64), axis=1)
-    s.cb = tq.Codebook(d, 4)
-    s.rot = tq.Rotation(d, 42)
     s.Xd = torch.from_numpy(s.X).cuda()
     s.Qd = torch.from_numpy(s.Q).cuda()
     s.idx = tq.Index(s.cb, s.rot, n_tenants=1)

@@ -10,6 +10,42 @@ SCORE_RTOL = 1e-4          # relative tolerance on scores
 SCORE_ATOL_Q = 1e-6        # absolute floor, times ||q||
 
 
+def oracle_tables(cb) -> "oracle.Codebook":
+    """The library's exported boundaries and centroids (tq.Codebook) as an
+    oracle Codebook.  The encode definition (section II-B steps 1-4) takes
+    the rotation and the tables as parameters: parity tests give the oracle
+    exactly the parameters the kernels use (the library's float32 R from
+    Rotation.matrix() and these tables), so the codes must agree bit for bit.
+    That the library's tables and rotation agree with the oracle's own solve
+    and factorisation is a separate host test (tests/test_lib_host.py)."""
+    bounds = np.array(cb.bounds, dtype=np.float64)
+    cents = np.array(cb.cents, dtype=np.float64)
+    bounds.setflags(write=False)
+    cents.setflags(write=False)
+    return oracle.Codebook(d=cb.d, bits=cb.bits, bounds=bounds, cents=cents, iterations=0,
+                           converged=True)
+
+
+def assert_codes_equal(codes_gpu_packed, codes_or, bits):
+    """Packed GPU codes equal to the oracle's unpacked codes, bit for bit;
+    on failure the message names the first differing (row, coordinate)."""
+    d = codes_or.shape[1]
+    got = oracle.unpack_codes(np.asarray(codes_gpu_packed), d, bits)
+    bad = np.argwhere(got != codes_or)
+    assert bad.size == 0, ("code mismatches", len(bad), bad[:5].tolist())
+    assert np.array_equal(np.asarray(codes_gpu_packed), oracle.pack_codes(codes_or, bits))
+
+
+def assert_scales_close(scales_gpu, scales_or, max_ulp=1):
+    """float32 scales within max_ulp units in the last place of the oracle's
+    float64 value rounded to float32 (the library sums the squared levels in
+    another order)."""
+    a = np.asarray(scales_gpu, dtype=np.float32).view(np.int32).astype(np.int64)
+    b = np.asarray(scales_or, dtype=np.float32).view(np.int32).astype(np.int64)
+    if a.size:
+        assert np.abs(a - b).max() <= max_ulp, int(np.abs(a - b).max())
+
+
 def score_tol(ref, qnorm):
     return np.maximum(SCORE_RTOL * np.abs(ref), SCORE_ATOL_Q * qnorm)
 

@@ -13,7 +13,7 @@ import pytest
 import oracle
 import synth
 from tests.conftest import gpu_available
-from tests.parity import check_topk, check_topk_sampled
+from tests.parity import check_topk, check_topk_sampled, oracle_tables
 
 pytestmark = pytest.mark.gpu
 if not gpu_available():
@@ -182,9 +182,8 @@ def test_largest_dimension():
     Qd = torch.from_numpy(Q).cuda()
     ids, sc = idx.search(Qd, 10, path="mfma")
     same_as_lut(idx, Qd, 10, ids, sc)
-    R32 = oracle.haar_rotation(d, 7)[1]
-    check_topk_sampled(ids.cpu().numpy(), sc.cpu().numpy(), X, R32, oracle.lloyd_max(d, 4), Q, 10,
-                       np.arange(X.shape[0]))
+    check_topk_sampled(ids.cpu().numpy(), sc.cpu().numpy(), X, rot.matrix(), oracle_tables(cb),
+                       Q, 10, np.arange(X.shape[0]))
 
 
 def test_unsupported_shapes_rejected(env):

@@ -1,18 +1,30 @@
-"""GPU parity at the full benchmark size: the 1,000,000 x 1536 power-law
-mixture corpus, 4-bit codes, k=10, in the launch configuration of bench.py
-(queries rotated first, then the scan with the rotation step skipped).
+"""GPU parity at the full benchmark size against the oracle's brute force over
+the whole corpus (section IV-A ground truth; section II-B for the codes and
+scores).
 
-The oracle cannot search 10^6 vectors per query here, so every check is on
-outputs it can compute one by one: codes of sampled rows (bit-exact), the
-score of every returned id, and the property that no sampled vector beats a
-returned list's worst entry (see tests.parity.check_topk_sampled)."""
+The 1,000,000 x 1536 power-law corpus is coded by the oracle in full at
+b = 2, 3, 4 and 8 and scored against 32 queries (tests/fullsize.py).  Then:
+
+* the index's codes equal the oracle's for every one of the 10^6 rows, at
+  every bit width;
+* every top-k list -- the single-query scan at k = 10 and 100, the batched
+  matrix-core path at k = 10 and 100, tenant-filtered searches at
+  T in {10, 100, 1000} with selective and broad allowlists (section V-C), and
+  the 2-, 3- and 8-bit scans -- is checked by tests.parity.check_topk against
+  the oracle's top-k over all 10^6 vectors;
+* the 999,000-row corpus (the first 999,000 rows, same queries) on the
+  single-query scan at k = 10 and 100 and in batched calls of 1, 32 and 256
+  queries.
+
+Searches run in bench.py's launch configuration: queries rotated first,
+then the scan with the rotation step skipped."""
 import numpy as np
 import pytest
 
 import oracle
 import synth
 from tests.conftest import gpu_available
-from tests.parity import check_topk_sampled
+from tests.parity import check_topk
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 if not gpu_available():
@@ -21,8 +33,10 @@ if not gpu_available():
 import torch  # noqa: E402
 
 import paper_2607_16973_amd as tq  # noqa: E402
+from tests.fullsize import PowerlawCorpus, assert_index_codes_equal  # noqa: E402
 
-D, N, K, NQ = 1536, 1_000_000, 10, 16
+D, N, NQ = 1536, 1_000_000, 32
+N999 = 999_000
 
 
 class Big:
@@ -32,42 +46,41 @@ class Big:
 @pytest.fixture(scope="module")
 def big():
     b = Big()
-    print("generating the 1M corpus", flush=True)
-    b.X, Q = synth.workload("powerlaw1m", d=D)
-    b.Q = np.ascontiguousarray(Q[:NQ])
-    b.R32 = oracle.haar_rotation(D, 42)[1]
-    b.ocb = oracle.lloyd_max(D, 4)
-    b.cb, b.rot = tq.Codebook(D, 4), tq.Rotation(D, 42)
-    b.Xd = torch.from_numpy(b.X).cuda()
-    b.idx = tq.Index(b.cb, b.rot, n_tenants=1)
+    b.c = PowerlawCorpus("powerlaw1m", nq=NQ, bits=(4, 2, 3, 8))
+    b.Xd = torch.from_numpy(b.c.X).cuda()
+    b.idx = tq.Index(b.c.cb[4], b.c.rot, n_tenants=1)
     b.idx.reserve(N)
     print("index add n=%d" % N, flush=True)
     b.idx.add(b.Xd)
-    b.Qrot = tq.rotate_queries(b.rot, torch.from_numpy(b.Q).cuda())
+    b.Qall = torch.from_numpy(b.c.Qall).cuda()
+    b.Qrot = tq.rotate_queries(b.c.rot, b.Qall[:NQ].contiguous())
     torch.cuda.synchronize()
-    b.sample = np.random.default_rng(7).choice(N, 20000, replace=False)
     yield b
     del b.Xd
     torch.cuda.empty_cache()
 
 
-def test_codes_of_sampled_rows(big):
-    rows = np.sort(np.random.default_rng(3).choice(N, 2000, replace=False))
-    codes, _, _ = big.idx.export()
-    got = codes[torch.from_numpy(rows).cuda()].cpu().numpy()
-    ref, _, _ = oracle.encode(np.ascontiguousarray(big.X[rows]), big.R32, big.ocb)
-    assert np.array_equal(got, oracle.pack_codes(ref, 4))
-    del codes
+def _check(big, bits, ids, sc, k, n=None, tenants=None, allow=None, masks=None):
+    c = big.c
+    n = N if n is None else n
+    ref_i, ref_s = c.topk(bits, k, n=n, tenants=tenants, allow=allow)
+    check_topk(ids[:NQ].cpu().numpy(), sc[:NQ].cpu().numpy(), c.codes[bits][:n],
+               c.scales[bits][:n], c.ocb[bits].cents, c.qrot, c.qn, k, ref_i, ref_s,
+               allowed=masks, n=n)
 
 
-@pytest.mark.parametrize("path", ["lut", "mfma"])
-def test_search_full_size(big, path):
-    print("search N=%d path=%s" % (N, path), flush=True)
-    ids, sc = big.idx.search(big.Qrot, K, path=path, prerotated=True)
-    check_topk_sampled(ids.cpu().numpy(), sc.cpu().numpy(), big.X, big.R32, big.ocb, big.Q, K,
-                       big.sample)
+def test_codes_of_every_row(big):
+    print("codes of %d rows, b=4" % N, flush=True)
+    assert_index_codes_equal(big.idx, big.c.codes[4], 4)
+
+
+@pytest.mark.parametrize("path,k", [("lut", 10), ("lut", 100), ("mfma", 10), ("mfma", 100)])
+def test_search_full_size(big, path, k):
+    print("search N=%d path=%s k=%d" % (N, path, k), flush=True)
+    ids, sc = big.idx.search(big.Qrot, k, path=path, prerotated=True)
+    _check(big, 4, ids, sc, k)
     if path == "mfma":
-        li, ls = big.idx.search(big.Qrot, K, path="lut", prerotated=True)
+        li, ls = big.idx.search(big.Qrot, k, path="lut", prerotated=True)
         assert torch.equal(torch.sort(sc, 1).values, torch.sort(ls, 1).values)
 
 
@@ -80,19 +93,58 @@ def test_top64_of_k64_and_k65_agree_full_size(big):
     assert torch.equal(a_i, b_i[:, :64]) and torch.equal(a_s, b_s[:, :64])
 
 
-def test_filtered_full_size(big):
-    T = 100
+@pytest.mark.parametrize("T", [10, 100, 1000])
+def test_filtered_full_size(big, T):
+    """Zipf(1.1) tenants at random positions; one tenant per query
+    (selective) or ceil(T/10) tenants (broad); blocks skipped by summary."""
     ten = synth.zipf_tenants(N, T, seed=44)
-    idx = tq.Index(big.cb, big.rot, n_tenants=T)
+    idx = tq.Index(big.c.cb[4], big.c.rot, n_tenants=T)
     idx.reserve(N)
     idx.add(big.Xd, torch.from_numpy(ten.view(np.int16)).cuda())
     for mode in ("selective", "broad"):
         print("filtered N=%d T=%d %s" % (N, T, mode), flush=True)
         bm = synth.allowlist_bitmap(synth.allowlists(NQ, T, mode, seed=45), T)
-        ids, sc = idx.search(big.Qrot, K, allow=torch.from_numpy(bm.view(np.int64)).cuda(),
+        ids, sc = idx.search(big.Qrot, 10, allow=torch.from_numpy(bm.view(np.int64)).cuda(),
                              prerotated=True)
         masks = [oracle.allowed_mask(ten, bm[b]) for b in range(NQ)]
-        check_topk_sampled(ids.cpu().numpy(), sc.cpu().numpy(), big.X, big.R32, big.ocb, big.Q, K,
-                           big.sample, allowed=masks)
+        _check(big, 4, ids, sc, 10, tenants=ten, allow=bm, masks=masks)
+    del idx
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("bits", [2, 3, 8])
+def test_other_bit_widths_full_size(big, bits):
+    """The bit-width sweep's corpus: the GPU encode of all 10^6 rows equals
+    the oracle's codes, and the single-query scan's top-10 the oracle's."""
+    print("encode and search N=%d b=%d" % (N, bits), flush=True)
+    idx = tq.Index(big.c.cb[bits], big.c.rot, n_tenants=1)
+    idx.reserve(N)
+    idx.add(big.Xd)
+    assert_index_codes_equal(idx, big.c.codes[bits], bits)
+    ids, sc = idx.search(big.Qrot, 10, prerotated=True)
+    _check(big, bits, ids, sc, 10)
+    del idx
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("k", [10, 100])
+def test_999k_single_query_and_batches_of_1_32_256(big, k):
+    """The 999K corpus: the single-query scan against the oracle's brute
+    force, and the batched path in calls of 1, 32 and 256 queries returning
+    the single-query path's scores (the first 32 queries also against the
+    oracle)."""
+    print("999K k=%d" % k, flush=True)
+    idx = tq.Index(big.c.cb[4], big.c.rot, n_tenants=1)
+    idx.reserve(N999)
+    idx.add(big.Xd[:N999])
+    q = big.Qall[:256].contiguous()
+    li, ls = idx.search(q, k, path="lut")
+    _check(big, 4, li, ls, k, n=N999)
+    for b in (1, 32, 256):
+        mi, ms = idx.search(q[:b].contiguous(), k, path="mfma")
+        print("batch %d fallbacks %d" % (b, tq.last_search_fallbacks()), flush=True)
+        assert np.array_equal(np.sort(ms.cpu().numpy(), axis=1), np.sort(ls[:b].cpu().numpy(), axis=1))
+        if b >= NQ:
+            _check(big, 4, mi, ms, k, n=N999)
     del idx
     torch.cuda.empty_cache()

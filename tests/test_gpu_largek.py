@@ -8,7 +8,7 @@ import pytest
 import oracle
 import synth
 from tests.conftest import gpu_available
-from tests.parity import check_topk
+from tests.parity import check_topk, oracle_tables
 
 pytestmark = pytest.mark.gpu
 if not gpu_available():
@@ -81,9 +81,10 @@ def test_large_k_filtered(env):
 def test_large_k_other_bit_widths(env, bits):
     print("large k bits=%d" % bits, flush=True)
     n = 2000
-    ocb = oracle.lloyd_max(D, bits)
+    cb = tq.Codebook(D, bits)
+    ocb = oracle_tables(cb)
     codes, _, scales = oracle.encode(env.X[:n], env.R32, ocb)
-    idx = tq.Index(tq.Codebook(D, bits), env.rot, n_tenants=1)
+    idx = tq.Index(cb, env.rot, n_tenants=1)
     idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
                   torch.from_numpy(scales).cuda())
     ids, sc = idx.search(env.Qd, 700)

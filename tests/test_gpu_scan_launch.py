@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 from tests.conftest import gpu_available
-from tests.parity import check_topk
+from tests.parity import check_topk, oracle_tables
 
 pytestmark = pytest.mark.gpu
 if not gpu_available():
@@ -73,10 +73,11 @@ def test_other_dimensions(d, bits):
     Q = np.ascontiguousarray(Q.astype(np.float32))
     rot = tq.Rotation(d, 11)
     R32 = rot.matrix()
-    ocb = oracle.lloyd_max(d, bits)
+    cb = tq.Codebook(d, bits)
+    ocb = oracle_tables(cb)
     codes, _, scales = oracle.encode(X, R32, ocb)
     tenants = rng.integers(0, 5, n).astype(np.uint16)
-    idx = tq.Index(tq.Codebook(d, bits), rot, n_tenants=5)
+    idx = tq.Index(cb, rot, n_tenants=5)
     idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
                   torch.from_numpy(scales).cuda(),
                   torch.from_numpy(tenants.view(np.int16)).cuda())

@@ -14,7 +14,8 @@ import pytest
 import oracle
 import synth
 from tests.conftest import gpu_available
-from tests.parity import check_topk
+from tests.parity import (assert_codes_equal, assert_scales_close, check_topk,
+                          oracle_tables)
 
 pytestmark = pytest.mark.gpu
 if not gpu_available():
@@ -40,9 +41,8 @@ def oracle_topk(s, k, tenants=None, allow=None, n=None):
 
 def test_index_holds_the_oracle_codes(env):
     codes, scales, tenants = env.idx.export()
-    assert np.array_equal(codes.cpu().numpy(), oracle.pack_codes(env.codes, 4))
-    s = scales.cpu().numpy()
-    assert np.abs(s.view(np.int32).astype(np.int64) - env.scales.view(np.int32).astype(np.int64)).max() <= 1
+    assert_codes_equal(codes.cpu().numpy(), env.codes, 4)
+    assert_scales_close(scales.cpu().numpy(), env.scales)
     assert np.all(tenants.cpu().numpy() == 0)
 
 
@@ -132,9 +132,9 @@ def test_bad_tenant_rejected(env):
 def test_other_bit_widths(env, bits):
     print("bits=%d search" % bits, flush=True)
     n = 2000
-    ocb = oracle.lloyd_max(D, bits)
-    codes, norms, scales = oracle.encode(env.X[:n], env.R32, ocb)
     cb = tq.Codebook(D, bits)
+    ocb = oracle_tables(cb)
+    codes, norms, scales = oracle.encode(env.X[:n], env.R32, ocb)
     idx = tq.Index(cb, env.rot, n_tenants=1)
     idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
                   torch.from_numpy(scales).cuda())
@@ -145,6 +145,6 @@ def test_other_bit_widths(env, bits):
     # the index built by the GPU encode holds the same codes
     idx2 = tq.Index(cb, env.rot, n_tenants=1)
     idx2.add(env.Xd[:n].contiguous())
-    c2, _, _ = idx2.export()
-    c2 = oracle.unpack_codes(c2.cpu().numpy(), D, bits)
-    assert np.count_nonzero(c2 != codes) <= 2
+    c2, s2, _ = idx2.export()
+    assert_codes_equal(c2.cpu().numpy(), codes, bits)
+    assert_scales_close(s2.cpu().numpy(), scales)

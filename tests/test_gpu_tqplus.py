@@ -2,11 +2,9 @@
 
 * The fit (per-coordinate mean and spread of the rotated, normalised first
   batch) matches oracle.tqplus_fit within float32 storage of float64 sums.
-* Given the library's installed (mu, kappa), codes equal oracle.encode_tqplus
-  bit for bit -- a mismatch is allowed only where the two sides' inputs
-  differ (their codebooks and rotations are solved separately) and the
-  oracle's own float64 value lies within 1e-9 ||x|| of a threshold -- and
-  scales agree to one float32 ulp.
+* Given the library's installed (mu, kappa), rotation and tables, codes
+  equal oracle.encode_tqplus bit for bit and scales agree to one float32
+  ulp.
 * Searches (unfiltered, tenant-filtered, large k, post-filter; b = 2, 3, 4,
   8) return lists the oracle's calibrated scores validate, as in the plain
   parity tests.
@@ -19,7 +17,7 @@ import pytest
 import oracle
 import synth
 from tests.conftest import gpu_available
-from tests.parity import check_topk
+from tests.parity import assert_codes_equal, assert_scales_close, check_topk, oracle_tables
 
 pytestmark = pytest.mark.gpu
 if not gpu_available():
@@ -41,10 +39,10 @@ def _build(d, bits, n, nq, n_fit, n_tenants=1, seed=42):
     e.d, e.bits = d, bits
     e.X = synth.shifted_mixture(n, d)
     e.Q = synth.isotropic_queries(e.X, nq, seed=47)
-    e.R32 = oracle.haar_rotation(d, seed)[1]
-    e.ocb = oracle.lloyd_max(d, bits)
     e.cb = tq.Codebook(d, bits)
     e.rot = tq.Rotation(d, seed)
+    e.R32 = e.rot.matrix()
+    e.ocb = oracle_tables(e.cb)
     e.Xd = torch.from_numpy(e.X).cuda()
     e.Qd = torch.from_numpy(e.Q).cuda()
     e.idx = tq.Index(e.cb, e.rot, n_tenants=n_tenants)
@@ -72,20 +70,8 @@ def env():
 
 def _check_codes(e):
     codes, scales, _ = e.idx.export()
-    c_gpu = oracle.unpack_codes(codes.cpu().numpy(), e.d, e.bits)
-    s_gpu = scales.cpu().numpy()
-    bad = np.argwhere(c_gpu != e.codes)
-    if bad.size:
-        S = e.X.astype(np.float64) @ e.R32.astype(np.float64).T
-        mu = e.mu.astype(np.float64)
-        ka = e.kappa.astype(np.float64)
-        for i, j in bad:
-            thr = (mu[j] + ka[j] * e.ocb.bounds) * e.norms[i]
-            margin = np.min(np.abs(S[i, j] - thr)) / e.norms[i]
-            assert margin <= 1e-9, ("unexplained code mismatch", int(i), int(j), float(margin))
-    assert len(bad) <= 1e-6 * c_gpu.size + 2
-    ulps = np.abs(s_gpu.view(np.int32).astype(np.int64) - e.scales.view(np.int32).astype(np.int64))
-    assert ulps.max() <= 1, ulps.max()
+    assert_codes_equal(codes.cpu().numpy(), e.codes, e.bits)
+    assert_scales_close(scales.cpu().numpy(), e.scales)
 
 
 def test_fit_matches_oracle(env):
@@ -98,8 +84,9 @@ def test_fit_over_several_chunks():
     # more rows than one rotation chunk of the fit (16384), d = 256
     d = 256
     X = synth.shifted_mixture(20000, d)
-    R32 = oracle.haar_rotation(d, 9)[1]
-    idx = tq.Index(tq.Codebook(d, 4), tq.Rotation(d, 9))
+    rot = tq.Rotation(d, 9)
+    R32 = rot.matrix()
+    idx = tq.Index(tq.Codebook(d, 4), rot)
     print("calibrate d=256 m=20000", flush=True)
     idx.calibrate(torch.from_numpy(X).cuda())
     mu, kappa = idx.calibration()

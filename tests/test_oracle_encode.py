@@ -148,3 +148,30 @@ def test_distortion_and_scale_match_the_codebook():
     # the scaled reconstruction has exactly the original length
     np.testing.assert_allclose(np.linalg.norm(xhat, axis=1) * s, 1.0, rtol=1e-7)
     assert abs(s.mean() - 1 / math.sqrt(1 - dm)) < 5 * s.std(ddof=1) / math.sqrt(s.size) + 1e-6
+
+
+def test_quantise_rotated_is_searchsorted_of_the_rotated_rows():
+    """Step 3 on rows already rotated: with the identity rotation the rotated
+    values are the rows themselves, so the codes are numpy's searchsorted of
+    x/||x|| against the boundaries (ties upper); a zero row gets L/2; and the
+    codes and scales equal encode's at every bit width."""
+    d = 128
+    rng = np.random.default_rng(11)
+    X = rng.standard_normal((50, d)).astype(np.float32)
+    X[3] = 0
+    R = oracle.haar_rotation(d, 3)[1]
+    _, norms, _, S = oracle.encode(X, R, oracle.lloyd_max(d, 4), return_rotated=True)
+    for bits in (1, 2, 3, 4, 8):
+        cb = oracle.lloyd_max(d, bits)
+        codes, scales = oracle.quantise_rotated(S, norms, cb)
+        c2, _, s2 = oracle.encode(X, R, cb)
+        assert np.array_equal(codes, c2) and np.array_equal(scales, s2)
+        assert np.all(codes[3] == (1 << bits) // 2) and scales[3] == 0
+        X64 = X.astype(np.float64)
+        Y = X64 / np.maximum(np.linalg.norm(X64, axis=1, keepdims=True), 1e-300)
+        ci, _ = oracle.quantise_rotated(X64, np.linalg.norm(X64, axis=1), cb)
+        ref = np.searchsorted(cb.bounds, Y, side="right")
+        ref[3] = (1 << bits) // 2
+        # X64 / n and fl64(t n) <= x agree except within one rounding of a
+        # boundary; random normal rows have none there
+        assert np.array_equal(ci, ref)

@@ -172,3 +172,21 @@ def test_postfilter_baseline():
     f_i, _ = oracle.postfilter_search(codes, scales, cb.cents, R, Q, 5, 80, ten, only2)
     g_i, _ = oracle.search(codes, scales, cb.cents, R, Q, 5, ten, only2)
     assert np.array_equal(f_i, g_i)
+
+
+def test_topk_from_scores_brute_force_with_ties():
+    """Selection on score rows full of ties (small integers) equals Python's
+    sort by (score desc, id asc) over the eligible ids, for k below, at and
+    above the number of eligible vectors."""
+    rng = np.random.default_rng(5)
+    sc = rng.integers(0, 6, (7, 40)).astype(np.float64)
+    masks = [None] + [rng.random(40) < p for p in (0.9, 0.5, 0.2, 0.05, 0.0, 1.0)]
+    for k in (1, 3, 8, 40, 50):
+        ids, out = oracle.topk_from_scores(sc, k, masks=masks)
+        for b in range(7):
+            elig = [i for i in range(40) if masks[b] is None or masks[b][i]]
+            ref = sorted(elig, key=lambda i: (-sc[b, i], i))[:k]
+            n = len(ref)
+            assert ids[b, :n].tolist() == ref
+            assert np.array_equal(out[b, :n], sc[b, ref])
+            assert np.all(ids[b, n:] == -1) and np.all(np.isneginf(out[b, n:]))
