@@ -358,6 +358,25 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq,
                        void *workspace_dev, size_t workspace_bytes,
                        int64_t *ids_dev, float *scores_dev, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): tq_search
+ * with the same arguments, meaning, layout and results (the single-query
+ * scan), whose workspace is a device array of TQ_NOALLOC_SCRATCH_BYTES held
+ * by the library (one per GPU, kept until the process ends) instead of a
+ * per-call allocation.  It calls no device allocation or free.
+ * Queries are taken in as many consecutive launches as the array needs; a
+ * search whose single query needs more than the array (k > 256 over a very
+ * large index) returns TQ_EUNSUPPORTED.  The index's rotation must already
+ * be on the current device -- it is uploaded by the first tq_index_add,
+ * tq_index_calibrate or allocating search on the index -- else TQ_EINVAL.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (two streams or threads) race and must be serialised by the
+ * caller; consecutive calls on one stream are safe. */
+#define TQ_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+tq_status tq_search_noalloc(const tq_index *idx, const float *Q_dev, int64_t nq,
+                            int32_t k, const uint64_t *allow_dev, int64_t *ids_dev,
+                            float *scores_dev, void *stream);
+
 /* Number of queries of the calling thread's last tq_search_ex call that the
  * TQ_PATH_MFMA path re-ran on the LUT path because their certificate failed
  * (0 after any other path). */

@@ -347,6 +347,26 @@ class Index:
                             _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
         return ids, scores
 
+    def search_noalloc(self, Q, k: int, allow=None, ids=None, scores=None):
+        """tq_search_noalloc: tq_search with the library's own device scratch
+        array as workspace (no device allocation inside the call).  ids and
+        scores may be given to write into existing tensors."""
+        torch = _torch()
+        nq = Q.shape[0]
+        _shape(Q, (nq, self.d), "Q")
+        _shape(allow, (nq, self.words), "allow")
+        _shape(ids, (nq, k), "ids")
+        _shape(scores, (nq, k), "scores")
+        if ids is None:
+            ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
+        if scores is None:
+            scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
+        check(lib.tq_search_noalloc(self._h, _dev_ptr(Q, torch.float32, "Q", 2), nq, k,
+                                    _dev_ptr(allow, torch.int64, "allow") if allow is not None else None,
+                                    _dev_ptr(ids, torch.int64, "ids"),
+                                    _dev_ptr(scores, torch.float32, "scores"), _stream(Q.device)))
+        return ids, scores
+
     # the free function is bound when the class is defined: module globals may
     # already be gone when an object is collected at interpreter exit
     def __del__(self, _free=lib.tq_index_free):

@@ -70,6 +70,7 @@ def _load():
         "tq_search_postfilter": ([P, P, I64, I32, I32, P, P, P, P], ctypes.c_int),
         "tq_search_workspace_size": ([P, I64, I32, I32, P], ctypes.c_int),
         "tq_search_ex": ([P, P, I64, I32, P, I32, P, SZ, P, P, P], ctypes.c_int),
+        "tq_search_noalloc": ([P, P, I64, I32, P, P, P, P], ctypes.c_int),
         "tq_last_search_fallbacks": ([], ctypes.c_int32),
     }
     for name, (args, res) in sig.items():
@@ -89,7 +90,7 @@ EXPORTED = ("tq_last_error", "tq_version", "tq_build_codebook", "tq_codebook_tab
             "tq_index_slots", "tq_slot_allowlist", "tq_index_calibrate",
             "tq_index_set_calibration", "tq_index_calibration",
             "tq_index_free", "tq_search", "tq_search_postfilter", "tq_search_workspace_size",
-            "tq_search_ex", "tq_last_search_fallbacks")
+            "tq_search_ex", "tq_search_noalloc", "tq_last_search_fallbacks")
 
 
 def check(status: int) -> None:

@@ -21,7 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtq.so")
 
-HIP_SOURCES = ["encode.hip", "scan.hip", "batch.hip", "layout.hip", "calib.hip", "api.cpp"]
+HIP_SOURCES = ["encode.hip", "scan.hip", "batch.hip", "layout.hip", "calib.hip", "noalloc.hip",
+               "api.cpp"]
 # Per-source extra flags.  The scan's prefetch ring must stay where it is
 # written: machine sinking would move every refill into the loop latch and
 # serialise the loads with the table lookups.  The atomic optimizer would

@@ -159,6 +159,22 @@ struct tq_index {
     double *ysq = nullptr;                   // [d][levels]: (mu_j + kappa_j c_c)^2
 };
 
+namespace tq {
+
+// Whether the index's rotation is already on the current device, so that a
+// search rotates its queries without allocating.
+bool index_rotation_resident(const tq_index *x) {
+    std::lock_guard<std::mutex> lk(x->rot.mu);
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return x->rot.R_dev != nullptr && x->rot.R_dev_device == dev;
+}
+
+}  // namespace tq
+
 namespace {
 
 size_t block_bytes(const tq_index *x) { return (size_t)x->chunks * 1024; }

@@ -30,6 +30,10 @@ bool solve_lloyd_max(int d, int bits, CodebookTables *out);
 // Haar orthogonal matrix for (d, seed), float32 row-major (host).
 bool make_rotation(int d, uint64_t seed, std::vector<float> *R32);
 
+// -------------------------------------------------------------------- index
+// Whether the index's rotation is already on the current device.
+bool index_rotation_resident(const tq_index *x);
+
 }  // namespace tq
 
 // Opaque handle definitions (C ABI types).
