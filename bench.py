@@ -135,8 +135,8 @@ def filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev, T=100):
         alg = scanned * 64 * (d * bits // 8 + 4 + 2) + nq * nblk * W * 8
         out[mode] = {"queries_per_s": nq / t, "blocks_scanned_fraction": scanned / (nq * nblk),
                      "achieved_GBps": alg / t / 1e9}
-        log("filtered %s: %.0f queries/s, %.3f of blocks scanned, %.0f GB/s"
-            % (mode, nq / t, scanned / (nq * nblk), alg / t / 1e9))
+        log("filtered T=%d %s: %.0f queries/s, %.3f of blocks scanned, %.0f GB/s"
+            % (T, mode, nq / t, scanned / (nq * nblk), alg / t / 1e9))
     return out
 
 
@@ -277,30 +277,55 @@ def bit_sweep(tq, rot, X, Qrot, k, n, d, stream):
     return out
 
 
-def cpu_baseline(X, Q, d, bits, k, n_full, sample_rows=131072, sample_queries=256):
-    """The oracle as it stands, on a bounded sample, scaled to N = n_full."""
-    import numpy as np
+def cpu_model() -> str:
+    """The host CPU's model name from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(X, Q, d, bits, k, n_full, sample_rows=131072, sample_queries=256,
+                 one_thread_rows=16384, one_thread_queries=64):
+    """The oracle as it stands, on a bounded sample, scaled to N = n_full:
+    with every host core of the affinity set, then with one thread (BLAS and
+    OpenMP limited to one) on a smaller sample."""
+    import threadpoolctl
 
     import oracle
     cores = len(os.sched_getaffinity(0))
     R32 = oracle.haar_rotation(d, 42)[1]
     cb = oracle.lloyd_max(d, bits)
-    t0 = time.perf_counter()
-    codes, norms, scales = oracle.encode(X[:sample_rows], R32, cb)
-    t_enc = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    oracle.search(codes, scales, cb.cents, R32, Q[:sample_queries], k)
-    t_search = time.perf_counter() - t0
-    qps_sample = sample_queries / t_search
+
+    def run(rows, nq):
+        t0 = time.perf_counter()
+        codes, norms, scales = oracle.encode(X[:rows], R32, cb)
+        t_enc = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        oracle.search(codes, scales, cb.cents, R32, Q[:nq], k)
+        t_search = time.perf_counter() - t0
+        return nq / t_search * rows / n_full, rows / t_enc
+
+    qps, enc = run(sample_rows, sample_queries)
+    with threadpoolctl.threadpool_limits(limits=1):
+        qps1, enc1 = run(one_thread_rows, one_thread_queries)
     return {
-        "value": qps_sample * sample_rows / n_full,
+        "value": qps,
         "unit": "queries/s",
         "cores": cores,
         "kind": "oracle",
         "sample": ("oracle search (float64 dequantise + BLAS, sort) of %d queries over the first "
                    "%d corpus vectors coded by the oracle's own encode; queries/s scaled "
                    "linearly to N=%d" % (sample_queries, sample_rows, n_full)),
-        "oracle_encode_vectors_per_s": sample_rows / t_enc,
+        "cpu_model": cpu_model(),
+        "oracle_encode_vectors_per_s": enc,
+        "one_thread": {"value": qps1, "oracle_encode_vectors_per_s": enc1,
+                       "sample": "%d queries over the first %d vectors, BLAS and OpenMP limited "
+                                 "to one thread" % (one_thread_queries, one_thread_rows)},
     }
 
 
@@ -313,8 +338,8 @@ def main() -> int:
     ap.add_argument("--k", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip recall / latency extras")
-    ap.add_argument("--sweep", action="store_true",
-                    help="also encode the corpus and search at b = 2, 3, 4, 8 bits")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the bit-width sweep (encode and search at b = 2, 3, 4, 8)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run three 1 GiB device-to-device copies (a kernel of "
                          "known traffic for scaling the HBM byte counters)")
@@ -460,10 +485,12 @@ def main() -> int:
         extra["single_query_latency_ms_p50"] = float(np.median(lat))
         log("recall@%d %.4f  single-query latency %.3f ms" % (k, rec, extra["single_query_latency_ms_p50"]))
         extra["batched_mfma"] = batched_path(tq, idx, Qrot, k, ids, scores, ex_ids, nr)
-        extra["filtered_T100"] = filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits, dev)
+        for T in (10, 100, 1000):
+            extra["filtered_T%d" % T] = filtered_path(tq, synth, cb, rot, X, Qrot, k, n, d, bits,
+                                                      dev, T=T)
         extra["filter_study_100k"] = filter_study(tq, synth, cb, rot, d, k, dev, stream)
         extra["tqplus"] = tqplus_study(tq, synth, cb, rot, X, Qrot, k, n, d, dev, stream)
-    if args.sweep:
+    if not args.no_extra and not args.no_sweep:
         extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
     del X
     torch.cuda.empty_cache()
@@ -480,7 +507,8 @@ def main() -> int:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(X_np, Q_np, d, bits, k, n)
-        log("oracle: %.3f queries/s at N=1M (scaled), %d cores" % (cpu["value"], cpu["cores"]))
+        log("oracle: %.3f queries/s at N=1M (scaled), %d cores; one thread %.3f queries/s (%s)"
+            % (cpu["value"], cpu["cores"], cpu["one_thread"]["value"], cpu["cpu_model"]))
 
     out = {
         "metric": METRIC,
