@@ -86,10 +86,19 @@ struct QInfo {
 // plus the float32 accumulation of d products in any order,
 //   gamma_d cmax16 (||q'||_1 + ||eps||_1 / alpha),  gamma_d = d u / (1 - d u),
 // u = 2^-24, and two float32 roundings when scaling (2^-23 of the same
-// magnitude).  The exact score (integer table, float conversion) is within
-// 7e-7 cmax ||q'||_1 of s_v <c, q'>.  The sum, times s_max and 1.1, is the
-// error before storage; the float16 storage of the approximate score adds
-// at most 2^-11 of its magnitude plus 2^-25 norm, accounted for where the
+// magnitude).  The exact score (the integer table of lut.h, d rows at
+// b = 4) differs from s_v <c, q'> by the table's rounding: each entry is
+// within 1/2 unit plus 2^-24 of its product, the integer sum is exact, and
+// its float conversion and the product with s_v add 2^-24 each.  The table
+// builder picks 2^sh > (2^31 - 1 - 2d) / (2 B'), B' = cmax tot (1 + 1e-5)
+// with tot its float sum of |q'_j| (within 1e-6 of ||q'||_1), so the d/2
+// units are below rho cmax ||q'||_1 in score units, rho = d (1 + 2e-5) /
+// (2^31 - 1 - 2d); with the 2^-24 terms the exact score is within
+// (rho + 4 * 2^-24) s_v cmax ||q'||_1 of s_v <c, q'> (cmax <= cmax16
+// (1 + 2^-10): float16 rounding moves a value by at most 2^-11 of it).
+// The sum of all terms times s_max is the error before storage (the factor
+// 1.1 is margin only); the float16 storage of the approximate score adds at
+// most 2^-11 of its magnitude plus 2^-25 norm, accounted for where the
 // certificate is checked.
 __global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const float *smax_p,
                             float cmax16, float dmax, _Float16 *__restrict__ q16,
@@ -148,8 +157,10 @@ __global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const fl
         const double u = ldexp(1.0, -24);
         const double gd = d * u / (1.0 - d * u);
         const double mag = (double)cmax16 * (s1 + se / alpha);
+        const double rho = d * (1.0 + 2e-5) / (2147483647.0 - 2.0 * d);
+        const double tab = (rho + 4 * u) * (double)cmax16 * (1.0 + ldexp(1.0, -10)) * s1;
         const double E = (double)dmax * s1 + (double)cmax16 * se / alpha + gd * mag +
-                         2 * ldexp(1.0, -23) * mag + 7e-7 * (double)cmax16 * s1;
+                         2 * ldexp(1.0, -23) * mag + tab;
         QInfo qi;
         qi.f = (float)(1.0 / ((double)alpha * norm));
         qi.norm = (float)norm;

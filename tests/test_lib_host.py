@@ -113,3 +113,17 @@ def test_device_calls_report_no_device():
     # argument errors are still reported first
     assert L.tq_search_workspace_size(idx._h, 4, 0, 0, ctypes.byref(b)) == _lib.TQ_EINVAL
     assert L.tq_search_workspace_size(idx._h, 4, 10, 9, ctypes.byref(b)) == _lib.TQ_EINVAL
+
+
+@pytest.mark.parametrize("d", [96, 160, 1568, 2080, 2112, 4096])
+def test_dimension_reading(d):
+    """d must be a multiple of 64 in [64, 2048]: multiples of 32 that are not
+    multiples of 64, and dimensions beyond 2048, are refused before any work
+    by both the codebook and the rotation."""
+    h = ctypes.c_void_p()
+    assert L.tq_build_codebook(d, 4, ctypes.byref(h)) == _lib.TQ_EINVAL
+    assert "multiple of 64" in L.tq_last_error().decode()
+    assert L.tq_rotation_create(d, 42, ctypes.byref(h)) == _lib.TQ_EINVAL
+    for ok in (64, 1536, 2048):
+        cb = tq.Codebook(ok, 4)
+        assert cb.cents.shape == (16,)
