@@ -25,8 +25,10 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        path = _build.LIB
-        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_build.SRC):
+        # TQ_ORACLE_LIBRARY: another build of tq_oracle.c (the sanitizer build)
+        path = os.environ.get("TQ_ORACLE_LIBRARY") or _build.LIB
+        if not os.environ.get("TQ_ORACLE_LIBRARY") and (
+                not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_build.SRC)):
             path = _build.build(force=True)
         lib = ctypes.CDLL(path)
         P = ctypes.c_void_p

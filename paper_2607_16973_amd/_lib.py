@@ -11,7 +11,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libtq.so")
+# TQ_LIBRARY names another build of the same sources (the host-sanitizer
+# build of sanitize.py); by default the in-tree libtq.so
+LIB_PATH = os.environ.get("TQ_LIBRARY") or os.path.join(HERE, "libtq.so")
 
 TQ_OK, TQ_EINVAL, TQ_ENOMEM, TQ_EDEVICE, TQ_EUNSUPPORTED = 0, -1, -2, -3, -4
 PATHS = {"auto": 0, "lut": 1, "mfma": 2}
