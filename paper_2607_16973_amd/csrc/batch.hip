@@ -30,10 +30,12 @@
 //     the single-query scan.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstdint>
 #include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "kernels.h"
@@ -46,6 +48,7 @@ namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float4v __attribute__((ext_vector_type(4)));
+typedef float float16v __attribute__((ext_vector_type(16)));
 
 constexpr int kTile = 32;          // queries per pass over the codes: two MFMA row tiles of 16
 constexpr int kCandMax = 512;      // candidates per query kept for exact rescoring (KC <= this)
@@ -971,6 +974,701 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
     }
 }
 
+// ============================================================ wide passes
+// Passes of 33 to 256 queries (QP = 64, 128 or 256 query slots) read the code
+// store once per pass and keep no score matrix:
+//  1. prep_kernel, then frag_kernel: the float16 queries in the A operand
+//     order of v_mfma_f32_32x32x16_f16.  Piece (c, f, l) (16 bytes) holds
+//     coordinates 32c + 16(f & 1) + 8(l >> 5) .. +7 of query
+//     32(f >> 1) + (l & 31), so the query part of a chunk is QP * 64
+//     contiguous bytes, and lane l of a wave reads fragment f (query tile
+//     f / 2, k-half f & 1) at offset (f * 64 + l) * 16.
+//  2. wide_scores_kernel, pilot launch: tiles of NG blocks (every pstride-th
+//     tile of the store, at most one per workgroup); every approximate score
+//     of their vectors is written, [query][pilot vector].
+//  3. pilot_select_kernel: per query, theta = the KC-th largest allowed
+//     pilot score (-inf when at most KC pilot vectors are allowed), and the
+//     allowed pilot vectors that reach it as candidates.  At least KC
+//     vectors of the store score theta or more.
+//  4. wide_scores_kernel, main launch: every other tile; a vector whose
+//     score reaches its query's theta (and whose tenant the query allows) is
+//     appended to the workgroup's list for that query.
+//  5. final_select_kernel: the KC best of the pilot's and the workgroups'
+//     candidates, and amin = the KC-th one's score.  A vector that is not
+//     taken scores below theta <= amin (never appended) or at most amin
+//     (behind the KC-th), which is the bound the certificate needs.
+//  6. rescore_kernel: exact scores, top k and certificate, as for tiles.
+// Work items of the score kernel are steps (tile, chunk): for each, the
+// workgroup stages one slab in LDS -- the chunk's query pieces and the
+// chunk of each of its NG blocks -- and its eight waves multiply them: wave
+// w takes block w % NG of the tile against query half w / NG (QW queries).
+// Slabs are loaded P steps ahead into registers and written to LDS one step
+// ahead (two LDS buffers, one barrier per step).
+constexpr int WD_THREADS = 512;
+constexpr int WD_WAVES = WD_THREADS / 64;
+constexpr int PS_THREADS = 1024;               // pilot_select_kernel, final_select_kernel
+constexpr int kPilotMax = 65536;               // pilot vectors per query (16-bit keys in 128 KiB of LDS)
+constexpr int kFinalMax = 16384;               // candidates a query's final selection gathers
+constexpr int kWideMaxQ = 256;
+constexpr int kWideMinChunks = 8;            // chunks per vector of a wide pass: more than its slabs ahead
+
+// Order-preserving map of float32 onto uint32; 0 marks an absent entry
+// (below every finite value and -inf).
+__device__ inline uint32_t ukey(float f) {
+    const uint32_t b = __float_as_uint(f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ inline float ukey_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+__global__ void frag_kernel(const _Float16 *__restrict__ q16, const QInfo *__restrict__ info,
+                            int nqt, int QP, int d, uint4 *__restrict__ qfrag,
+                            float *__restrict__ qf) {
+    const int64_t per_chunk = (int64_t)QP * 4;
+    const int64_t tot = (int64_t)(d / 32) * per_chunk;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < tot;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int c = (int)(e / per_chunk);
+        const int rem = (int)(e - c * per_chunk);
+        const int f = rem >> 6, l = rem & 63;   // fragment (query tile f / 2, k-half f & 1)
+        const int q = 32 * (f >> 1) + (l & 31);
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (q < nqt)
+            v = *reinterpret_cast<const uint4 *>(q16 + (int64_t)q * d + 32 * c + 16 * (f & 1) +
+                                                 8 * (l >> 5));
+        qfrag[e] = v;
+    }
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < QP;
+         q += (int64_t)gridDim.x * blockDim.x)
+        qf[q] = q < nqt ? info[q].f : 0.f;
+}
+
+struct WideParams {
+    const uint4 *codes;        // blocked store (b = 4)
+    const float *scales;
+    const uint4 *qfrag;        // [chunks][QP * 4] query pieces
+    const float *qf;           // [QP] score factor (0 for unused slots)
+    const float *cents;        // 16 levels
+    int64_t n, nblk, ntiles;   // tiles of NG blocks
+    int chunks, pstride, npil; // pilot tiles: i * pstride, i < npil
+    int pilot;                 // 1: pilot launch, 0: main launch
+    float *pil;                // pilot: [QP][npil * 64 NG] scores
+    const float *theta;        // main: [nqt] thresholds
+    const uint16_t *tenants;   // main, filtered
+    const uint64_t *allow;     // main: [nqt][W] allowlists, or null
+    int W, nqt;
+    float *cand_s;             // main: [grid][QP][S] appended scores and ids
+    int *cand_i;
+    int *cand_n;               // main: [grid][QP] appended per workgroup and query
+    int S;
+};
+
+constexpr int WD_NG = 4;                       // blocks per tile (wave w: block w % 4)
+constexpr int WD_NH = WD_WAVES / WD_NG;        // query halves (wave w: half w / 4)
+
+// Slab buffers in LDS per query-slot count.  A slab holds the chunk's QF
+// query pieces (pieces 0..QF-1) and the chunk of each of the tile's 4 blocks
+// (pieces QF..QF+3), 1 KiB each; piece i is loaded by wave i % 8 as its
+// (i / 8)-th load and stored at position (i % 8) DW + i / 8, so that each
+// wave's pieces are contiguous (one LDS base per wave and slab; DW = the
+// most loads a wave makes per slab).  NB buffers hold the slab being
+// multiplied, the next one (whose codes are turned into operands meanwhile)
+// and NB - 2 in flight.
+template <int QW>
+struct WideShape {
+    static constexpr int QP = QW * WD_NH;
+    static constexpr int QF = QP / 16;                 // query pieces of a slab
+    static constexpr int NI = QF + WD_NG;              // 1 KiB pieces of a slab
+    static constexpr int DW = (NI + WD_WAVES - 1) / WD_WAVES;
+    static constexpr int SU = WD_WAVES * DW * 64;      // uint4 of a slab
+    static constexpr int NB = QW == 128 ? 5 : QW == 64 ? 7 : 8;   // slab buffers
+    static constexpr int PD = NB - 1;                  // slabs requested ahead
+    static constexpr size_t lds = kTableBytes + (size_t)NB * SU * 16 + 2 * 1024 +
+                                  3 * (size_t)QP * 4;
+    // uint4 offset of piece i within a slab
+    static constexpr int pos(int i) { return ((i % WD_WAVES) * DW + i / WD_WAVES) * 64; }
+};
+
+// Loads 16 bytes per lane from global memory straight into LDS: lane l's
+// bytes go to LDS byte address lds_base + 16 l (lds_base wave-uniform).  The
+// compiler does not see these loads, so their completion is awaited with
+// explicit vector-memory counter waits before the barrier that publishes
+// the slab (a wait on the counter also covers any older access).
+__device__ inline void lds_dma16(const void *src, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(src) : "memory");
+}
+// Several such loads from one LDS base: set_lds_base, then lds_dma16_at<K>
+// with the lane's source address; load K lands at base + K KiB + 16 l (the
+// instruction offset moves both addresses, so it is taken off the source).
+// Setting the base once per group of loads matters: a load must read the
+// base before it may be changed again.
+__device__ inline void set_lds_base(uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" :: "s"(__builtin_amdgcn_readfirstlane(lds_base))
+                 : "memory");
+}
+template <int K, bool NT>
+__device__ inline void lds_dma16_at(const void *src) {
+    const char *s = static_cast<const char *>(src) - K * 1024;
+    if constexpr (NT)
+        asm volatile("global_load_lds_dwordx4 %0, off offset:%1 nt" :: "v"(s), "i"(K * 1024) : "memory");
+    else
+        asm volatile("global_load_lds_dwordx4 %0, off offset:%1" :: "v"(s), "i"(K * 1024) : "memory");
+}
+// s_waitcnt until at most N vector-memory operations of this wave are
+// outstanding (other counters unconstrained).
+template <int N>
+__device__ inline void wait_vmem() {
+    static_assert(N >= 0 && N < 64, "vector-memory counter range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Barrier that orders LDS accesses only: outstanding global stores of the
+// epilogue (candidates for a later kernel) need not complete here.
+__device__ inline void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int QW>
+__global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
+    using WS = WideShape<QW>;
+    constexpr int QP = WS::QP, QF = WS::QF, NI = WS::NI, SU = WS::SU, NB = WS::NB, PD = WS::PD;
+    static_assert(WS::DW * 1024 <= 4096, "a wave's loads of a slab within one instruction-offset span");
+    constexpr int NG = WD_NG;
+    constexpr int QT = QW / 32;                // 32-query tiles of a wave
+    constexpr int QU = QF * 64;                // uint4 of a slab's query part
+    // 1 KiB loads of a slab per wave: load i goes to wave i % 8
+    constexpr int DHI = (NI + WD_WAVES - 1) / WD_WAVES, NHI = NI - (DHI - 1) * WD_WAVES;
+    static_assert(PD >= 2, "the next slab must be present a step ahead");
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    uint32_t *T = reinterpret_cast<uint32_t *>(smem);                 // byte table x 32
+    uint4 *slab = reinterpret_cast<uint4 *>(smem + kTableBytes);      // [NB][SU]
+    float *sclv = reinterpret_cast<float *>(slab + NB * SU);           // [2][256] tile scales
+    float *fq = sclv + 512;                                            // [QP]
+    float *th = fq + QP;                                               // [QP]
+    int *cnt = reinterpret_cast<int *>(th + QP);                       // [QP]
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
+    const int g = wave % NG, h = wave / NG;
+    const int G = gridDim.x, wg = blockIdx.x;
+    const int CH = p.chunks;
+    const int64_t nt_all = p.pilot ? p.npil : p.ntiles - p.npil;
+    const int64_t my_tiles = nt_all > wg ? (nt_all - wg + G - 1) / G : 0;
+    // the i-th tile of this workgroup
+    auto tile_of = [&](int64_t i) -> int64_t {
+        const int64_t j = wg + i * G;
+        if (p.pilot) return j * p.pstride;
+        const int64_t r = p.pstride - 1;   // >= 1 whenever there are main tiles
+        return (j / r) * p.pstride + 1 + j % r;
+    };
+
+    for (int e = tid; e < 256 * 32; e += WD_THREADS) {
+        const int v = e >> 5;
+        const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v & 15]);
+        const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v >> 4]);
+        T[e] = lo | (hi << 16);
+    }
+    for (int q = tid; q < QP; q += WD_THREADS) {
+        fq[q] = p.qf[q];
+        th[q] = (!p.pilot && q < p.nqt) ? p.theta[q] : INFINITY;
+        cnt[q] = 0;
+    }
+    if (my_tiles > 0) {
+        const uint32_t lb = (uint32_t)(lane & 31) * 4;
+        const uint32_t slab_lds = (uint32_t)(uintptr_t)slab;
+        const uint32_t scl_lds = (uint32_t)(uintptr_t)sclv;
+        // this wave's loads of a slab: DHI of them for waves below NHI
+        const bool hi_wave = wave < NHI;
+        // next slab to request: tile ordinal, tile, chunk, buffer
+        int64_t ld_i = 0, ld_tile = tile_of(0);
+        int ld_c = 0, ld_b = 0;
+        // the j-th load of this wave for the next slab to request (piece
+        // i = 8j + wave, stored at this wave's base + j KiB); request_base
+        // first, once per slab
+        auto request_base = [&]() {
+            set_lds_base(slab_lds + (uint32_t)ld_b * (SU * 16) + (uint32_t)(wave * WS::DW) * 1024);
+        };
+        auto request_part = [&](auto J) {
+            constexpr int j = decltype(J)::value;
+            const int i = j * WD_WAVES + wave;
+            if (i < NI) {   // uniform
+                if (i < QF) {
+                    lds_dma16_at<j, false>(p.qfrag + (int64_t)ld_c * QU + i * 64 + lane);
+                } else {
+                    int64_t b = ld_tile * NG + (i - QF);
+                    b = b < p.nblk ? b : p.nblk - 1;
+                    lds_dma16_at<j, true>(p.codes + (b * CH + ld_c) * 64 + lane);
+                }
+            }
+        };
+        auto request_done = [&]() {
+            if (ld_c == 0 && wave == WD_WAVES - 1) {
+                // the tile's 256 scales (4 per lane, block clamped like the codes)
+                int64_t v = ld_tile * 256 + 4 * lane;
+                if (v >= p.nblk * 64) v -= (ld_tile * NG + lane / 16 - (p.nblk - 1)) * 64;
+                lds_dma16(p.scales + v, scl_lds + (uint32_t)(ld_i & 1) * 1024);
+            }
+            ld_b = ld_b + 1 == NB ? 0 : ld_b + 1;
+            // past the last step the last tile's slabs are requested again (unused)
+            if (++ld_c == CH) {
+                ld_c = 0;
+                if (ld_i + 1 < my_tiles) ld_tile = tile_of(++ld_i);
+            }
+        };
+        auto request = [&]() {
+            request_base();
+            request_part(std::integral_constant<int, 0>());
+            if constexpr (DHI > 1) request_part(std::integral_constant<int, 1>());
+            if constexpr (DHI > 2) request_part(std::integral_constant<int, 2>());
+            static_assert(DHI <= 3, "at most three loads per wave and slab");
+            request_done();
+        };
+        // until the oldest requested slab but `ahead` has landed
+        auto wait_slabs = [&](auto ahead) {
+            constexpr int A = decltype(ahead)::value;
+            if (hi_wave) wait_vmem<A * DHI>();
+            else wait_vmem<A * (DHI - 1)>();
+        };
+        // B operands of a chunk: b[2m + ks] for vectors 32m .. 32m + 31 of the
+        // wave's block and coordinates 16ks .. 16ks + 15 of the chunk (lane l:
+        // vector 32m + (l & 31), coordinates 16ks + 8(l >> 5) .. +7).  Lane v
+        // holds words 0..3 of vector v; permlane32_swap(w0, w1) leaves word 0
+        // of vectors 0..31 in lanes 0..31 and word 1 of the same vectors in
+        // lanes 32..63 (first result), and words 0, 1 of vectors 32..63 the
+        // same way (second); likewise (w2, w3) for the second k-half.
+        half8 bcur[4];
+        auto operands = [&](const uint4 *sb, half8 (&b)[4]) {
+            const uint4 w = sb[WS::pos(QF + g) + lane];
+            const auto k0 = __builtin_amdgcn_permlane32_swap(w.x, w.y, false, false);
+            const auto k1 = __builtin_amdgcn_permlane32_swap(w.z, w.w, false, false);
+            b[0] = dequant8(k0[0], lb);   // vectors 0..31, k-half 0
+            b[1] = dequant8(k1[0], lb);   // vectors 0..31, k-half 1
+            b[2] = dequant8(k0[1], lb);   // vectors 32..63, k-half 0
+            b[3] = dequant8(k1[1], lb);   // vectors 32..63, k-half 1
+        };
+#pragma unroll 1
+        for (int x = 0; x < PD; ++x) request();
+        wait_slabs(std::integral_constant<int, PD - 1>());
+        lds_barrier();
+        operands(slab, bcur);
+
+        float16v acc[QT][2];
+        auto clear_acc = [&]() {
+#pragma unroll
+            for (int t = 0; t < QT; ++t)
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[t][m][e] = 0.f;
+        };
+        clear_acc();
+        int64_t ti = 0;       // tile ordinal of the current step
+        int64_t tile = tile_of(0);
+        int buf = 0;          // buffer of the current step's slab
+        // lane holds vectors 32m + (lane & 31) of its block and, in element e
+        // of tile t, query h QW + 32t + 8(e >> 2) + 4(lane >> 5) + (e & 3)
+        auto epilogue = [&]() {
+            // hq is made opaque so that the per-query offsets below are
+            // formed here, once per tile, rather than hoisted out of the step
+            // loop into registers held across it
+            int hq = h * QW + 4 * (lane >> 5);
+            asm volatile("" : "+v"(hq));
+            const float *ts = sclv + (ti & 1) * 256 + g * 64 + (lane & 31);
+            const float scl[2] = {ts[0], ts[32]};
+            const int64_t vb = (tile * NG + g) * 64 + (lane & 31);
+            const bool vin[2] = {vb < p.n, vb + 32 < p.n};
+            if (p.pilot) {
+                const int64_t prow = (int64_t)p.npil * 64 * NG;
+                const int64_t pcol = (wg + ti * G) * 64 * NG + g * 64 + (lane & 31);
+#pragma unroll
+                for (int t = 0; t < QT; ++t)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int q = hq + 32 * t + 8 * (e >> 2) + (e & 3);
+                        const float f = fq[q];
+#pragma unroll
+                        for (int m = 0; m < 2; ++m)
+                            p.pil[q * prow + pcol + 32 * m] = vin[m] ? acc[t][m][e] * scl[m] * f : -INFINITY;
+                    }
+            } else {
+                // which entries reach their query's threshold, without
+                // branches (bit 2e + m of hit[t]) ...
+                uint32_t hit[QT];
+#pragma unroll
+                for (int t = 0; t < QT; ++t) {
+                    float fr[16], tr[16];   // the tile row's factors and thresholds, read together
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int q = hq + 32 * t + 8 * (e >> 2) + (e & 3);
+                        fr[e] = fq[q];
+                        tr[e] = th[q];
+                    }
+                    uint32_t hb = 0u;
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        hb |= (vin[0] && acc[t][0][e] * scl[0] * fr[e] >= tr[e]) ? 1u << (2 * e) : 0u;
+                        hb |= (vin[1] && acc[t][1][e] * scl[1] * fr[e] >= tr[e]) ? 2u << (2 * e) : 0u;
+                    }
+                    hit[t] = hb;
+                }
+                // ... then append those (rare)
+#pragma unroll
+                for (int t = 0; t < QT; ++t) {
+                    if (!__ballot(hit[t] != 0u)) continue;
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const uint32_t two = (hit[t] >> (2 * e)) & 3u;
+                        if (!__ballot(two != 0u)) continue;
+                        const int q = hq + 32 * t + 8 * (e >> 2) + (e & 3);
+                        float f = fq[q];
+                        // opaque: the products are formed again here rather
+                        // than kept live from the test above
+                        asm volatile("" : "+v"(f));
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) {
+                            if ((two >> m) & 1u) {
+                                const float val = acc[t][m][e] * scl[m] * f;
+                                const int64_t v = vb + 32 * m;
+                                bool ok = true;
+                                if (p.allow) {
+                                    const int tn = p.tenants[v];
+                                    ok = (tn >> 6) < p.W &&
+                                         ((p.allow[(int64_t)q * p.W + (tn >> 6)] >> (tn & 63)) & 1ull);
+                                }
+                                if (ok) {
+                                    const int slot = atomicAdd(&cnt[q], 1);
+                                    if (slot < p.S) {
+                                        const int64_t o = ((int64_t)wg * QP + q) * p.S + slot;
+                                        p.cand_s[o] = val;
+                                        p.cand_i[o] = (int)v;
+                                    }
+                                }
+                            }
+                        }
+                    }
+                }
+            }
+            clear_acc();
+        };
+        for (;;) {
+            for (int c = 0; c < CH; ++c) {
+                // the next step's slab has landed (own loads), then everyone's;
+                // every wave is done with the buffer the new request overwrites
+                wait_slabs(std::integral_constant<int, PD - 2>());
+                lds_barrier();
+                // the products of slab s in QT groups; the code word of slab
+                // s + 1 turned into the next B operands, and this step's
+                // loads, are issued between the groups so that they overlap
+                // the matrix cores' work instead of following it
+                const uint4 *sb = slab + buf * SU;
+                buf = buf + 1 == NB ? 0 : buf + 1;
+                const half8 *qa = reinterpret_cast<const half8 *>(sb) + lane;
+                const uint4 wn = slab[buf * SU + WS::pos(QF + g) + lane];
+                half8 bnext[4];
+                // k-half outer, so that the two products into one accumulator
+                // are 2 QT products apart (a product waits for the previous
+                // one into the same accumulator to finish)
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                    for (int t = 0; t < QT; ++t) {
+                        const half8 a = qa[WS::pos(h * 2 * QT + 2 * t + ks)];
+                        acc[t][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bcur[ks], acc[t][0], 0, 0, 0);
+                        acc[t][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bcur[2 + ks], acc[t][1], 0, 0, 0);
+                        const int grp = ks * QT + t;   // groups of two products
+                        if (grp == 0) {
+                            const auto k0 = __builtin_amdgcn_permlane32_swap(wn.x, wn.y, false, false);
+                            const auto k1 = __builtin_amdgcn_permlane32_swap(wn.z, wn.w, false, false);
+                            bnext[0] = dequant8(k0[0], lb);
+                            bnext[1] = dequant8(k1[0], lb);
+                            bnext[2] = dequant8(k0[1], lb);
+                            bnext[3] = dequant8(k1[1], lb);
+                        }
+                        if (grp == 1) {
+                            request_base();
+                            request_part(std::integral_constant<int, 0>());
+                        }
+                        if constexpr (DHI > 1)
+                            if (grp == 2) request_part(std::integral_constant<int, 1>());
+                        if constexpr (DHI > 2)
+                            if (grp == 3) request_part(std::integral_constant<int, 2>());
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                // loads that found no group after them
+                if constexpr (DHI > 1 && 2 * QT <= 2) request_part(std::integral_constant<int, 1>());
+                if constexpr (DHI > 2 && 2 * QT <= 3) request_part(std::integral_constant<int, 2>());
+                request_done();
+#pragma unroll
+                for (int m = 0; m < 4; ++m) bcur[m] = bnext[m];
+            }
+            epilogue();
+            if (++ti == my_tiles) break;
+            tile = tile_of(ti);
+        }
+    }
+    if (!p.pilot) {
+        __syncthreads();
+        for (int q = tid; q < QP; q += WD_THREADS) p.cand_n[(int64_t)wg * QP + q] = cnt[q];
+    }
+}
+
+// K-th largest of the BITS-bit keys visited by `each` (K >= 1, at most the
+// number of non-zero keys; zero keys are absent): 8-bit radix passes with
+// LDS histograms.  Returns the key and sets n_above to the number of
+// keys above it.  Called by every thread of the workgroup.
+template <int BITS, class Each>
+__device__ uint32_t radix_kth(Each each, int K, int *hist, int *sh, int &n_above) {
+    static_assert(BITS % 8 == 0, "8-bit digits");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int *hc = hist + (lane & 3) * kHistStride;
+    uint32_t prefix = 0, pmask = 0;
+    int above = 0;
+    for (int pass = 0; pass < BITS / 8; ++pass) {
+        const int shift = BITS - 8 - 8 * pass;
+        for (int i = tid; i < kHistCopies * kHistStride; i += blockDim.x) hist[i] = 0;
+        __syncthreads();
+        // the lanes of a wave that share the first active lane's digit add
+        // their count once (the high digits of one query's scores are mostly
+        // equal, and their single-lane atomics would serialise); the others
+        // add one each
+        each([&](uint32_t k) {
+            const bool act = k != 0u && (k & pmask) == prefix;
+            const uint32_t dg = (k >> shift) & 255u;
+            const uint64_t live = __ballot(act);
+            if (live) {
+                const int leader = __builtin_ctzll(live);
+                const uint32_t dl = __builtin_amdgcn_readlane(dg, leader);
+                const bool same = act && dg == dl;
+                const uint64_t sm = __ballot(same);
+                if (lane == leader) atomicAdd(&hc[dl], (int)__popcll(sm));
+                else if (act && !same) atomicAdd(&hc[dg], 1);
+            }
+        });
+        __syncthreads();
+        if (wave == 0) find_digit(hist, K - above, sh);
+        __syncthreads();
+        prefix |= (uint32_t)sh[0] << shift;
+        pmask |= 255u << shift;
+        above += sh[1];
+        __syncthreads();   // sh is read before it is written again
+    }
+    n_above = above;
+    return prefix;
+}
+
+struct PilotParams {
+    const float *pil;          // [QP][npv]
+    int64_t npv;               // pilot vectors per query (npil * 64 WD_NG)
+    int pstride;
+    int64_t n;
+    const uint16_t *tenants;
+    const uint64_t *allow;     // [nqt][W] or null
+    int W, KC, PCM;
+    float *theta;              // [nqt]
+    int *pc_n;                 // [nqt] pilot candidates (may exceed PCM: overflow)
+    int *pc_i;                 // [nqt][PCM]
+    float *pc_s;
+};
+
+// One workgroup per query.  The selection runs on 16-bit keys, the top half
+// of the order-preserving key of each allowed pilot score, held in LDS: the
+// KC-th largest such key kt gives theta = the smallest float whose key starts
+// with kt, so at least KC allowed pilot vectors score theta or more, and a
+// pilot vector reaches theta exactly when its 16-bit key reaches kt.
+__global__ __launch_bounds__(PS_THREADS) void pilot_select_kernel(PilotParams p) {
+    constexpr int TV = 64 * WD_NG;                 // vectors per pilot tile
+    extern __shared__ __attribute__((aligned(16))) uint16_t k16[];   // [npv], 0: absent
+    __shared__ int hist[kHistCopies * kHistStride];
+    __shared__ int sh[8];
+    const int q = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    const int npv = (int)p.npv;
+    const float *row = p.pil + (int64_t)q * p.npv;
+    const uint64_t *arow = p.allow ? p.allow + (int64_t)q * p.W : nullptr;
+    auto vec_of = [&](int e) -> int64_t { return (int64_t)(e / TV) * p.pstride * TV + e % TV; };
+    if (tid == 0) {
+        sh[4] = 0;
+        sh[5] = 0;
+    }
+    __shared__ uint64_t allow_s[64];
+    if (arow)
+        for (int w = tid; w < p.W; w += PS_THREADS) allow_s[w] = arow[w];
+    __syncthreads();
+    int cnt = 0;
+    // rounds of 16 loads per thread, all issued before any is used
+    constexpr int R = 16;
+    for (int e0 = 0; e0 < npv; e0 += R * PS_THREADS) {
+        float val[R];
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const int e = e0 + tid + u * PS_THREADS;
+            val[u] = row[e < npv ? e : 0];
+        }
+        int tn[R];
+        if (arow) {
+#pragma unroll
+            for (int u = 0; u < R; ++u) {
+                const int e = e0 + tid + u * PS_THREADS;
+                tn[u] = p.tenants[vec_of(e < npv ? e : 0)];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const int e = e0 + tid + u * PS_THREADS;
+            if (e < npv) {
+                bool ok = val[u] > -INFINITY;
+                if (arow)
+                    ok = ok && (tn[u] >> 6) < p.W && ((allow_s[tn[u] >> 6] >> (tn[u] & 63)) & 1ull);
+                k16[e] = ok ? (uint16_t)(ukey(val[u]) >> 16) : (uint16_t)0;   // a finite key's top half is >= 0x80
+                cnt += ok;
+            }
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    __syncthreads();
+    if (lane == 0) atomicAdd(&sh[5], cnt);
+    __syncthreads();
+    const int allowed = sh[5];
+    uint32_t thk = 1u;   // every present key
+    if (allowed > p.KC) {
+        int n_above;
+        thk = radix_kth<16>([&](auto fn) {
+            for (int e = tid; e < npv; e += PS_THREADS) fn((uint32_t)k16[e]);
+        }, p.KC, hist, sh, n_above);
+    }
+    if (tid == 0) p.theta[q] = allowed > p.KC ? ukey_value(thk << 16) : -INFINITY;
+    for (int e = tid; e < npv; e += PS_THREADS) {
+        const uint32_t k = k16[e];
+        if (k != 0u && k >= thk) {
+            const int pos = atomicAdd(&sh[4], 1);
+            if (pos < p.PCM) {
+                p.pc_i[(int64_t)q * p.PCM + pos] = (int)vec_of(e);
+                p.pc_s[(int64_t)q * p.PCM + pos] = row[e];
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0) p.pc_n[q] = sh[4];
+}
+
+struct FinalParams {
+    const float *theta;
+    const int *pc_n;
+    const int *pc_i;
+    const float *pc_s;
+    int PCM;
+    const float *cand_s;       // [G][QP][S]
+    const int *cand_i;
+    const int *cand_n;         // [G][QP]
+    int G, QP, S, KC;
+    int *top_i;                // [nqt][KC] (INT_MAX: none)
+    float *amin;
+    int *state;
+};
+
+// One workgroup per query: the query's candidates gathered in LDS, then the
+// KC best.
+__global__ __launch_bounds__(PS_THREADS) void final_select_kernel(FinalParams p) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    uint32_t *ck = reinterpret_cast<uint32_t *>(smem);        // [kFinalMax] keys
+    int *cv = reinterpret_cast<int *>(ck + kFinalMax);         // [kFinalMax] ids
+    __shared__ int hist[kHistCopies * kHistStride];
+    __shared__ int sh[8];
+    const int q = blockIdx.x, tid = threadIdx.x;
+    int *out = p.top_i + (int64_t)q * p.KC;
+    __shared__ int goff[1025];                  // exclusive offsets of the workgroup lists
+    __shared__ int wsum[PS_THREADS / 64];
+    const int lane = tid & 63, wave = tid >> 6;
+    const int n0 = p.pc_n[q];
+    const int base = n0 < p.PCM ? n0 : p.PCM;
+    if (tid == 0) {
+        sh[3] = n0 > p.PCM;         // overflow
+        sh[4] = 0;
+        sh[5] = 0;
+    }
+    __syncthreads();
+    // the G list lengths (G <= PS_THREADS), an exclusive scan over them
+    int c = 0;
+    if (tid < p.G) {
+        c = p.cand_n[(int64_t)tid * p.QP + q];
+        if (c > p.S) sh[3] = 1;
+    }
+    int incl = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += t;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    goff[tid] = base + before + incl - c;
+    if (tid == PS_THREADS - 1) goff[PS_THREADS] = base + before + incl;
+    __syncthreads();
+    const int ng = p.G < PS_THREADS ? p.G : PS_THREADS;
+    const int total_all = goff[ng];
+    for (int e = tid; e < base && e < kFinalMax; e += PS_THREADS) {
+        ck[e] = ukey(p.pc_s[(int64_t)q * p.PCM + e]);
+        cv[e] = p.pc_i[(int64_t)q * p.PCM + e];
+    }
+    if (!sh[3] && total_all <= kFinalMax) {
+        for (int e = base + tid; e < total_all; e += PS_THREADS) {
+            int lo = 0, hi = ng - 1;   // last list whose offset is <= e
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (goff[mid] <= e) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t src = ((int64_t)lo * p.QP + q) * p.S + (e - goff[lo]);
+            ck[e] = ukey(p.cand_s[src]);
+            cv[e] = p.cand_i[src];
+        }
+    }
+    if (tid == 0) sh[2] = total_all;
+    __syncthreads();
+    const int tot = sh[2];
+    const float theta = p.theta[q];
+    if (sh[3] || tot > kFinalMax) {
+        for (int i = tid; i < p.KC; i += PS_THREADS) out[i] = INT_MAX;
+        if (tid == 0) {
+            p.amin[q] = INFINITY;
+            p.state[q] = kSelOverflow;
+        }
+        return;
+    }
+    if (tot <= p.KC) {
+        // every candidate kept: all allowed vectors when theta = -inf, else
+        // every vector below theta is outside
+        for (int i = tid; i < p.KC; i += PS_THREADS) out[i] = i < tot ? cv[i] : INT_MAX;
+        if (tid == 0) {
+            p.amin[q] = theta;
+            p.state[q] = theta == -INFINITY ? kSelAll : kSelBound;
+        }
+        return;
+    }
+    int n_gt;
+    const uint32_t thk = radix_kth<32>([&](auto fn) {
+        for (int i = tid; i < tot; i += PS_THREADS) fn(ck[i]);
+    }, p.KC, hist, sh, n_gt);
+    const int need_eq = p.KC - n_gt;   // keys equal to thk to take (>= 1)
+    for (int i = tid; i < tot; i += PS_THREADS) {
+        const uint32_t k = ck[i];
+        if (k > thk) {
+            out[atomicAdd(&sh[4], 1)] = cv[i];
+        } else if (k == thk) {
+            const int e = atomicAdd(&sh[5], 1);
+            if (e < need_eq) out[n_gt + e] = cv[i];
+        }
+    }
+    if (tid == 0) {
+        p.amin[q] = ukey_value(thk);
+        p.state[q] = kSelBound;
+    }
+}
+
 // ------------------------------------------------------ fallback helpers
 // Global bounds are kept one 128-byte line apart (kBoundStride ints): every
 // wave of a query's selection reads and raises its query's bound, and bounds
@@ -1048,7 +1746,39 @@ void with_slots(int KC, Fn fn) {
 struct BatchLayout {
     size_t q16, info, approx, bmax, cand_s, cand_i, top_i, amin, state, gbound, flags, rows, qc,
         allow_c, ids_c, scores_c, lut, total;
+    // wide passes
+    size_t w_q16, w_info, w_qfrag, w_qf, w_pil, w_theta, w_pcn, w_pci, w_pcs, w_cs, w_ci, w_cn,
+        w_top, w_amin, w_state;
 };
+
+// Geometry of a wide pass with NG blocks per tile.
+struct WideGeom {
+    int NG, tilev, pstride, npil, S;
+    int64_t ntiles, nmain;
+};
+
+WideGeom wide_geom(const ScanShape &s, int NG, int grid, int KC) {
+    WideGeom w{};
+    w.NG = NG;
+    w.tilev = 64 * NG;
+    w.ntiles = (s.nblk + NG - 1) / NG;
+    // pilot tiles: at most one per workgroup, their scores within kPilotMax per query
+    const int64_t cap = std::min<int64_t>(grid, kPilotMax / w.tilev);
+    w.pstride = (int)((w.ntiles + cap - 1) / cap);
+    w.npil = (int)((w.ntiles + w.pstride - 1) / w.pstride);
+    w.nmain = w.ntiles - w.npil;
+    // theta is about the (KC ntiles / npil)-th score of the store, so a
+    // workgroup appends about KC nmain / (npil grid) vectors per query
+    const double per = (double)KC * (double)w.nmain / ((double)w.npil * grid);
+    int S = (int)std::ceil(2.0 * per + 16.0);
+    S = (S + 7) / 8 * 8;
+    w.S = std::min(std::max(S, 16), 512);
+    return w;
+}
+
+// Query slots of a wide pass of nqt > kTile queries.
+int wide_slots(int nqt) { return nqt <= 64 ? 64 : nqt <= 128 ? 128 : 256; }
+
 
 // Row length of the approximate-score matrix: whole 512-vector select units.
 int64_t approx_row(const ScanShape &s) { return (s.nblk * 64 + 511) / 512 * 512; }
@@ -1091,8 +1821,56 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
     o += align256((size_t)nq * k * 4);
     L.lut = o;
     o += lut_search_workspace_bytes(s, nq, k, grid);
+    if (nq > kTile && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
+        const int KC = batch_candidates(k), PCM = 2 * KC;
+        const int QP = wide_slots((int)std::min<int64_t>(nq, kWideMaxQ));
+        const WideGeom w = wide_geom(s, WD_NG, grid, KC);
+        auto take = [&](size_t bytes) {
+            const size_t at = o;
+            o += align256(bytes);
+            return at;
+        };
+        L.w_q16 = take((size_t)QP * s.d * 2);
+        L.w_info = take((size_t)QP * sizeof(QInfo));
+        L.w_qfrag = take((size_t)QP * s.d * 2);
+        L.w_qf = take((size_t)QP * 4);
+        L.w_pil = take((size_t)QP * w.npil * w.tilev * 4);
+        L.w_theta = take((size_t)QP * 4);
+        L.w_pcn = take((size_t)QP * 4);
+        L.w_pci = take((size_t)QP * PCM * 4);
+        L.w_pcs = take((size_t)QP * PCM * 4);
+        L.w_cs = take((size_t)grid * QP * w.S * 4);
+        L.w_ci = take((size_t)grid * QP * w.S * 4);
+        L.w_cn = take((size_t)grid * QP * 4);
+        L.w_top = take((size_t)QP * KC * 4);
+        L.w_amin = take((size_t)QP * 4);
+        L.w_state = take((size_t)QP * 4);
+    }
     L.total = o + 256;
     return L;
+}
+
+// Launches wide_scores_kernel for a pass of QP query slots (QP / 2 queries
+// per wave).
+hipError_t launch_wide_scores(int QP, const WideParams &wp, int grid, hipStream_t stream) {
+    static bool attr[3] = {false, false, false};
+    hipError_t err = hipSuccess;
+    auto go = [&](int slot, auto kern, size_t lds) {
+        if (!attr[slot]) {
+            err = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      (int)lds);
+            if (err != hipSuccess) return;
+            attr[slot] = true;
+        }
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(WD_THREADS), lds, stream, wp);
+        err = hipGetLastError();
+    };
+    switch (QP) {
+    case 64: go(0, wide_scores_kernel<32>, WideShape<32>::lds); break;
+    case 128: go(1, wide_scores_kernel<64>, WideShape<64>::lds); break;
+    default: go(2, wide_scores_kernel<128>, WideShape<128>::lds); break;
+    }
+    return err;
 }
 
 }  // namespace
@@ -1153,11 +1931,138 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
                 e = hipFuncSetAttribute((const void *)rescore_kernel<decltype(sc)::value>,
                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
             });
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)final_select_kernel,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)(kFinalMax * 8));
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)pilot_select_kernel,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, kPilotMax * 2);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    for (int64_t q0 = 0; q0 < nq; q0 += kTile) {
-        const int nqt = (int)((nq - q0) < kTile ? (nq - q0) : kTile);
+    auto rescore = [&](int64_t q0, int nqt, const int *ti, const float *am, const int *st,
+                       const QInfo *qi) {
+        RescoreParams rp{};
+        rp.codes = reinterpret_cast<const uint4 *>(blocked);
+        rp.scales = scales;
+        rp.qrot = Qrot + q0 * s.d;
+        rp.cents = cents32;
+        rp.top_i = ti;
+        rp.amin = am;
+        rp.state = st;
+        rp.info = qi;
+        rp.ids = ids + q0 * k;
+        rp.scores = scores + q0 * k;
+        rp.flags = flags + q0;
+        rp.d = s.d;
+        rp.bits = s.bits;
+        rp.chunks = s.chunks;
+        rp.lut_words = s.chunks * 512;
+        rp.k = k;
+        with_slots(KC, [&](auto sc) {
+            constexpr int S = decltype(sc)::value;
+            hipLaunchKernelGGL(rescore_kernel<S>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream,
+                               rp);
+        });
+    };
+    for (int64_t q0 = 0; q0 < nq;) {
+        if (nq - q0 > kTile && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
+            // a wide pass of up to kWideMaxQ queries
+            const int nqt = (int)std::min<int64_t>(nq - q0, kWideMaxQ);
+            const int QP = wide_slots(nqt);
+            const int PCM = 2 * KC;
+            const WideGeom w = wide_geom(s, WD_NG, grid, KC);
+            _Float16 *wq16 = reinterpret_cast<_Float16 *>(w8 + L.w_q16);
+            QInfo *winfo = reinterpret_cast<QInfo *>(w8 + L.w_info);
+            uint4 *wqfrag = reinterpret_cast<uint4 *>(w8 + L.w_qfrag);
+            float *wqf = reinterpret_cast<float *>(w8 + L.w_qf);
+            float *wpil = reinterpret_cast<float *>(w8 + L.w_pil);
+            float *wtheta = reinterpret_cast<float *>(w8 + L.w_theta);
+            int *wpcn = reinterpret_cast<int *>(w8 + L.w_pcn);
+            int *wpci = reinterpret_cast<int *>(w8 + L.w_pci);
+            float *wpcs = reinterpret_cast<float *>(w8 + L.w_pcs);
+            float *wcs = reinterpret_cast<float *>(w8 + L.w_cs);
+            int *wci = reinterpret_cast<int *>(w8 + L.w_ci);
+            int *wcn = reinterpret_cast<int *>(w8 + L.w_cn);
+            int *wtop = reinterpret_cast<int *>(w8 + L.w_top);
+            float *wamin = reinterpret_cast<float *>(w8 + L.w_amin);
+            int *wstate = reinterpret_cast<int *>(w8 + L.w_state);
+            const uint64_t *allow_p = allow ? allow + q0 * s.W : nullptr;
+            hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream,
+                               Qrot + q0 * s.d, nqt, s.d, smax, cmax16, dmax, wq16, winfo);
+            const int64_t fr = (int64_t)(s.d / 32) * QP * 4;
+            hipLaunchKernelGGL(frag_kernel, dim3((int)std::min<int64_t>((fr + 255) / 256, 1024)),
+                               dim3(256), 0, stream, wq16, winfo, nqt, QP, s.d, wqfrag, wqf);
+            WideParams wp{};
+            wp.codes = reinterpret_cast<const uint4 *>(blocked);
+            wp.scales = scales;
+            wp.qfrag = wqfrag;
+            wp.qf = wqf;
+            wp.cents = cents32;
+            wp.n = s.n;
+            wp.nblk = s.nblk;
+            wp.ntiles = w.ntiles;
+            wp.chunks = s.chunks;
+            wp.pstride = w.pstride;
+            wp.npil = w.npil;
+            wp.pil = wpil;
+            wp.theta = wtheta;
+            wp.tenants = tenants;
+            wp.allow = allow_p;
+            wp.W = s.W;
+            wp.nqt = nqt;
+            wp.cand_s = wcs;
+            wp.cand_i = wci;
+            wp.cand_n = wcn;
+            wp.S = w.S;
+            wp.pilot = 1;
+            hipError_t e = launch_wide_scores(QP, wp, grid, stream);
+            if (e != hipSuccess) return e;
+            PilotParams pp{};
+            pp.pil = wpil;
+            pp.npv = (int64_t)w.npil * w.tilev;
+            pp.pstride = w.pstride;
+            pp.n = s.n;
+            pp.tenants = tenants;
+            pp.allow = allow_p;
+            pp.W = s.W;
+            pp.KC = KC;
+            pp.PCM = PCM;
+            pp.theta = wtheta;
+            pp.pc_n = wpcn;
+            pp.pc_i = wpci;
+            pp.pc_s = wpcs;
+            hipLaunchKernelGGL(pilot_select_kernel, dim3(nqt), dim3(PS_THREADS), (size_t)pp.npv * 2, stream,
+                               pp);
+            wp.pilot = 0;
+            e = launch_wide_scores(QP, wp, grid, stream);
+            if (e != hipSuccess) return e;
+            FinalParams fp{};
+            fp.theta = wtheta;
+            fp.pc_n = wpcn;
+            fp.pc_i = wpci;
+            fp.pc_s = wpcs;
+            fp.PCM = PCM;
+            fp.cand_s = wcs;
+            fp.cand_i = wci;
+            fp.cand_n = wcn;
+            fp.G = grid;
+            fp.QP = QP;
+            fp.S = w.S;
+            fp.KC = KC;
+            fp.top_i = wtop;
+            fp.amin = wamin;
+            fp.state = wstate;
+            hipLaunchKernelGGL(final_select_kernel, dim3(nqt), dim3(PS_THREADS),
+                               (size_t)kFinalMax * 8, stream, fp);
+            rescore(q0, nqt, wtop, wamin, wstate, winfo);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            q0 += nqt;
+            continue;
+        }
+        const int nqt = (int)(nq - q0);
         hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream, Qrot + q0 * s.d,
                            nqt, s.d, smax, cmax16, dmax, q16, info);
         ScoreParams sp{};
@@ -1208,30 +2113,10 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
             bp.KC = KC;
             hipLaunchKernelGGL(block_select_kernel, dim3(nqt), dim3(BS_THREADS), 0, stream, bp);
         }
-        RescoreParams rp{};
-        rp.codes = reinterpret_cast<const uint4 *>(blocked);
-        rp.scales = scales;
-        rp.qrot = Qrot + q0 * s.d;
-        rp.cents = cents32;
-        rp.top_i = top_i;
-        rp.amin = amin;
-        rp.state = state;
-        rp.info = info;
-        rp.ids = ids + q0 * k;
-        rp.scores = scores + q0 * k;
-        rp.flags = flags + q0;
-        rp.d = s.d;
-        rp.bits = s.bits;
-        rp.chunks = s.chunks;
-        rp.lut_words = s.chunks * 512;
-        rp.k = k;
-        with_slots(KC, [&](auto sc) {
-            constexpr int S = decltype(sc)::value;
-            hipLaunchKernelGGL(rescore_kernel<S>, dim3(nqt), dim3(kTableThreads), lds_rescore, stream,
-                               rp);
-        });
+        rescore(q0, nqt, top_i, amin, state, info);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        q0 += nqt;
     }
     // queries whose top k is not proven run on the single-query scan
     std::vector<int> hf((size_t)nq);
