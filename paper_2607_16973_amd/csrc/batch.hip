@@ -1052,7 +1052,7 @@ struct WideParams {
     const float *cents;        // 16 levels
     int64_t n, nblk, ntiles;   // tiles of NG blocks
     int chunks, pstride, npil; // pilot tiles: i * pstride, i < npil
-    int pilot;                 // 1: pilot launch, 0: main launch
+    int pilot;                 // 1: pilot launch, 0: main launch (selects the kernel)
     float *pil;                // pilot: [QP][npil * 64 NG] scores
     const float *theta;        // main: [nqt] thresholds
     const uint16_t *tenants;   // main, filtered
@@ -1131,7 +1131,7 @@ __device__ inline void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-template <int QW>
+template <int QW, bool PILOT>
 __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
     using WS = WideShape<QW>;
     constexpr int QP = WS::QP, QF = WS::QF, NI = WS::NI, SU = WS::SU, NB = WS::NB, PD = WS::PD;
@@ -1155,12 +1155,12 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
     const int g = wave % NG, h = wave / NG;
     const int G = gridDim.x, wg = blockIdx.x;
     const int CH = p.chunks;
-    const int64_t nt_all = p.pilot ? p.npil : p.ntiles - p.npil;
+    const int64_t nt_all = PILOT ? p.npil : p.ntiles - p.npil;
     const int64_t my_tiles = nt_all > wg ? (nt_all - wg + G - 1) / G : 0;
     // the i-th tile of this workgroup
     auto tile_of = [&](int64_t i) -> int64_t {
         const int64_t j = wg + i * G;
-        if (p.pilot) return j * p.pstride;
+        if (PILOT) return j * p.pstride;
         const int64_t r = p.pstride - 1;   // >= 1 whenever there are main tiles
         return (j / r) * p.pstride + 1 + j % r;
     };
@@ -1173,7 +1173,7 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
     }
     for (int q = tid; q < QP; q += WD_THREADS) {
         fq[q] = p.qf[q];
-        th[q] = (!p.pilot && q < p.nqt) ? p.theta[q] : INFINITY;
+        th[q] = (!PILOT && q < p.nqt) ? p.theta[q] : INFINITY;
         cnt[q] = 0;
     }
     if (my_tiles > 0) {
@@ -1254,6 +1254,14 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
         wait_slabs(std::integral_constant<int, PD - 1>());
         lds_barrier();
         operands(slab, bcur);
+        // this wave's A operands of a slab: fragment 2t + ks of its query half
+        half8 acur[2 * QT];
+        auto a_operands = [&](const uint4 *sb) {
+#pragma unroll
+            for (int f = 0; f < 2 * QT; ++f)
+                acur[f] = reinterpret_cast<const half8 *>(sb)[WS::pos(h * 2 * QT + f) + lane];
+        };
+        a_operands(slab);
 
         float16v acc[QT][2];
         auto clear_acc = [&]() {
@@ -1280,7 +1288,7 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
             const float scl[2] = {ts[0], ts[32]};
             const int64_t vb = (tile * NG + g) * 64 + (lane & 31);
             const bool vin[2] = {vb < p.n, vb + 32 < p.n};
-            if (p.pilot) {
+            if constexpr (PILOT) {
                 const int64_t prow = (int64_t)p.npil * 64 * NG;
                 const int64_t pcol = (wg + ti * G) * 64 * NG + g * 64 + (lane & 31);
 #pragma unroll
@@ -1299,53 +1307,71 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
                 uint32_t hit[QT];
 #pragma unroll
                 for (int t = 0; t < QT; ++t) {
-                    float fr[16], tr[16];   // the tile row's factors and thresholds, read together
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int q = hq + 32 * t + 8 * (e >> 2) + (e & 3);
-                        fr[e] = fq[q];
-                        tr[e] = th[q];
-                    }
                     uint32_t hb = 0u;
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        hb |= (vin[0] && acc[t][0][e] * scl[0] * fr[e] >= tr[e]) ? 1u << (2 * e) : 0u;
-                        hb |= (vin[1] && acc[t][1][e] * scl[1] * fr[e] >= tr[e]) ? 2u << (2 * e) : 0u;
+                    for (int i = 0; i < 4; ++i) {
+                        // four queries' factors and thresholds, read together
+                        const float4 f4 = *reinterpret_cast<const float4 *>(fq + hq + 32 * t + 8 * i);
+                        const float4 t4 = *reinterpret_cast<const float4 *>(th + hq + 32 * t + 8 * i);
+                        const float fr[4] = {f4.x, f4.y, f4.z, f4.w}, tr[4] = {t4.x, t4.y, t4.z, t4.w};
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const int e = 4 * i + j;
+                            hb |= (vin[0] && acc[t][0][e] * scl[0] * fr[j] >= tr[j]) ? 1u << (2 * e) : 0u;
+                            hb |= (vin[1] && acc[t][1][e] * scl[1] * fr[j] >= tr[j]) ? 2u << (2 * e) : 0u;
+                        }
                     }
                     hit[t] = hb;
                 }
-                // ... then append those (rare)
+                // ... then append those (rare): one entry per lane and round,
+                // its value picked out of the accumulators by its bit index
+                // (a fixed select chain: the accumulators stay in registers)
+                uint32_t pend[QT];
 #pragma unroll
-                for (int t = 0; t < QT; ++t) {
-                    if (!__ballot(hit[t] != 0u)) continue;
+                for (int t = 0; t < QT; ++t) pend[t] = hit[t];
+                auto any_pending = [&]() {
+                    uint32_t o = 0u;
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const uint32_t two = (hit[t] >> (2 * e)) & 3u;
-                        if (!__ballot(two != 0u)) continue;
-                        const int q = hq + 32 * t + 8 * (e >> 2) + (e & 3);
-                        float f = fq[q];
-                        // opaque: the products are formed again here rather
-                        // than kept live from the test above
-                        asm volatile("" : "+v"(f));
+                    for (int t = 0; t < QT; ++t) o |= pend[t];
+                    return o != 0u;
+                };
+                while (__ballot(any_pending())) {
+                    if (any_pending()) {
+                        int bt = 0;   // lowest pending bit: tile bt, bit bb = 2e + m
 #pragma unroll
-                        for (int m = 0; m < 2; ++m) {
-                            if ((two >> m) & 1u) {
-                                const float val = acc[t][m][e] * scl[m] * f;
-                                const int64_t v = vb + 32 * m;
-                                bool ok = true;
-                                if (p.allow) {
-                                    const int tn = p.tenants[v];
-                                    ok = (tn >> 6) < p.W &&
-                                         ((p.allow[(int64_t)q * p.W + (tn >> 6)] >> (tn & 63)) & 1ull);
-                                }
-                                if (ok) {
-                                    const int slot = atomicAdd(&cnt[q], 1);
-                                    if (slot < p.S) {
-                                        const int64_t o = ((int64_t)wg * QP + q) * p.S + slot;
-                                        p.cand_s[o] = val;
-                                        p.cand_i[o] = (int)v;
-                                    }
-                                }
+                        for (int t = QT - 1; t >= 0; --t)
+                            if (pend[t]) bt = t;
+                        uint32_t word = pend[0];
+#pragma unroll
+                        for (int t = 1; t < QT; ++t) word = bt == t ? pend[t] : word;
+                        const int bb = __builtin_ctz(word);
+#pragma unroll
+                        for (int t = 0; t < QT; ++t)
+                            if (bt == t) pend[t] &= pend[t] - 1u;
+                        float a = 0.f;
+#pragma unroll
+                        for (int t = 0; t < QT; ++t)
+#pragma unroll
+                            for (int e = 0; e < 16; ++e)
+#pragma unroll
+                                for (int m = 0; m < 2; ++m)
+                                    a = (bt == t && bb == 2 * e + m) ? acc[t][m][e] : a;
+                        const int e = bb >> 1, m = bb & 1;
+                        const int q = hq + 32 * bt + 8 * (e >> 2) + (e & 3);
+                        const float val = a * scl[m] * fq[q];
+                        const int64_t v = vb + 32 * m;
+                        bool ok = true;
+                        if (p.allow) {
+                            const int tn = p.tenants[v];
+                            ok = (tn >> 6) < p.W &&
+                                 ((p.allow[(int64_t)q * p.W + (tn >> 6)] >> (tn & 63)) & 1ull);
+                        }
+                        if (ok) {
+                            const int slot = atomicAdd(&cnt[q], 1);
+                            if (slot < p.S) {
+                                const int64_t o = ((int64_t)wg * QP + q) * p.S + slot;
+                                p.cand_s[o] = val;
+                                p.cand_i[o] = (int)v;
                             }
                         }
                     }
@@ -1359,13 +1385,11 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
                 // every wave is done with the buffer the new request overwrites
                 wait_slabs(std::integral_constant<int, PD - 2>());
                 lds_barrier();
-                // the products of slab s in QT groups; the code word of slab
-                // s + 1 turned into the next B operands, and this step's
-                // loads, are issued between the groups so that they overlap
-                // the matrix cores' work instead of following it
-                const uint4 *sb = slab + buf * SU;
+                // the products of slab s (operands read a step ahead) in groups
+                // of two; the code word of slab s + 1 turned into the next B
+                // operands, and this step's loads, are issued between the
+                // groups so that they overlap the matrix cores' work
                 buf = buf + 1 == NB ? 0 : buf + 1;
-                const half8 *qa = reinterpret_cast<const half8 *>(sb) + lane;
                 const uint4 wn = slab[buf * SU + WS::pos(QF + g) + lane];
                 half8 bnext[4];
                 // k-half outer, so that the two products into one accumulator
@@ -1375,7 +1399,7 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
                 for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
                     for (int t = 0; t < QT; ++t) {
-                        const half8 a = qa[WS::pos(h * 2 * QT + 2 * t + ks)];
+                        const half8 a = acur[2 * t + ks];
                         acc[t][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bcur[ks], acc[t][0], 0, 0, 0);
                         acc[t][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, bcur[2 + ks], acc[t][1], 0, 0, 0);
                         const int grp = ks * QT + t;   // groups of two products
@@ -1401,15 +1425,22 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
                 if constexpr (DHI > 1 && 2 * QT <= 2) request_part(std::integral_constant<int, 1>());
                 if constexpr (DHI > 2 && 2 * QT <= 3) request_part(std::integral_constant<int, 2>());
                 request_done();
+                // the next slab's A operands, read now so that they arrive
+                // while this wave waits at the next barrier
+                a_operands(slab + buf * SU);
 #pragma unroll
                 for (int m = 0; m < 4; ++m) bcur[m] = bnext[m];
             }
             epilogue();
             if (++ti == my_tiles) break;
             tile = tile_of(ti);
+            // the next step's operands again (its slab stays in place until the
+            // next request): not held in registers across the epilogue
+            a_operands(slab + buf * SU);
+            operands(slab + buf * SU, bcur);
         }
     }
-    if (!p.pilot) {
+    if (!PILOT) {
         __syncthreads();
         for (int q = tid; q < QP; q += WD_THREADS) p.cand_n[(int64_t)wg * QP + q] = cnt[q];
     }
@@ -1853,7 +1884,7 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
 // Launches wide_scores_kernel for a pass of QP query slots (QP / 2 queries
 // per wave).
 hipError_t launch_wide_scores(int QP, const WideParams &wp, int grid, hipStream_t stream) {
-    static bool attr[3] = {false, false, false};
+    static bool attr[6] = {false, false, false, false, false, false};
     hipError_t err = hipSuccess;
     auto go = [&](int slot, auto kern, size_t lds) {
         if (!attr[slot]) {
@@ -1865,10 +1896,20 @@ hipError_t launch_wide_scores(int QP, const WideParams &wp, int grid, hipStream_
         hipLaunchKernelGGL(kern, dim3(grid), dim3(WD_THREADS), lds, stream, wp);
         err = hipGetLastError();
     };
+    const int pl = wp.pilot ? 1 : 0;
     switch (QP) {
-    case 64: go(0, wide_scores_kernel<32>, WideShape<32>::lds); break;
-    case 128: go(1, wide_scores_kernel<64>, WideShape<64>::lds); break;
-    default: go(2, wide_scores_kernel<128>, WideShape<128>::lds); break;
+    case 64:
+        if (pl) go(0, wide_scores_kernel<32, true>, WideShape<32>::lds);
+        else go(3, wide_scores_kernel<32, false>, WideShape<32>::lds);
+        break;
+    case 128:
+        if (pl) go(1, wide_scores_kernel<64, true>, WideShape<64>::lds);
+        else go(4, wide_scores_kernel<64, false>, WideShape<64>::lds);
+        break;
+    default:
+        if (pl) go(2, wide_scores_kernel<128, true>, WideShape<128>::lds);
+        else go(5, wide_scores_kernel<128, false>, WideShape<128>::lds);
+        break;
     }
     return err;
 }
