@@ -1010,6 +1010,7 @@ constexpr int PS_THREADS = 1024;               // pilot_select_kernel, final_sel
 constexpr int kPilotMax = 65536;               // pilot vectors per query (16-bit keys in 128 KiB of LDS)
 constexpr int kFinalMax = 16384;               // candidates a query's final selection gathers
 constexpr int kWideMaxQ = 256;
+constexpr int kWideMinQ = 64;                 // passes of more queries take the wide path (fewer: tiles of 32)
 constexpr int kWideMinChunks = 8;            // chunks per vector of a wide pass: more than its slabs ahead
 
 // Order-preserving map of float32 onto uint32; 0 marks an absent entry
@@ -1082,7 +1083,7 @@ struct WideShape {
     static constexpr int NI = QF + WD_NG;              // 1 KiB pieces of a slab
     static constexpr int DW = (NI + WD_WAVES - 1) / WD_WAVES;
     static constexpr int SU = WD_WAVES * DW * 64;      // uint4 of a slab
-    static constexpr int NB = QW == 128 ? 5 : QW == 64 ? 7 : 8;   // slab buffers
+    static constexpr int NB = QW == 128 ? 5 : 7;       // slab buffers
     static constexpr int PD = NB - 1;                  // slabs requested ahead
     static constexpr size_t lds = kTableBytes + (size_t)NB * SU * 16 + 2 * 1024 +
                                   3 * (size_t)QP * 4;
@@ -1808,7 +1809,7 @@ WideGeom wide_geom(const ScanShape &s, int NG, int grid, int KC) {
 }
 
 // Query slots of a wide pass of nqt > kTile queries.
-int wide_slots(int nqt) { return nqt <= 64 ? 64 : nqt <= 128 ? 128 : 256; }
+int wide_slots(int nqt) { return nqt <= 128 ? 128 : 256; }
 
 
 // Row length of the approximate-score matrix: whole 512-vector select units.
@@ -1852,7 +1853,7 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
     o += align256((size_t)nq * k * 4);
     L.lut = o;
     o += lut_search_workspace_bytes(s, nq, k, grid);
-    if (nq > kTile && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
+    if (nq > kWideMinQ && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
         const int KC = batch_candidates(k), PCM = 2 * KC;
         const int QP = wide_slots((int)std::min<int64_t>(nq, kWideMaxQ));
         const WideGeom w = wide_geom(s, WD_NG, grid, KC);
@@ -1898,10 +1899,6 @@ hipError_t launch_wide_scores(int QP, const WideParams &wp, int grid, hipStream_
     };
     const int pl = wp.pilot ? 1 : 0;
     switch (QP) {
-    case 64:
-        if (pl) go(0, wide_scores_kernel<32, true>, WideShape<32>::lds);
-        else go(3, wide_scores_kernel<32, false>, WideShape<32>::lds);
-        break;
     case 128:
         if (pl) go(1, wide_scores_kernel<64, true>, WideShape<64>::lds);
         else go(4, wide_scores_kernel<64, false>, WideShape<64>::lds);
@@ -2008,7 +2005,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         });
     };
     for (int64_t q0 = 0; q0 < nq;) {
-        if (nq - q0 > kTile && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
+        if (nq - q0 > kWideMinQ && s.chunks >= kWideMinChunks && grid <= PS_THREADS) {
             // a wide pass of up to kWideMaxQ queries
             const int nqt = (int)std::min<int64_t>(nq - q0, kWideMaxQ);
             const int QP = wide_slots(nqt);
@@ -2103,7 +2100,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
             q0 += nqt;
             continue;
         }
-        const int nqt = (int)(nq - q0);
+        const int nqt = (int)std::min<int64_t>(nq - q0, kTile);
         hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream, Qrot + q0 * s.d,
                            nqt, s.d, smax, cmax16, dmax, q16, info);
         ScoreParams sp{};

@@ -1,4 +1,4 @@
-"""GPU parity of the batched matrix-core path in passes of 33 to 256 queries
+"""GPU parity of the batched matrix-core path in passes of 65 to 256 queries
 (one pass over the code store per pass, no score matrix: a pilot launch
 scores every vector of some tiles, the KC-th best allowed pilot score per
 query is its threshold, the main launch keeps only vectors that reach it,
@@ -9,9 +9,10 @@ scores, section IV-A ground truth) and against the single-query path's
 scores for the same ids:
 
 * the 10,000-row workload, where every tile is a pilot tile, in passes of
-  33, 64, 200 and 300 (256 + 44) queries at k = 10 and 100;
+  65, 100, 200 and 300 (a pass of 256, then 44 queries in tiles of 32) at
+  k = 10 and 100;
 * a 70,037-row corpus (274 tiles: pilot and main launches both work, the
-  last block is partial) in passes of 40, 128 and 256 queries, k = 10 and
+  last block is partial) in passes of 65, 128 and 256 queries, k = 10 and
   100, and filtered by Zipf tenants (section V-C), selective and broad;
 * forced failures (all scores tied) in a pass of 64 queries, re-run on the
   single-query path."""
@@ -85,7 +86,7 @@ def _check(c, nq, k, ids, sc, tenants=None, bm=None):
                c.qn[:nq], k, ref_i, ref_s, allowed=masks)
 
 
-@pytest.mark.parametrize("nq,k", [(33, 10), (64, 100), (200, 10), (300, 100), (300, 10)])
+@pytest.mark.parametrize("nq,k", [(65, 10), (100, 100), (200, 10), (300, 100), (300, 10)])
 def test_all_pilot_passes(small, nq, k):
     print("wide small nq=%d k=%d" % (nq, k), flush=True)
     Q = small.Qd[:nq].contiguous()
@@ -95,7 +96,7 @@ def test_all_pilot_passes(small, nq, k):
     same_as_lut(small.idx, Q, k, ids, sc)
 
 
-@pytest.mark.parametrize("nq,k", [(40, 10), (128, 10), (256, 10), (256, 100), (128, 100)])
+@pytest.mark.parametrize("nq,k", [(65, 10), (128, 10), (256, 10), (256, 100), (128, 100)])
 def test_pilot_and_main_passes(mid, nq, k):
     print("wide mid nq=%d k=%d" % (nq, k), flush=True)
     Q = mid.Qd[:nq].contiguous()
@@ -137,24 +138,27 @@ def test_tied_scores_fall_back(small_env):
     idx = tq.Index(e.cb, e.rot, n_tenants=1)
     idx.add_codes(torch.from_numpy(one).cuda().expand(n, -1).contiguous(),
                   torch.from_numpy(e.scales[:1]).cuda().expand(n).contiguous())
-    Q = e.Qd[:64].contiguous()
+    Q = torch.cat([e.Qd, e.Qd[:16]]).contiguous()   # 80 queries: one wide pass
     ids, sc = idx.search(Q, 10, path="mfma")
-    assert tq.last_search_fallbacks() == 64
+    assert tq.last_search_fallbacks() == 80
     li, ls = idx.search(Q, 10, path="lut")
     assert torch.equal(ids, li) and torch.equal(sc, ls)
     assert np.array_equal(ids.cpu().numpy()[0], np.arange(10))
 
 
 def test_few_vectors_every_one_a_candidate(small_env):
-    """100 vectors and 64 queries at k = 10: fewer vectors than candidate
+    """100 vectors and 80 queries at k = 10: fewer vectors than candidate
     slots, so every vector is a candidate and the result is certified
     without a threshold."""
     e = small_env
     idx = tq.Index(e.cb, e.rot, n_tenants=1)
     idx.add_codes(torch.from_numpy(oracle.pack_codes(e.codes[:100], 4)).cuda(),
                   torch.from_numpy(e.scales[:100]).cuda())
-    ids, sc = idx.search(e.Qd, 10, path="mfma")
+    Q = np.concatenate([e.Q, e.Q[:16]])
+    ids, sc = idx.search(torch.from_numpy(Q).cuda(), 10, path="mfma")
     assert tq.last_search_fallbacks() == 0
-    ref_i, ref_s = oracle.search(e.codes[:100], e.scales[:100], e.ocb.cents, e.R32, e.Q, 10)
+    ref_i, ref_s = oracle.search(e.codes[:100], e.scales[:100], e.ocb.cents, e.R32, Q, 10)
+    qrot = oracle.rotate_queries(e.R32, Q)
+    qn = np.linalg.norm(Q.astype(np.float64), axis=1)
     check_topk(ids.cpu().numpy(), sc.cpu().numpy(), e.codes[:100], e.scales[:100], e.ocb.cents,
-               e.qrot, e.qn, 10, ref_i, ref_s, n=100)
+               qrot, qn, 10, ref_i, ref_s, n=100)
