@@ -340,6 +340,9 @@ def main() -> int:
     ap.add_argument("--no-extra", action="store_true", help="skip recall / latency extras")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the bit-width sweep (encode and search at b = 2, 3, 4, 8)")
+    ap.add_argument("--batched-calls", type=int, default=0,
+                    help="after timing, run this many batched (matrix-core) calls of 256 queries "
+                         "at k = 10 (for counter collection with --no-extra)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run three 1 GiB device-to-device copies (a kernel of "
                          "known traffic for scaling the HBM byte counters)")
@@ -492,6 +495,12 @@ def main() -> int:
         extra["tqplus"] = tqplus_study(tq, synth, cb, rot, X, Qrot, k, n, d, dev, stream)
     if not args.no_extra and not args.no_sweep:
         extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
+    if args.batched_calls > 0:
+        qb = Qrot[:256].contiguous()
+        for _ in range(args.batched_calls):
+            idx.search(qb, 10, path="mfma", prerotated=True)
+        torch.cuda.synchronize()
+        log("batched calls: %d of 256 queries at k = 10" % args.batched_calls)
     del X
     torch.cuda.empty_cache()
     if args.copy_calibration:
