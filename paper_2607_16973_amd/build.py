@@ -25,10 +25,12 @@ HIP_SOURCES = ["encode.hip", "scan.hip", "batch.hip", "layout.hip", "calib.hip",
                "api.cpp"]
 # Per-source extra flags.  The scan's prefetch ring must stay where it is
 # written: machine sinking would move every refill into the loop latch and
-# serialise the loads with the table lookups.  The atomic optimizer would
+# serialise the loads with the table lookups (in the encode GEMM it moves
+# the float64 folds out of the matrix-core stream and spills).  The atomic optimizer would
 # turn the one-lane work-claim atomics into wave-wide ones whose result is
 # read at once, stalling on the LDS round trip the scan hides.
-EXTRA_FLAGS = {"scan.hip": ["-mllvm", "-disable-machine-sink",
+EXTRA_FLAGS = {"encode.hip": ["-mllvm", "-disable-machine-sink"],
+               "scan.hip": ["-mllvm", "-disable-machine-sink",
                             "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
                "batch.hip": ["-mllvm", "-disable-machine-sink",
                              "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}

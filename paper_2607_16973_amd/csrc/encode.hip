@@ -1,16 +1,16 @@
 // Rotation + quantisation of float32 rows on gfx950 (section II-B, steps 1-5).
 //
 // Pipeline per chunk of rows:
-//  1. rot_gemm<QuantEpilogue>: Y = X R^T on the matrix cores
-//     (v_mfma_f32_16x16x4_f32), with each 32-wide slab of k accumulated in
-//     float32 and then added into float64 accumulators.  The same kernel
-//     computes the exact row norm n = sqrt(sum_k x_k^2) (sequential float64
-//     over k, from the staged A tile) and reports non-finite inputs.  The
-//     epilogue turns every y into a code by comparing it with fl64(t_i * n)
-//     and flags the coordinate when y lies within tau of a threshold, where
-//     tau bounds |y - S| for S the float64 sequential dot product of the
-//     definition:
-//       per slab, float32 MFMA accumulation of 32 products from 0:
+//  0. row_norm_kernel: the exact row norm n = sqrt(sum_k x_k^2) (sequential
+//     float64 over k) and a report of non-finite inputs.
+//  1. encode_gemm: Y = X R^T on the matrix cores (v_mfma_f32_32x32x2f32),
+//     with each 32-wide slab of k accumulated in float32 and then added into
+//     float64 accumulators.  The epilogue turns every y into a code by
+//     comparing it with fl64(t_i * n) and flags the coordinate when y lies
+//     within tau of a threshold, where tau bounds |y - S| for S the float64
+//     sequential dot product of the definition:
+//       per slab, float32 MFMA accumulation of 32 products from 0, in any
+//       order:
 //         |err| <= gamma_33 * sum|R_jk x_k|   (gamma_m = m u / (1 - m u),
 //                                              u = 2^-24; doubled for margin)
 //       float64 sum of 48 slab partials and the float64 reference itself:
@@ -41,6 +41,14 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+// Barrier that orders LDS accesses only (outstanding global loads of the
+// staging registers need not complete here).
+__device__ inline void lds_barrier_local() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 constexpr int BM = 128;                 // rows of X per workgroup
 constexpr int BN = 128;                 // rows of R (output columns) per workgroup
 constexpr int KB = 32;                  // k per slab
@@ -62,10 +70,6 @@ struct QuantArgs {
     int *status;            // set non-zero on a non-finite input
 };
 
-struct F32Args {
-    float *Y;               // [rows][d]
-};
-
 // XCD-aware tile order: the d/BN column tiles of one row tile go to the same
 // XCD (workgroups are dealt to the 8 XCDs round-robin), so the X tile is read
 // from HBM once and then served by that XCD's L2.
@@ -76,17 +80,16 @@ __device__ inline void tile_of(int bid, int ncol, int &rt, int &ct) {
     rt = (rest / ncol) * 8 + x;
 }
 
-template <bool QUANT>
+// Y = X R^T in float32 (query rotation).  Each 32-wide k-slab is
+// accumulated on the matrix cores (v_mfma_f32_16x16x4f32, lane (l16, g4)
+// feeding k = 16 sub + 4 g4 + st to step st of sub-slab sub) and then added
+// into float64 accumulators in slab order; the result is rounded to float32
+// once.  rot_small_kernel repeats exactly this arithmetic.
 __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
     const float *__restrict__ X, int64_t m, const float *__restrict__ R, int d,
-    int n_row_tiles, QuantArgs qa, F32Args fa) {
+    int n_row_tiles, float *__restrict__ Y) {
     __shared__ __attribute__((aligned(16))) float As[2][BM * LDS_STRIDE];
     __shared__ __attribute__((aligned(16))) float Bs[2][BN * LDS_STRIDE];
-    __shared__ double norm_s[BM];
-    __shared__ double bnd_s[255];   // the shared thresholds t_i (no TQ+ tables)
-    // TQ+ thresholds of this tile's columns, [levels-1][BN], for b <= 4
-    __shared__ double athr_s[QUANT ? 15 * BN : 1];
-    __shared__ unsigned int nflag_s;
 
     const int ncol = (d + BN - 1) / BN;
     int rt, ct;
@@ -143,40 +146,14 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
 #pragma unroll
             for (int v = 0; v < 4; ++v) accd[i][j][v] = 0.0;
         }
-    double nrm2 = 0.0;       // sequential sum of squares (threads < BM own a row)
-    bool finite = true;
 
     const int nslab = d / KB;
-    if (QUANT && !qa.athr)
-        for (int i = tid; i < qa.levels - 1; i += GEMM_THREADS) bnd_s[i] = qa.bounds[i];
-    const bool athr_lds = QUANT && qa.athr && qa.levels <= 16;
-    if (athr_lds)
-        for (int e = tid; e < (qa.levels - 1) * BN; e += GEMM_THREADS) {
-            const int i = e / BN, c = col0 + e % BN;
-            athr_s[e] = c < d ? qa.athr[(int64_t)i * d + c] : 0.0;
-        }
-    if (QUANT && tid == 0) nflag_s = 0;
     load_slab(0);
     store_slab(0);
     __syncthreads();
     for (int s = 0; s < nslab; ++s) {
         const int buf = s & 1;
         if (s + 1 < nslab) load_slab((s + 1) * KB);
-        if (QUANT && tid < BM) {
-            // row norm, k in order
-            const float *a = &As[buf][tid * LDS_STRIDE];
-#pragma unroll
-            for (int q = 0; q < KB; q += 4) {
-                const f4 v = *reinterpret_cast<const f4 *>(a + q);
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const double xv = (double)v[c];
-                    finite = finite && std::isfinite(v[c]);
-                    const double sq = xv * xv;
-                    nrm2 = nrm2 + sq;
-                }
-            }
-        }
 #pragma unroll
         for (int sub = 0; sub < KB / 16; ++sub) {
             f4 af[4], bf[2];
@@ -210,85 +187,282 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
         __syncthreads();
     }
 
-    if (QUANT) {
-        if (tid < BM) {
-            const double nrm = std::sqrt(nrm2);
-            norm_s[tid] = nrm;
-            const int64_t gr = row0 + tid;
-            if (gr < m) {
-                if (ct == 0) qa.norms[gr] = nrm;
-                if (!finite) atomicOr(qa.status, 1);
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int lr = wr * 64 + ti * 16 + g4 * 4 + v;
+            const int64_t gr = row0 + lr;
+            if (gr >= m) continue;
+#pragma unroll
+            for (int tj = 0; tj < 2; ++tj) {
+                const int col = col0 + wc * 32 + tj * 16 + l16;
+                if (col < d) Y[gr * d + col] = (float)accd[ti][tj][v];
             }
         }
-        __syncthreads();
-        const int L = qa.levels;
-        const int64_t tile = (int64_t)rt * ncol + ct;
-        uint32_t *tflags = qa.flags + tile * (BM * BN);
+}
+
+// ------------------------------------------------------------- row norms
+// n = sqrt(sum_k x_k^2) of every row of the chunk: one thread per row adds
+// the squares in k order in float64 (x^2 is exact in float64, so the fused
+// multiply-add rounds exactly as add(fl(x^2))), streaming its row AHEAD
+// 16-byte pieces ahead (d/4 is a multiple of AHEAD).  A non-finite input
+// makes the sum non-finite (x^2 of a finite float32 cannot overflow
+// float64), which sets *status.
+template <int AHEAD>
+__global__ __launch_bounds__(64) void row_norm_kernel(const float *__restrict__ X, int64_t m,
+                                                      int d, double *__restrict__ norms,
+                                                      int *__restrict__ status) {
+    const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (r >= m) return;
+    const f4 *p = reinterpret_cast<const f4 *>(X + r * d);
+    const int nq = d / 4;
+    f4 buf[AHEAD];
 #pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
+    for (int u = 0; u < AHEAD; ++u) buf[u] = p[u];
+    double s2 = 0.0;
+    for (int q0 = 0; q0 < nq; q0 += AHEAD) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int lr = wr * 64 + ti * 16 + g4 * 4 + v;
+        for (int u = 0; u < AHEAD; ++u) {
+            const f4 v = buf[u];
+            if (q0 + AHEAD + u < nq) buf[u] = p[q0 + AHEAD + u];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const double x = (double)v[c];
+                s2 = __builtin_fma(x, x, s2);
+            }
+        }
+    }
+    norms[r] = std::sqrt(s2);
+    if (!std::isfinite(s2)) atomicOr(status, 1);
+}
+
+// ------------------------------------------------------------- encode_gemm
+// Y = X R^T with the quantiser epilogue, for the encode.  Same tiles and
+// workgroup shape as rot_gemm (128 x 128, k-slabs of 32, 8 waves of 64 x 32),
+// but built for throughput:
+//  - v_mfma_f32_32x32x2f32 (two 32 x 32 tiles per wave), which keeps the
+//    matrix pipe busier than 16x16x4 at two waves per SIMD;
+//  - a three-stage LDS ring written two slabs ahead and one barrier per
+//    slab, with each k-group's operands read from LDS one group ahead, so
+//    that no LDS latency sits between a barrier and the next MFMA;
+//  - two sets of float32 accumulators: the float64 fold of slab s-1 is
+//    interleaved with the MFMAs of slab s;
+//  - the row norms come from row_norm_kernel (float64 vector work in this
+//    loop does not overlap the matrix pipe).
+// Slab s covers k in [32s, 32s+32); group g of it k in [32s+8g, 32s+8g+8).
+// Lane l (h = l / 32) of a wave feeds k = 32s + 8g + 4h + t to step t of
+// group g, so one 16-byte LDS read per operand and group serves 4 MFMAs.
+// The float32 partial of a slab sums its 32 products in an order of the
+// matrix core's choosing; the error bound behind tau (any order of a
+// 32-term float32 sum from zero) is the same as for rot_gemm.
+constexpr int EG_STAGES = 3;
+constexpr int EG_OPER = BM * LDS_STRIDE;            // floats of one operand tile in a stage
+constexpr int EG_STAGE = 2 * EG_OPER;               // A then B
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
+    const float *__restrict__ X, int64_t m, const float *__restrict__ R, int d,
+    int n_row_tiles, QuantArgs qa) {
+    __shared__ __attribute__((aligned(16))) float stg[EG_STAGES * EG_STAGE];
+    __shared__ double norm_s[BM];
+    __shared__ double bnd_s[255];
+    __shared__ double athr_s[15 * BN];   // TQ+ thresholds of the tile's columns, b <= 4
+    __shared__ unsigned int nflag_s;
+
+    const int ncol = (d + BN - 1) / BN;
+    int rt, ct;
+    tile_of(blockIdx.x, ncol, rt, ct);
+    if (rt >= n_row_tiles) return;
+    const int64_t row0 = (int64_t)rt * BM;
+    const int col0 = ct * BN;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = wave >> 2;     // 0..1 : 64-row half
+    const int wc = wave & 3;      // 0..3 : 32-column quarter
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    const int nslab = d / KB;     // even: d is a multiple of 64
+
+    // global -> LDS staging: 2 x 16 B of A and of B per thread and slab.
+    // Rows of X past m and rows of R past d are clamped to the last one: they
+    // only feed outputs that the epilogue drops.
+    uint32_t ga_o[2], gb_o[2];    // element offsets of the thread's pieces at slab 0
+    int st_off[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int e = tid + r * GEMM_THREADS;
+        const int row = e >> 3;
+        const int kq = (e & 7) * 4;
+        const int64_t ar = row0 + row < m ? row0 + row : m - 1;
+        const int br = col0 + row < d ? col0 + row : d - 1;
+        ga_o[r] = (uint32_t)(ar * d + kq);
+        gb_o[r] = (uint32_t)(br * d + kq);
+        st_off[r] = row * LDS_STRIDE + kq;
+    }
+    f4 ga[2], gb[2];
+    auto gload = [&](int s) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            ga[r] = *reinterpret_cast<const f4 *>(X + ga_o[r] + s * KB);
+            gb[r] = *reinterpret_cast<const f4 *>(R + gb_o[r] + s * KB);
+        }
+    };
+    auto gstore = [&](int stage) {
+        float *A = stg + stage * EG_STAGE;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            *reinterpret_cast<f4 *>(A + st_off[r]) = ga[r];
+            *reinterpret_cast<f4 *>(A + EG_OPER + st_off[r]) = gb[r];
+        }
+    };
+    // operands of group g: A rows of the wave's two 32-row tiles, B columns
+    const int a_off = (wr * 64 + l32) * LDS_STRIDE + 4 * h;
+    const int b_off = EG_OPER + (wc * 32 + l32) * LDS_STRIDE + 4 * h;
+    auto opread = [&](int stage, int g, f4 &a0, f4 &a1, f4 &b) {
+        const float *S = stg + stage * EG_STAGE + 8 * g;
+        a0 = *reinterpret_cast<const f4 *>(S + a_off);
+        a1 = *reinterpret_cast<const f4 *>(S + a_off + 32 * LDS_STRIDE);
+        b = *reinterpret_cast<const f4 *>(S + b_off);
+    };
+
+    if (!qa.athr)
+        for (int i = tid; i < qa.levels - 1; i += GEMM_THREADS) bnd_s[i] = qa.bounds[i];
+    const bool athr_lds = qa.athr && qa.levels <= 16;
+    if (athr_lds)
+        for (int e = tid; e < (qa.levels - 1) * BN; e += GEMM_THREADS) {
+            const int i = e / BN, c = col0 + e % BN;
+            athr_s[e] = c < d ? qa.athr[(int64_t)i * d + c] : 0.0;
+        }
+    if (tid == 0) nflag_s = 0;
+    if (tid < BM) norm_s[tid] = row0 + tid < m ? qa.norms[row0 + tid] : 0.0;
+
+    // prologue: slabs 0 and 1 in stages 0 and 1, slab 2 in flight
+    gload(0);
+    gstore(0);
+    gload(1);
+    gstore(1);
+    if (nslab > 2) gload(2);
+    __syncthreads();
+
+    const f16v zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
+                       0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    f16v acc[2][2];     // [set][tile]: float32 partials of slab s (set s & 1)
+    double accd[2][16]; // [tile][i]
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        acc[1][t] = zero;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) accd[t][i] = 0.0;
+    }
+    f4 ca0, ca1, cb;
+    opread(0, 0, ca0, ca1, cb);
+
+    auto slab = [&](int s, f16v(&cur)[2], const f16v(&prv)[2]) {
+        const int stage = s % EG_STAGES;
+        const int stage1 = (s + 1) % EG_STAGES;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f4 na0, na1, nb;
+            if (g < 3)
+                opread(stage, g + 1, na0, na1, nb);
+            else if (s + 1 < nslab)
+                opread(stage1, 0, na0, na1, nb);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                cur[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(ca0[t], cb[t],
+                                                              (g == 0 && t == 0) ? zero : cur[0], 0, 0, 0);
+                cur[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(ca1[t], cb[t],
+                                                              (g == 0 && t == 0) ? zero : cur[1], 0, 0, 0);
+            }
+            // fold a quarter of slab s-1's partials (zeros before slab 0)
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                accd[g >> 1][(g & 1) * 8 + i] += (double)prv[g >> 1][(g & 1) * 8 + i];
+            if (g == 1) {
+                // every wave is past slab s-1: its stage, (s+2) % 3, is free
+                lds_barrier_local();
+                if (s + 2 < nslab) gstore((s + 2) % EG_STAGES);
+                if (s + 3 < nslab) gload(s + 3);
+            }
+            ca0 = na0;
+            ca1 = na1;
+            cb = nb;
+        }
+    };
+    for (int s = 0; s < nslab; s += 2) {
+        slab(s, acc[0], acc[1]);
+        slab(s + 1, acc[1], acc[0]);
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) accd[t][i] += (double)acc[1][t][i];
+
+    const int L = qa.levels;
+    const int64_t tile = (int64_t)rt * ncol + ct;
+    uint32_t *tflags = qa.flags + tile * (BM * BN);
+    const int lc = wc * 32 + l32;
+    const int col = col0 + lc;
+    // Code and flag of the lane's 32 outputs (one column, 32 rows).  thr(q)
+    // is threshold q of this column before scaling by n.  The binary search
+    // runs level by level over a tile's 16 outputs, so that their threshold
+    // reads are independent (L is a power of two: c + step - 1 <= L - 2).
+    auto epilogue = [&](auto thr) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            int c[16];
+            double nr[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                c[i] = 0;
+                nr[i] = norm_s[wr * 64 + t * 32 + 8 * (i >> 2) + 4 * h + (i & 3)];
+            }
+            for (int step = L / 2; step >= 1; step >>= 1) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+                    c[i] += (thr(c[i] + step - 1) * nr[i] <= accd[t][i]) ? step : 0;
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int lr = wr * 64 + t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
                 const int64_t gr = row0 + lr;
-                if (gr >= m) continue;
-                const double nrm = norm_s[lr];
+                const double y = accd[t][i];
+                const double nrm = nr[i];
                 const double tau = kTauRel * nrm + kTauAbs;
-#pragma unroll
-                for (int tj = 0; tj < 2; ++tj) {
-                    const int col = col0 + wc * 32 + tj * 16 + l16;
-                    if (col >= d) continue;
-                    const double y = accd[ti][tj][v];
-                    int code;
-                    bool flag = false;
-                    if (nrm == 0.0) {
-                        code = L / 2;
-                    } else {
-                        // threshold i of this coordinate, before scaling by n
-                        auto thr = [&](int i) {
-                            if (!qa.athr) return bnd_s[i];
-                            return athr_lds ? athr_s[i * BN + (col - col0)]
-                                            : qa.athr[(int64_t)i * d + col];
-                        };
-                        int c = 0;
-                        for (int step = L / 2; step >= 1; step >>= 1) {
-                            if (c + step <= L - 1) {
-                                const double t = thr(c + step - 1) * nrm;
-                                if (t <= y) c += step;
-                            }
-                        }
-                        code = c;
-                        if (!std::isfinite(y)) {
-                            flag = true;
-                        } else {
-                            if (c > 0 && y - thr(c - 1) * nrm <= tau) flag = true;
-                            if (c < L - 1 && thr(c) * nrm - y <= tau) flag = true;
-                        }
-                    }
+                const int ci = c[i];
+                const double lo = thr(ci > 0 ? ci - 1 : 0) * nrm;
+                const double hi = thr(ci < L - 1 ? ci : L - 2) * nrm;
+                bool flag = !std::isfinite(y) || (ci > 0 && y - lo <= tau) ||
+                            (ci < L - 1 && hi - y <= tau);
+                int code = ci;
+                if (nrm == 0.0) {
+                    code = L / 2;
+                    flag = false;
+                }
+                if (gr < m && col < d) {
                     qa.codes_tmp[gr * d + col] = (uint8_t)code;
                     if (flag) {
                         // a slot of this tile's list (an LDS counter)
                         const unsigned int slot = atomicAdd(&nflag_s, 1u);
-                        tflags[slot] = ((uint32_t)lr << 7) | (uint32_t)(col - col0);
+                        tflags[slot] = ((uint32_t)lr << 7) | (uint32_t)lc;
                     }
                 }
             }
-        __syncthreads();
-        if (tid == 0) qa.tile_count[tile] = nflag_s;
+        }
+    };
+    if (!qa.athr) {
+        epilogue([&](int q) { return bnd_s[q]; });
+    } else if (athr_lds) {
+        epilogue([&](int q) { return athr_s[q * BN + lc]; });
     } else {
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int lr = wr * 64 + ti * 16 + g4 * 4 + v;
-                const int64_t gr = row0 + lr;
-                if (gr >= m) continue;
-#pragma unroll
-                for (int tj = 0; tj < 2; ++tj) {
-                    const int col = col0 + wc * 32 + tj * 16 + l16;
-                    if (col < d) fa.Y[gr * d + col] = (float)accd[ti][tj][v];
-                }
-            }
+        const double *ac = qa.athr + (col < d ? col : d - 1);
+        epilogue([&](int q) { return ac[(int64_t)q * d]; });
     }
+    __syncthreads();
+    if (tid == 0) qa.tile_count[tile] = nflag_s;
 }
 
 // The code of coordinate j of a row with norm nrm whose exact sum is S.
@@ -487,7 +661,7 @@ __global__ __launch_bounds__(256) void pack_kernel(
 }
 
 // Y = X R^T for a few rows (m <= kSmallRows), with exactly the arithmetic of
-// rot_gemm<false>: every output element goes through the same
+// rot_gemm: every output element goes through the same
 // v_mfma_f32_16x16x4f32 sequence (the same k in the same operand slots, sub
 // and step order), its float32 partial is folded into float64 after each
 // 32-wide slab and rounded to float32 at the end, so a row rotates to the
@@ -601,9 +775,17 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
         const int groups = (nrt + 7) / 8;
         // every output tile of the chunk writes its flag count
         QuantArgs qa{bounds, calib.athr, cb.levels, codes_tmp, norms, flags, tile_count, status_dev};
-        F32Args fa{nullptr};
-        hipLaunchKernelGGL((rot_gemm<true>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
-                           stream, X + r0 * d, m, R, d, nrt, qa, fa);
+        // one wave per 64 rows, spread over the CUs
+        if (d % 128 == 0)
+            hipLaunchKernelGGL(row_norm_kernel<32>, dim3((unsigned)((m + 63) / 64)), dim3(64), 0,
+                               stream, X + r0 * d, m, d, norms, status_dev);
+        else
+            hipLaunchKernelGGL(row_norm_kernel<16>, dim3((unsigned)((m + 63) / 64)), dim3(64), 0,
+                               stream, X + r0 * d, m, d, norms, status_dev);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(encode_gemm, dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
+                           stream, X + r0 * d, m, R, d, nrt, qa);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         // 8-bit codes flag about 2% of coordinates (thresholds ~4e-4 apart
@@ -644,10 +826,8 @@ hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R, flo
     const int ncol = (d + BN - 1) / BN;
     const int nrt = (int)((m + BM - 1) / BM);
     const int groups = (nrt + 7) / 8;
-    QuantArgs qa{};
-    F32Args fa{Y};
-    hipLaunchKernelGGL((rot_gemm<false>), dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
-                       stream, X, m, R, d, nrt, qa, fa);
+    hipLaunchKernelGGL(rot_gemm, dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0, stream, X, m, R,
+                       d, nrt, Y);
     return hipGetLastError();
 }
 
