@@ -576,7 +576,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void fixup_tile_kernel(
 }
 
 // Packs PACK_ROWS rows per workgroup: scale, canonical bitstream, blocked layout.
-constexpr int PACK_ROWS = 32;   // PACK_ROWS * d bytes of LDS (<= 64 KiB at d = 2048)
+// The codes are staged in LDS with a row stride of d + 16 bytes, so that the
+// scale threads (one per row, reading 16 codes at a time) meet different
+// banks.
+constexpr int PACK_ROWS = 32;   // PACK_ROWS * (d + 16) bytes of LDS (66 KiB at d = 2048)
 
 __global__ __launch_bounds__(256) void pack_kernel(
     const uint8_t *__restrict__ codes_tmp, int64_t m, int d, int bits,
@@ -585,29 +588,56 @@ __global__ __launch_bounds__(256) void pack_kernel(
     uint8_t *__restrict__ canon, float *__restrict__ scales,
     uint8_t *__restrict__ blocked, float *__restrict__ blocked_scales, int64_t base,
     int chunks) {
-    extern __shared__ __attribute__((aligned(16))) uint8_t cs[];   // [PACK_ROWS][d]
+    extern __shared__ __attribute__((aligned(16))) uint8_t cs_raw[];   // [PACK_ROWS][d + 16]
+    __shared__ double csq_s[256];
     const int64_t r0 = (int64_t)blockIdx.x * PACK_ROWS;
     const int rows = (int)((m - r0) < PACK_ROWS ? (m - r0) : PACK_ROWS);
     const int tid = threadIdx.x;
-    // stage codes (16 B per thread per step)
+    const int L = 1 << bits;
+    const int ps = d + 16;           // LDS row stride
+    if (!ysq)
+        for (int i = tid; i < L; i += blockDim.x) csq_s[i] = cent_sq[i];
+    // stage codes, 16 B per piece; each thread's pieces are loaded together
     const int vec_per_row = d / 16;
-    for (int e = tid; e < rows * vec_per_row; e += blockDim.x) {
+    const int total = rows * vec_per_row;
+    constexpr int PIECES = PACK_ROWS * (2048 / 16) / 256;   // at most 16 per thread
+    uint4 v[PIECES];
+#pragma unroll
+    for (int u = 0; u < PIECES; ++u) {
+        const int e = min(tid + u * 256, total - 1);   // rows >= 1: a valid piece
         const int r = e / vec_per_row, q = e % vec_per_row;
-        reinterpret_cast<uint4 *>(cs + r * d)[q] =
-            reinterpret_cast<const uint4 *>(codes_tmp + (r0 + r) * d)[q];
+        v[u] = reinterpret_cast<const uint4 *>(codes_tmp + (r0 + r) * d)[q];
+    }
+#pragma unroll
+    for (int u = 0; u < PIECES; ++u) {
+        const int e = tid + u * 256;
+        if (e < total) {
+            const int r = e / vec_per_row, q = e % vec_per_row;
+            reinterpret_cast<uint4 *>(cs_raw + r * ps)[q] = v[u];
+        }
     }
     __syncthreads();
     // scale: one thread per row, j in order
     if (tid < rows) {
-        const uint8_t *c = cs + tid * d;
+        const uint8_t *c = cs_raw + tid * ps;
         // sum_j fl64(yhat_j^2): c[code]^2, or with TQ+ the calibrated
         // reconstruction's square, per coordinate ([d][levels])
-        const int L = 1 << bits;
         double h2 = 0.0;
-        if (ysq)
+        if (ysq) {
             for (int j = 0; j < d; ++j) h2 = h2 + ysq[(int64_t)j * L + c[j]];
-        else
-            for (int j = 0; j < d; ++j) h2 = h2 + cent_sq[c[j]];
+        } else {
+            for (int j = 0; j < d; j += 16) {
+                const uint4 w = *reinterpret_cast<const uint4 *>(c + j);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) h2 = h2 + csq_s[(w.x >> (8 * q)) & 255];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) h2 = h2 + csq_s[(w.y >> (8 * q)) & 255];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) h2 = h2 + csq_s[(w.z >> (8 * q)) & 255];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) h2 = h2 + csq_s[(w.w >> (8 * q)) & 255];
+            }
+        }
         const double nrm = norms[r0 + tid];
         const float s = (nrm == 0.0) ? 0.0f : (float)(nrm / std::sqrt(h2));
         if (scales) scales[r0 + tid] = s;
@@ -618,7 +648,7 @@ __global__ __launch_bounds__(256) void pack_kernel(
     if (canon) {
         for (int e = tid; e < rows * wpr; e += blockDim.x) {
             const int r = e / wpr, w = e % wpr;
-            const uint8_t *c = cs + r * d;
+            const uint8_t *c = cs_raw + r * ps;
             uint32_t word = 0;
             if (bits == 3) {
                 const int b0 = w * 32;
@@ -639,7 +669,7 @@ __global__ __launch_bounds__(256) void pack_kernel(
         for (int e = tid; e < rows * chunks * 4; e += blockDim.x) {
             const int r = e / (chunks * 4), rem = e % (chunks * 4);
             const int ch = rem >> 2, wq = rem & 3;
-            const uint8_t *c = cs + r * d;
+            const uint8_t *c = cs_raw + r * ps;
             uint32_t word = 0;
             if (bits == 3) {
                 const int j0 = (ch * 4 + wq) * 10;
@@ -801,7 +831,7 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);
-        hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * d, stream,
+        hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * (d + 16), stream,
                            codes_tmp, m, d, cb.bits, cent_sq, calib.ysq, norms,
                            out.canonical ? out.canonical + r0 * (int64_t)(d * cb.bits / 8) : nullptr,
                            out.scales ? out.scales + r0 : nullptr, out.blocked,
