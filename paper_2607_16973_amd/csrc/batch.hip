@@ -39,6 +39,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "lds_dma.h"
 #include "lut.h"
 #include "stream.h"
 #include "topk.h"
@@ -1090,47 +1091,6 @@ struct WideShape {
     // uint4 offset of piece i within a slab
     static constexpr int pos(int i) { return ((i % WD_WAVES) * DW + i / WD_WAVES) * 64; }
 };
-
-// Loads 16 bytes per lane from global memory straight into LDS: lane l's
-// bytes go to LDS byte address lds_base + 16 l (lds_base wave-uniform).  The
-// compiler does not see these loads, so their completion is awaited with
-// explicit vector-memory counter waits before the barrier that publishes
-// the slab (a wait on the counter also covers any older access).
-__device__ inline void lds_dma16(const void *src, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(src) : "memory");
-}
-// Several such loads from one LDS base: set_lds_base, then lds_dma16_at<K>
-// with the lane's source address; load K lands at base + K KiB + 16 l (the
-// instruction offset moves both addresses, so it is taken off the source).
-// Setting the base once per group of loads matters: a load must read the
-// base before it may be changed again.
-__device__ inline void set_lds_base(uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0" :: "s"(__builtin_amdgcn_readfirstlane(lds_base))
-                 : "memory");
-}
-template <int K, bool NT>
-__device__ inline void lds_dma16_at(const void *src) {
-    const char *s = static_cast<const char *>(src) - K * 1024;
-    if constexpr (NT)
-        asm volatile("global_load_lds_dwordx4 %0, off offset:%1 nt" :: "v"(s), "i"(K * 1024) : "memory");
-    else
-        asm volatile("global_load_lds_dwordx4 %0, off offset:%1" :: "v"(s), "i"(K * 1024) : "memory");
-}
-// s_waitcnt until at most N vector-memory operations of this wave are
-// outstanding (other counters unconstrained).
-template <int N>
-__device__ inline void wait_vmem() {
-    static_assert(N >= 0 && N < 64, "vector-memory counter range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-// Barrier that orders LDS accesses only: outstanding global stores of the
-// epilogue (candidates for a later kernel) need not complete here.
-__device__ inline void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 template <int QW, bool PILOT>
 __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {

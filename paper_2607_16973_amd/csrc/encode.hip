@@ -33,21 +33,15 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace tq {
 namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
-
-// Barrier that orders LDS accesses only (outstanding global loads of the
-// staging registers need not complete here).
-__device__ inline void lds_barrier_local() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 constexpr int BM = 128;                 // rows of X per workgroup
 constexpr int BN = 128;                 // rows of R (output columns) per workgroup
@@ -243,9 +237,10 @@ __global__ __launch_bounds__(64) void row_norm_kernel(const float *__restrict__ 
 // but built for throughput:
 //  - v_mfma_f32_32x32x2f32 (two 32 x 32 tiles per wave), which keeps the
 //    matrix pipe busier than 16x16x4 at two waves per SIMD;
-//  - a three-stage LDS ring written two slabs ahead and one barrier per
-//    slab, with each k-group's operands read from LDS one group ahead, so
-//    that no LDS latency sits between a barrier and the next MFMA;
+//  - a four-stage LDS ring filled by direct global -> LDS loads three slabs
+//    ahead, one barrier per slab, and each k-group's operands read from LDS
+//    one group ahead, so that no load or LDS latency sits between a barrier
+//    and the next MFMA;
 //  - two sets of float32 accumulators: the float64 fold of slab s-1 is
 //    interleaved with the MFMAs of slab s;
 //  - the row norms come from row_norm_kernel (float64 vector work in this
@@ -256,16 +251,24 @@ __global__ __launch_bounds__(64) void row_norm_kernel(const float *__restrict__ 
 // The float32 partial of a slab sums its 32 products in an order of the
 // matrix core's choosing; the error bound behind tau (any order of a
 // 32-term float32 sum from zero) is the same as for rot_gemm.
-constexpr int EG_STAGES = 3;
-constexpr int EG_OPER = BM * LDS_STRIDE;            // floats of one operand tile in a stage
-constexpr int EG_STAGE = 2 * EG_OPER;               // A then B
+constexpr int EG_STAGES = 4;
+constexpr int EG_OPER_B = BM * KB * 4;   // bytes of one operand tile of a slab (16 KiB)
+constexpr int EG_STAGE_B = 2 * EG_OPER_B;  // A then B
+
+// Operand tiles are stored unpadded in four planes, one per k-group g:
+// plane g holds, for each of the 128 rows, the row's floats 8g .. 8g+7 of
+// the slab as two 16-byte pieces, piece h at byte 4096 g + 32 r +
+// 16 (h ^ eg_swz(r)).  A read of piece h of 16 consecutive rows (8, with
+// 32 banks) then meets distinct banks, and the group index is an immediate
+// offset.
+__device__ inline int eg_swz(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
 __global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
     const float *__restrict__ X, int64_t m, const float *__restrict__ R, int d,
     int n_row_tiles, QuantArgs qa) {
-    __shared__ __attribute__((aligned(16))) float stg[EG_STAGES * EG_STAGE];
+    __shared__ __attribute__((aligned(1024))) char stg[EG_STAGES * EG_STAGE_B];
     __shared__ double norm_s[BM];
     __shared__ double bnd_s[255];
     __shared__ double athr_s[15 * BN];   // TQ+ thresholds of the tile's columns, b <= 4
@@ -286,46 +289,47 @@ __global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
     const int h = lane >> 5;
     const int nslab = d / KB;     // even: d is a multiple of 64
 
-    // global -> LDS staging: 2 x 16 B of A and of B per thread and slab.
-    // Rows of X past m and rows of R past d are clamped to the last one: they
-    // only feed outputs that the epilogue drops.
-    uint32_t ga_o[2], gb_o[2];    // element offsets of the thread's pieces at slab 0
-    int st_off[2];
+    // This wave's loads of a slab: pieces 128 wave + 64 j + lane (j = 0, 1)
+    // of the A tile and of the B tile.  Rows of X past m and rows of R past
+    // d are clamped to the last one: they only feed outputs the epilogue
+    // drops.
+    // This wave's loads of a slab: 1 KiB pieces 2 wave + j (j = 0, 1) of the
+    // A tile and of the B tile, i.e. plane wave / 2, rows 32 ((2 wave + j) & 3)
+    // + lane / 2.  Rows of X past m and rows of R past d are clamped to the
+    // last one: they only feed outputs that the epilogue drops.
+    uint32_t off_a[2], off_b[2];   // byte offsets of the lane's pieces in slab 0
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-        const int e = tid + r * GEMM_THREADS;
-        const int row = e >> 3;
-        const int kq = (e & 7) * 4;
+    for (int j = 0; j < 2; ++j) {
+        const int i = 2 * wave + j;
+        const int row = 32 * (i & 3) + (lane >> 1);
+        const int k = 8 * (i >> 2) + 4 * ((lane & 1) ^ eg_swz(row));
         const int64_t ar = row0 + row < m ? row0 + row : m - 1;
         const int br = col0 + row < d ? col0 + row : d - 1;
-        ga_o[r] = (uint32_t)(ar * d + kq);
-        gb_o[r] = (uint32_t)(br * d + kq);
-        st_off[r] = row * LDS_STRIDE + kq;
+        off_a[j] = (uint32_t)((ar * d + k) * 4);
+        off_b[j] = (uint32_t)(((int64_t)br * d + k) * 4);
     }
-    f4 ga[2], gb[2];
-    auto gload = [&](int s) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            ga[r] = *reinterpret_cast<const f4 *>(X + ga_o[r] + s * KB);
-            gb[r] = *reinterpret_cast<const f4 *>(R + gb_o[r] + s * KB);
-        }
-    };
-    auto gstore = [&](int stage) {
-        float *A = stg + stage * EG_STAGE;
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            *reinterpret_cast<f4 *>(A + st_off[r]) = ga[r];
-            *reinterpret_cast<f4 *>(A + EG_OPER + st_off[r]) = gb[r];
-        }
+    const uint32_t stg_lds = (uint32_t)(uintptr_t)stg;
+    // slab s into stage ST: 4 loads per wave (uniform base + 32-bit lane offset)
+    auto request = [&](int s, auto ST) {
+        constexpr uint32_t stage = decltype(ST)::value;
+        const uint32_t base = stg_lds + stage * EG_STAGE_B + (uint32_t)wave * 2048;
+        const float *xa = X + s * KB;
+        const float *rb = R + s * KB;
+        lds_dma16_s(off_a[0], xa, base);
+        lds_dma16_s(off_a[1], xa, base + 1024);
+        lds_dma16_s(off_b[0], rb, base + EG_OPER_B);
+        lds_dma16_s(off_b[1], rb, base + EG_OPER_B + 1024);
     };
     // operands of group g: A rows of the wave's two 32-row tiles, B columns
-    const int a_off = (wr * 64 + l32) * LDS_STRIDE + 4 * h;
-    const int b_off = EG_OPER + (wc * 32 + l32) * LDS_STRIDE + 4 * h;
-    auto opread = [&](int stage, int g, f4 &a0, f4 &a1, f4 &b) {
-        const float *S = stg + stage * EG_STAGE + 8 * g;
-        a0 = *reinterpret_cast<const f4 *>(S + a_off);
-        a1 = *reinterpret_cast<const f4 *>(S + a_off + 32 * LDS_STRIDE);
-        b = *reinterpret_cast<const f4 *>(S + b_off);
+    const int pz = 16 * (h ^ eg_swz(l32));   // eg_swz(row) of every row this lane reads
+    const int a_base = (wr * 64 + l32) * 32 + pz;
+    const int b_base = EG_OPER_B + (wc * 32 + l32) * 32 + pz;
+    auto opread = [&](auto ST, int g, f4 &a0, f4 &a1, f4 &b) {
+        constexpr int stage = decltype(ST)::value;
+        const char *S = stg + stage * EG_STAGE_B + 4096 * g;
+        a0 = *reinterpret_cast<const f4 *>(S + a_base);
+        a1 = *reinterpret_cast<const f4 *>(S + a_base + 32 * 32);
+        b = *reinterpret_cast<const f4 *>(S + b_base);
     };
 
     if (!qa.athr)
@@ -339,13 +343,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
     if (tid == 0) nflag_s = 0;
     if (tid < BM) norm_s[tid] = row0 + tid < m ? qa.norms[row0 + tid] : 0.0;
 
-    // prologue: slabs 0 and 1 in stages 0 and 1, slab 2 in flight
-    gload(0);
-    gstore(0);
-    gload(1);
-    gstore(1);
-    if (nslab > 2) gload(2);
-    __syncthreads();
+    // prologue: slabs 0, 1 and 2 requested, 0 and 1 landed
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    request(0, I0());
+    request(1, I1());
+    if (nslab > 2) {
+        request(2, I2());
+        wait_vmem<4>();
+    } else {
+        wait_vmem<0>();
+    }
+    lds_barrier();
 
     const f16v zero = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f,
                        0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -357,24 +368,29 @@ __global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
 #pragma unroll
         for (int i = 0; i < 16; ++i) accd[t][i] = 0.0;
     }
-    f4 ca0, ca1, cb;
-    opread(0, 0, ca0, ca1, cb);
+    // operands: set g & 1 feeds group g while group g + 1's are read into
+    // the other set (static indices once unrolled: no register copies)
+    f4 op[2][3];
+    opread(I0(), 0, op[0][0], op[0][1], op[0][2]);
 
-    auto slab = [&](int s, f16v(&cur)[2], const f16v(&prv)[2]) {
-        const int stage = s % EG_STAGES;
-        const int stage1 = (s + 1) % EG_STAGES;
+    // slab s, held in stage ST (static, so that every LDS address is an
+    // offset from a fixed register)
+    auto slab = [&](int s, auto ST, f16v(&cur)[2], const f16v(&prv)[2]) {
+        using Next = std::integral_constant<int, (decltype(ST)::value + 1) % EG_STAGES>;
+        using Far = std::integral_constant<int, (decltype(ST)::value + 3) % EG_STAGES>;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            f4 na0, na1, nb;
+            f4(&c)[3] = op[g & 1];
+            f4(&n)[3] = op[(g + 1) & 1];
             if (g < 3)
-                opread(stage, g + 1, na0, na1, nb);
+                opread(ST, g + 1, n[0], n[1], n[2]);
             else if (s + 1 < nslab)
-                opread(stage1, 0, na0, na1, nb);
+                opread(Next(), 0, n[0], n[1], n[2]);
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                cur[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(ca0[t], cb[t],
+                cur[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(c[0][t], c[2][t],
                                                               (g == 0 && t == 0) ? zero : cur[0], 0, 0, 0);
-                cur[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(ca1[t], cb[t],
+                cur[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(c[1][t], c[2][t],
                                                               (g == 0 && t == 0) ? zero : cur[1], 0, 0, 0);
             }
             // fold a quarter of slab s-1's partials (zeros before slab 0)
@@ -382,19 +398,28 @@ __global__ __launch_bounds__(GEMM_THREADS) void encode_gemm(
             for (int i = 0; i < 8; ++i)
                 accd[g >> 1][(g & 1) * 8 + i] += (double)prv[g >> 1][(g & 1) * 8 + i];
             if (g == 1) {
-                // every wave is past slab s-1: its stage, (s+2) % 3, is free
-                lds_barrier_local();
-                if (s + 2 < nslab) gstore((s + 2) % EG_STAGES);
-                if (s + 3 < nslab) gload(s + 3);
+                // slab s+1 has landed (this wave's loads; the barrier makes it
+                // every wave's), and every wave is past slab s-1, whose stage,
+                // (s+3) % 4, takes slab s+3
+                if (s + 2 < nslab)
+                    wait_vmem<4>();
+                else
+                    wait_vmem<0>();
+                lds_barrier();
+                if (s + 3 < nslab) request(s + 3, Far());
             }
-            ca0 = na0;
-            ca1 = na1;
-            cb = nb;
         }
     };
-    for (int s = 0; s < nslab; s += 2) {
-        slab(s, acc[0], acc[1]);
-        slab(s + 1, acc[1], acc[0]);
+    int s0 = 0;
+    for (; s0 + 4 <= nslab; s0 += 4) {
+        slab(s0, I0(), acc[0], acc[1]);
+        slab(s0 + 1, I1(), acc[1], acc[0]);
+        slab(s0 + 2, I2(), acc[0], acc[1]);
+        slab(s0 + 3, I3(), acc[1], acc[0]);
+    }
+    if (s0 < nslab) {   // nslab = 2 mod 4: two more, in stages 0 and 1
+        slab(s0, I0(), acc[0], acc[1]);
+        slab(s0 + 1, I1(), acc[1], acc[0]);
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
