@@ -502,10 +502,14 @@ __device__ inline int exact_code(double S, double nrm, int j, int d, const doubl
 }
 
 // Exact recomputation of flagged coordinates, one thread per flag (one
-// workgroup per output tile): the sequential float64 sum of the definition
+// wave per output tile): the sequential float64 sum of the definition
 // (products of float32 values are exact in float64, so fused and unfused
-// multiply-adds agree).
-__global__ __launch_bounds__(256) void fixup_kernel(
+// multiply-adds agree).  Each thread streams its X row and R row AHEAD
+// 16-byte pieces ahead, so that the loads of a flag overlap instead of
+// following one another (d/4 is a multiple of AHEAD).
+constexpr int FIX_AHEAD = 16;
+
+__global__ __launch_bounds__(64) void fixup_kernel(
     const float *__restrict__ X, const float *__restrict__ R, int d, int ncol,
     const double *__restrict__ bounds, const double *__restrict__ athr, int levels,
     const double *__restrict__ norms,
@@ -516,20 +520,34 @@ __global__ __launch_bounds__(256) void fixup_kernel(
     const int col0 = (tile % ncol) * BN;
     const unsigned int cnt = tile_count[tile];
     const uint32_t *tflags = flags + (int64_t)tile * (BM * BN);
-    for (unsigned int e = threadIdx.x; e < cnt; e += blockDim.x) {
+    const int nq = d / 4;
+    for (unsigned int e = threadIdx.x; e < cnt; e += 64) {
         const uint32_t f = tflags[e];
         const int64_t row = row0 + (f >> 7);
         const int j = col0 + (int)(f & 127);
         const f4 *xr = reinterpret_cast<const f4 *>(X + row * d);
         const f4 *rr = reinterpret_cast<const f4 *>(R + (int64_t)j * d);
-        double S = 0.0;
-        for (int q = 0; q < d / 4; ++q) {
-            const f4 a = rr[q];
-            const f4 b = xr[q];
+        f4 bx[FIX_AHEAD], br[FIX_AHEAD];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const double prod = (double)a[c] * (double)b[c];
-                S = S + prod;
+        for (int u = 0; u < FIX_AHEAD; ++u) {
+            bx[u] = xr[u];
+            br[u] = rr[u];
+        }
+        double S = 0.0;
+        for (int q0 = 0; q0 < nq; q0 += FIX_AHEAD) {
+#pragma unroll
+            for (int u = 0; u < FIX_AHEAD; ++u) {
+                const f4 a = br[u];
+                const f4 b = bx[u];
+                if (q0 + FIX_AHEAD + u < nq) {
+                    bx[u] = xr[q0 + FIX_AHEAD + u];
+                    br[u] = rr[q0 + FIX_AHEAD + u];
+                }
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const double prod = (double)a[c] * (double)b[c];
+                    S = S + prod;
+                }
             }
         }
         codes_tmp[row * d + j] = (uint8_t)exact_code(S, norms[row], j, d, bounds, athr, levels);
@@ -850,7 +868,7 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                                X + r0 * d, m, R, d, ncol, bounds, calib.athr, cb.levels, norms,
                                flags, tile_count, codes_tmp);
         else
-            hipLaunchKernelGGL(fixup_kernel, dim3(nrt * ncol), dim3(256), 0, stream, X + r0 * d, R,
+            hipLaunchKernelGGL(fixup_kernel, dim3(nrt * ncol), dim3(64), 0, stream, X + r0 * d, R,
                                d, ncol, bounds, calib.athr, cb.levels, norms, flags, tile_count,
                                codes_tmp);
         e = hipGetLastError();
