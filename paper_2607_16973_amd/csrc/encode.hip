@@ -735,62 +735,70 @@ __global__ __launch_bounds__(256) void pack_kernel(
 
 // Y = X R^T for a few rows (m <= kSmallRows), with exactly the arithmetic of
 // rot_gemm: every output element goes through the same
-// v_mfma_f32_16x16x4f32 sequence (the same k in the same operand slots, sub
-// and step order), its float32 partial is folded into float64 after each
-// 32-wide slab and rounded to float32 at the end, so a row rotates to the
-// same bits in either kernel.  One wave per 16 x 16 output block reads its
-// fragments straight from memory, P slabs ahead: many small workgroups
-// instead of a few 128 x 128 tiles, for the latency of short batches.
+// v_mfma_f32_16x16x4f32 sequence per 32-wide slab (the same k in the same
+// operand slots, sub and step order, from zero), the slab partials are
+// folded into float64 in slab order and rounded to float32 at the end, so a
+// row rotates to the same bits in either kernel.  The slab partials do not
+// depend on each other, so they are computed in parallel: one workgroup per
+// 16 x 16 output block, its 16 waves taking every 16th slab with all their
+// loads issued at once; the partials meet in LDS and 256 threads fold them
+// in order.  For short batches this is a few microseconds of latency (one
+// round of loads) instead of 48 dependent slab steps.
 constexpr int kSmallRows = 64;
+constexpr int SPLIT_WAVES = 16;
+constexpr int SPLIT_SLABS = 2048 / KB / SPLIT_WAVES;   // slabs per wave at most
 
-template <int P>
-__global__ __launch_bounds__(256) void rot_small_kernel(const float *__restrict__ X, int64_t m,
-                                                        int d, const float *__restrict__ R,
-                                                        float *__restrict__ Y) {
+__global__ __launch_bounds__(SPLIT_WAVES * 64) void rot_small_kernel(
+    const float *__restrict__ X, int64_t m, int d, const float *__restrict__ R,
+    float *__restrict__ Y) {
+    __shared__ f4 part[2048 / KB][64];   // [slab][lane]: the 16 x 16 partial of a slab
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int l16 = lane & 15;
     const int g4 = lane >> 4;
     const int64_t r0 = (int64_t)blockIdx.y * 16;
-    const int c0 = (blockIdx.x * 4 + wave) * 16;
-    if (c0 >= d) return;   // no barrier in this kernel
+    const int c0 = blockIdx.x * 16;
     const int64_t gr = r0 + l16;   // the row of X this lane loads
     const bool rowok = gr < m;
     const float *xa = X + (rowok ? gr : 0) * d + g4 * 4;
     const float *rb = R + (int64_t)(c0 + l16) * d + g4 * 4;
-    const int nslab = d / KB;      // even; a multiple of P
-    f4 fa[P][2], fb[P][2];
-    auto load = [&](int s, f4 (&A)[2], f4 (&B)[2]) {
+    const int nslab = d / KB;
+    f4 fa[SPLIT_SLABS][2], fb[SPLIT_SLABS][2];
 #pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-            A[sub] = rowok ? *reinterpret_cast<const f4 *>(xa + s * KB + sub * 16)
-                           : f4{0.f, 0.f, 0.f, 0.f};
-            B[sub] = *reinterpret_cast<const f4 *>(rb + s * KB + sub * 16);
+    for (int u = 0; u < SPLIT_SLABS; ++u) {
+        const int s = wave + u * SPLIT_WAVES;
+        if (s < nslab) {
+#pragma unroll
+            for (int sub = 0; sub < 2; ++sub) {
+                fa[u][sub] = rowok ? *reinterpret_cast<const f4 *>(xa + s * KB + sub * 16)
+                                   : f4{0.f, 0.f, 0.f, 0.f};
+                fb[u][sub] = *reinterpret_cast<const f4 *>(rb + s * KB + sub * 16);
+            }
         }
-    };
+    }
 #pragma unroll
-    for (int u = 0; u < P; ++u) load(u, fa[u], fb[u]);
-    f4 acc = f4{0.f, 0.f, 0.f, 0.f};
-    double accd[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int s0 = 0; s0 < nslab; s0 += P) {
-#pragma unroll
-        for (int u = 0; u < P; ++u) {
+    for (int u = 0; u < SPLIT_SLABS; ++u) {
+        const int s = wave + u * SPLIT_WAVES;
+        if (s < nslab) {
+            f4 acc = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
                 for (int st = 0; st < 4; ++st)
                     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[u][sub][st], fb[u][sub][st],
                                                                acc, 0, 0, 0);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) accd[v] += (double)acc[v];
-            acc = f4{0.f, 0.f, 0.f, 0.f};
-            if (s0 + u + P < nslab) load(s0 + u + P, fa[u], fb[u]);
+            part[s][lane] = acc;
         }
     }
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        const int64_t row = r0 + g4 * 4 + v;
-        if (row < m) Y[row * d + c0 + l16] = (float)accd[v];
+    __syncthreads();
+    if (threadIdx.x < 256) {
+        // output (row g4*4 + v, column l16) of the block: element v of lane (l16, g4)
+        const int ln = threadIdx.x & 63;
+        const int v = threadIdx.x >> 6;
+        double accd = 0.0;
+        for (int s = 0; s < nslab; ++s) accd += (double)part[s][ln][v];
+        const int64_t row = r0 + (ln >> 4) * 4 + v;
+        if (row < m) Y[row * d + c0 + (ln & 15)] = (float)accd;
     }
 }
 
@@ -889,11 +897,8 @@ hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R, flo
                            hipStream_t stream) {
     if (m <= 0) return hipSuccess;
     if (m <= kSmallRows) {
-        const dim3 grid((unsigned)((d + 63) / 64), (unsigned)((m + 15) / 16));
-        if ((d / KB) % 4 == 0)
-            hipLaunchKernelGGL(rot_small_kernel<4>, grid, dim3(256), 0, stream, X, m, d, R, Y);
-        else
-            hipLaunchKernelGGL(rot_small_kernel<2>, grid, dim3(256), 0, stream, X, m, d, R, Y);
+        const dim3 grid((unsigned)(d / 16), (unsigned)((m + 15) / 16));
+        hipLaunchKernelGGL(rot_small_kernel, grid, dim3(SPLIT_WAVES * 64), 0, stream, X, m, d, R, Y);
         return hipGetLastError();
     }
     const int ncol = (d + BN - 1) / BN;

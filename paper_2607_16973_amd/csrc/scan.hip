@@ -227,9 +227,18 @@ __device__ inline void collect_survivors(const WaveTopK<S> &top, int wg_key, flo
     }
 }
 
+// The workgroup's k best are k distinct vectors, so its k-th best score is a
+// lower bound on the query's k-th best: raising the query's global bound
+// with it lets the final merge keep only the entries that reach the best
+// workgroup's k-th score (wave-level bounds alone leave most entries in).
+__device__ inline void raise_query_bound(float kth, int *gkey, int lane) {
+    if (gkey && lane == 0 && kth > -INFINITY)
+        __hip_atomic_fetch_max(gkey, fkey(kth), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <int S>
 __device__ inline void write_survivors(const float *surv_s, const int *surv_i, int total,
-                                       const ScanParams &p, int64_t out, int lane) {
+                                       const ScanParams &p, int64_t out, int lane, int *gkey) {
     float sv = lane < total ? surv_s[lane] : -INFINITY;
     int iv = lane < total ? surv_i[lane] : INT_MAX;
     wave_sort64(sv, iv, lane);
@@ -241,13 +250,14 @@ __device__ inline void write_survivors(const float *surv_s, const int *surv_i, i
             p.cand_i[out + r] = a == 0 ? iv : INT_MAX;
         }
     }
+    if (p.k <= 64) raise_query_bound(__shfl(sv, p.k - 1), gkey, lane);
 }
 
 // Pairwise merge of the 16 wave lists through LDS (stage_* hold 16 x 64*S
 // entries); wave 0 writes the result.  Starts and ends with a barrier.
 template <int S>
 __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i, int wave,
-                                  int lane, const ScanParams &p, int64_t out) {
+                                  int lane, const ScanParams &p, int64_t out, int *gkey) {
     __syncthreads();
 #pragma unroll
     for (int a = 0; a < S; ++a) {
@@ -275,6 +285,7 @@ __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i
         __syncthreads();
     }
     if (wave == 0) {
+        float kth = -INFINITY;
 #pragma unroll
         for (int a = 0; a < S; ++a) {
             const int r = a * 64 + lane;
@@ -282,7 +293,9 @@ __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i
                 p.cand_s[out + r] = top.ls[a];
                 p.cand_i[out + r] = top.li[a];
             }
+            if (a == (p.k - 1) / 64) kth = top.ls[a];
         }
+        if (p.k <= 64 * S) raise_query_bound(__shfl(kth, (p.k - 1) % 64), gkey, lane);
     }
     __syncthreads();
 }
@@ -298,10 +311,11 @@ __device__ inline void workgroup_merge(WaveTopK<S> &top, float *stage_s, int *st
     collect_survivors<S>(top, misc[0], stage_s, stage_i, misc + 2, lane);
     __syncthreads();
     const int total = misc[2];
+    int *gkey = p.gbound ? p.gbound + qi : nullptr;
     if (total <= 64) {
-        if (wave == 0) write_survivors<S>(stage_s, stage_i, total, p, out, lane);
+        if (wave == 0) write_survivors<S>(stage_s, stage_i, total, p, out, lane, gkey);
     } else {
-        tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);
+        tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, gkey);
     }
     __syncthreads();   // LDS is rebuilt for the next query
     if (threadIdx.x == 0) misc[2] = 0;
@@ -608,9 +622,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         __syncthreads();
         const int ns = misc[2];
         if (ns <= 64) {
-            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane, p.gbound + qi);
         } else {
-            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, p.gbound + qi);   // rare: LDS of the table
         }
         if (more) sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
         if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
@@ -796,9 +810,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
         __syncthreads();
         const int ns = misc[2];
         if (ns <= 64) {
-            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane, p.gbound + qi);
         } else {
-            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, p.gbound + qi);   // rare: LDS of the table
         }
         if (more) {
             sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
@@ -824,27 +838,52 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
                                                     float *__restrict__ scores) {
     __shared__ float st_s[4 * 64 * S];
     __shared__ int st_i[4 * 64 * S];
+    // survivors of the bound (k <= 64)
+    constexpr int MCAP = S == 1 ? 4096 : 1;
+    __shared__ float sv_s[MCAP];
+    __shared__ int sv_i[MCAP];
     __shared__ int nsurv;
     const int q = blockIdx.x;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     // The k best score at least the final bound gbound[q] (a proven lower
     // bound on the k-th best score), so only entries that reach it can be in
-    // the result.  For k <= 64, when at most 64 do, one wave sorts them;
-    // otherwise (and for larger k) the lists are merged in full.
-    if (threadIdx.x == 0) nsurv = k <= 64 ? 0 : 65;
+    // the result.  For k <= 64 those entries are gathered in LDS: when at
+    // most 64 survive one wave sorts them; up to MCAP, each wave folds its
+    // share in sorted runs of 64 into a running top 64 and the four lists
+    // are merged; beyond that (and for larger k) the lists are merged in
+    // full.
+    if (threadIdx.x == 0) nsurv = k <= 64 ? 0 : (1 << 30);   // k > 64: the full merge
     __syncthreads();
     if (k <= 64) {
         const float bound = unfkey(gbound[q]);
         const int64_t base = (int64_t)q * G * k;
-        for (int e = threadIdx.x; e < G * k; e += 256) {
-            const float sc = cs[base + e];
-            const int id = ci[base + e];
-            if (id != INT_MAX && !(sc < bound)) {
-                const int pos = atomicAdd(&nsurv, 1);
-                if (pos < 64) {
-                    st_s[pos] = sc;
-                    st_i[pos] = id;
+        // rounds of MERGE_BATCH entries per thread, loaded together (one
+        // memory round trip per round instead of one per entry)
+        constexpr int MERGE_BATCH = 16;
+        for (int e0 = 0; e0 < G * k; e0 += 256 * MERGE_BATCH) {
+            float sc[MERGE_BATCH];
+            int id[MERGE_BATCH];
+#pragma unroll
+            for (int u = 0; u < MERGE_BATCH; ++u) {
+                const int e = e0 + u * 256 + threadIdx.x;
+                const bool in = e < G * k;
+                sc[u] = in ? cs[base + e] : -INFINITY;
+                id[u] = in ? ci[base + e] : INT_MAX;
+            }
+#pragma unroll
+            for (int u = 0; u < MERGE_BATCH; ++u) {
+                const bool keep = id[u] != INT_MAX && !(sc[u] < bound);
+                const uint64_t m = __ballot(keep);
+                if (m) {
+                    int pos0 = 0;
+                    if (lane == 0) pos0 = atomicAdd(&nsurv, __popcll(m));
+                    pos0 = __shfl(pos0, 0);
+                    const int pos = pos0 + __popcll(m & ((1ull << lane) - 1));
+                    if (keep && pos < MCAP) {
+                        sv_s[pos] = sc[u];
+                        sv_i[pos] = id[u];
+                    }
                 }
             }
         }
@@ -853,13 +892,39 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
     const int ns = nsurv;
     if (ns <= 64) {
         if (wave == 0) {
-            float sv = lane < ns ? st_s[lane] : -INFINITY;
-            int iv = lane < ns ? st_i[lane] : INT_MAX;
+            float sv = lane < ns ? sv_s[lane] : -INFINITY;
+            int iv = lane < ns ? sv_i[lane] : INT_MAX;
             wave_sort64(sv, iv, lane);
             for (int r = lane; r < k; r += 64) {
                 const bool empty = r >= 64 || !(sv > -INFINITY);
                 ids[(int64_t)q * k + r] = empty ? -1 : (int64_t)iv;
                 scores[(int64_t)q * k + r] = empty ? -INFINITY : sv;
+            }
+        }
+        return;
+    }
+    if (S == 1 && ns <= MCAP) {
+        float ls1[1] = {-INFINITY};
+        int li1[1] = {INT_MAX};
+        for (int c = wave * 64; c < ns; c += 256) {
+            float v = c + lane < ns ? sv_s[c + lane] : -INFINITY;
+            int iv = c + lane < ns ? sv_i[c + lane] : INT_MAX;
+            wave_sort64(v, iv, lane);
+            merge_sorted64<1>(ls1, li1, v, iv, lane);
+        }
+        st_s[wave * 64 + lane] = ls1[0];
+        st_i[wave * 64 + lane] = li1[0];
+        __syncthreads();
+        if (wave == 0) {
+            for (int w = 1; w < 4; ++w) {
+                const float os[1] = {st_s[w * 64 + lane]};
+                const int oi[1] = {st_i[w * 64 + lane]};
+                merge_lists<1>(ls1, li1, os, oi, lane);
+            }
+            if (lane < k) {
+                const bool empty = !(ls1[0] > -INFINITY);
+                ids[(int64_t)q * k + lane] = empty ? -1 : (int64_t)li1[0];
+                scores[(int64_t)q * k + lane] = empty ? -INFINITY : ls1[0];
             }
         }
         return;
