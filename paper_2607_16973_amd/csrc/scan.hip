@@ -227,18 +227,9 @@ __device__ inline void collect_survivors(const WaveTopK<S> &top, int wg_key, flo
     }
 }
 
-// The workgroup's k best are k distinct vectors, so its k-th best score is a
-// lower bound on the query's k-th best: raising the query's global bound
-// with it lets the final merge keep only the entries that reach the best
-// workgroup's k-th score (wave-level bounds alone leave most entries in).
-__device__ inline void raise_query_bound(float kth, int *gkey, int lane) {
-    if (gkey && lane == 0 && kth > -INFINITY)
-        __hip_atomic_fetch_max(gkey, fkey(kth), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 template <int S>
 __device__ inline void write_survivors(const float *surv_s, const int *surv_i, int total,
-                                       const ScanParams &p, int64_t out, int lane, int *gkey) {
+                                       const ScanParams &p, int64_t out, int lane) {
     float sv = lane < total ? surv_s[lane] : -INFINITY;
     int iv = lane < total ? surv_i[lane] : INT_MAX;
     wave_sort64(sv, iv, lane);
@@ -250,14 +241,13 @@ __device__ inline void write_survivors(const float *surv_s, const int *surv_i, i
             p.cand_i[out + r] = a == 0 ? iv : INT_MAX;
         }
     }
-    if (p.k <= 64) raise_query_bound(__shfl(sv, p.k - 1), gkey, lane);
 }
 
 // Pairwise merge of the 16 wave lists through LDS (stage_* hold 16 x 64*S
 // entries); wave 0 writes the result.  Starts and ends with a barrier.
 template <int S>
 __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i, int wave,
-                                  int lane, const ScanParams &p, int64_t out, int *gkey) {
+                                  int lane, const ScanParams &p, int64_t out) {
     __syncthreads();
 #pragma unroll
     for (int a = 0; a < S; ++a) {
@@ -285,7 +275,6 @@ __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i
         __syncthreads();
     }
     if (wave == 0) {
-        float kth = -INFINITY;
 #pragma unroll
         for (int a = 0; a < S; ++a) {
             const int r = a * 64 + lane;
@@ -293,9 +282,7 @@ __device__ inline void tree_merge(WaveTopK<S> &top, float *stage_s, int *stage_i
                 p.cand_s[out + r] = top.ls[a];
                 p.cand_i[out + r] = top.li[a];
             }
-            if (a == (p.k - 1) / 64) kth = top.ls[a];
         }
-        if (p.k <= 64 * S) raise_query_bound(__shfl(kth, (p.k - 1) % 64), gkey, lane);
     }
     __syncthreads();
 }
@@ -311,11 +298,10 @@ __device__ inline void workgroup_merge(WaveTopK<S> &top, float *stage_s, int *st
     collect_survivors<S>(top, misc[0], stage_s, stage_i, misc + 2, lane);
     __syncthreads();
     const int total = misc[2];
-    int *gkey = p.gbound ? p.gbound + qi : nullptr;
     if (total <= 64) {
-        if (wave == 0) write_survivors<S>(stage_s, stage_i, total, p, out, lane, gkey);
+        if (wave == 0) write_survivors<S>(stage_s, stage_i, total, p, out, lane);
     } else {
-        tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, gkey);
+        tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);
     }
     __syncthreads();   // LDS is rebuilt for the next query
     if (threadIdx.x == 0) misc[2] = 0;
@@ -622,9 +608,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
         __syncthreads();
         const int ns = misc[2];
         if (ns <= 64) {
-            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane, p.gbound + qi);
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
         } else {
-            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, p.gbound + qi);   // rare: LDS of the table
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
         if (more) sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
         if (tid == 0) misc[0] = fkey(-INFINITY);   // every wave has read it (previous barrier)
@@ -810,9 +796,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
         __syncthreads();
         const int ns = misc[2];
         if (ns <= 64) {
-            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane, p.gbound + qi);
+            if (wave == 0) write_survivors<S>(surv_s, surv_i, ns, p, out, lane);
         } else {
-            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out, p.gbound + qi);   // rare: LDS of the table
+            tree_merge<S>(top, stage_s, stage_i, wave, lane, p, out);   // rare: LDS of the table
         }
         if (more) {
             sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, qi + 1));
@@ -843,21 +829,33 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
     __shared__ float sv_s[MCAP];
     __shared__ int sv_i[MCAP];
     __shared__ int nsurv;
+    __shared__ int lkey;
     const int q = blockIdx.x;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     // The k best score at least the final bound gbound[q] (a proven lower
-    // bound on the k-th best score), so only entries that reach it can be in
-    // the result.  For k <= 64 those entries are gathered in LDS: when at
+    // bound on the k-th best score) and at least the k-th entry of every
+    // workgroup list, so only entries that reach both can be in the result.  For k <= 64 those entries are gathered in LDS: when at
     // most 64 survive one wave sorts them; up to MCAP, each wave folds its
     // share in sorted runs of 64 into a running top 64 and the four lists
     // are merged; beyond that (and for larger k) the lists are merged in
     // full.
-    if (threadIdx.x == 0) nsurv = k <= 64 ? 0 : (1 << 30);   // k > 64: the full merge
+    if (threadIdx.x == 0) {
+        nsurv = k <= 64 ? 0 : (1 << 30);   // k > 64: the full merge
+        lkey = gbound[q];
+    }
     __syncthreads();
     if (k <= 64) {
-        const float bound = unfkey(gbound[q]);
         const int64_t base = (int64_t)q * G * k;
+        // Each workgroup's list is sorted, and its k best are k distinct
+        // vectors: the k-th entry of any list is also a lower bound on the
+        // query's k-th best score, and usually a much tighter one.
+        for (int g = threadIdx.x; g < G; g += 256) {
+            const int64_t e = base + (int64_t)g * k + (k - 1);
+            if (ci[e] != INT_MAX) atomicMax(&lkey, fkey(cs[e]));
+        }
+        __syncthreads();
+        const float bound = unfkey(lkey);
         // rounds of MERGE_BATCH entries per thread, loaded together (one
         // memory round trip per round instead of one per entry)
         constexpr int MERGE_BATCH = 16;
