@@ -10,8 +10,8 @@
 //     after a block's last chunk the approximate scores s_v <c_hat, q'> are
 //     written, scaled to a float16 range, as a [query][vector] matrix, and
 //     each query's largest score in the block as a [query][block] matrix.
-//  3. Selection of at most KC candidates per query (KC = 256, or 512 for
-//     k > 64) with a bound amin on the approximate score of every other
+//  3. Selection of at most KC candidates per query (KC = eight per result,
+//     64 to 512) with a bound amin on the approximate score of every other
 //     vector.  Unfiltered: block_select_kernel.  The R-th largest block
 //     maximum (R = KC - 32) is a score of R distinct vectors, so at least R
 //     vectors reach it, and every vector that does lies in a block whose
@@ -976,8 +976,9 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
 }
 
 // ============================================================ wide passes
-// Passes of 33 to 256 queries (QP = 64, 128 or 256 query slots) read the code
-// store once per pass and keep no score matrix:
+// Passes of 65 to 256 queries (QP = 128 or 256 query slots) read the code
+// store once per pass and keep no score matrix (passes of at most 64 queries
+// take tiles of 32, which are faster there):
 //  1. prep_kernel, then frag_kernel: the float16 queries in the A operand
 //     order of v_mfma_f32_32x32x16_f16.  Piece (c, f, l) (16 bytes) holds
 //     coordinates 32c + 16(f & 1) + 8(l >> 5) .. +7 of query
@@ -1003,8 +1004,10 @@ __global__ __launch_bounds__(kTableThreads) void rescore_kernel(RescoreParams p)
 // workgroup stages one slab in LDS -- the chunk's query pieces and the
 // chunk of each of its NG blocks -- and its eight waves multiply them: wave
 // w takes block w % NG of the tile against query half w / NG (QW queries).
-// Slabs are loaded P steps ahead into registers and written to LDS one step
-// ahead (two LDS buffers, one barrier per step).
+// Slabs go straight from global memory into a ring of NB LDS buffers
+// (direct loads, NB - 2 steps ahead); one barrier per step publishes the
+// next slab, whose codes are turned into MFMA operands while the current
+// slab is multiplied.
 constexpr int WD_THREADS = 512;
 constexpr int WD_WAVES = WD_THREADS / 64;
 constexpr int PS_THREADS = 1024;               // pilot_select_kernel, final_select_kernel
@@ -1768,7 +1771,7 @@ WideGeom wide_geom(const ScanShape &s, int NG, int grid, int KC) {
     return w;
 }
 
-// Query slots of a wide pass of nqt > kTile queries.
+// Query slots of a wide pass of nqt > kWideMinQ queries.
 int wide_slots(int nqt) { return nqt <= 128 ? 128 : 256; }
 
 
