@@ -1191,6 +1191,13 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
         if (e != hipSuccess) return hip_fail(e, "padding copy");
         return TQ_OK;
     }
+    // the LUT path's global bounds first: that launch and the scan's host
+    // work then overlap the query rotation
+    bool bounds_ready = false;
+    if (!use_mfma(sh, k, base)) {
+        const hipError_t e = lut_search_prefill(sh, nq, k, grid, workspace_dev, s, &bounds_ready);
+        if (e != hipSuccess) return hip_fail(e, "search bounds");
+    }
     const float *Qrot = Q_dev;
     if (!prerotated) {
         const float *R = nullptr;
@@ -1226,7 +1233,7 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
     }
     hipError_t e = lut_search(sh, idx->codes, idx->scales, idx->tenants, idx->summ, idx->cents_dev,
                               Qrot, nq, k, filter, grid, workspace_dev, workspace_bytes, ids_dev,
-                              scores_dev, s, qconst);
+                              scores_dev, s, qconst, bounds_ready);
     if (e != hipSuccess) return hip_fail(e, "scan");
     if (idx->idmap && (e = map_ids(ids_dev, nq * k, idx->ext, s)) != hipSuccess)
         return hip_fail(e, "id mapping");

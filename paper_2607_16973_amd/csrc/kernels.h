@@ -135,13 +135,21 @@ struct SearchFilter {
 };
 
 // qconst: [nq] constant terms of TQ+ calibrated scores (Qrot then holds
-// kappa * q'), or null.
+// kappa * q'), or null.  bounds_ready: lut_search_prefill has set the
+// queries' global bounds already.
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries,
                       const float *cents32, const float *Qrot, int64_t nq, int k,
                       const SearchFilter &filter, int grid, void *ws, size_t ws_bytes,
                       int64_t *ids, float *scores, hipStream_t stream,
-                      const float *qconst = nullptr);
+                      const float *qconst = nullptr, bool bounds_ready = false);
+// Sets the global bounds of a search that lut_search will run in one query
+// chunk (top-k path), ahead of it on the same stream: a search issues this
+// first, before the query rotation, so that its launch and the scan's host
+// work overlap the rotation instead of following it.  *done tells whether it
+// did (then lut_search takes bounds_ready = true).
+hipError_t lut_search_prefill(const ScanShape &s, int64_t nq, int k, int grid, void *ws,
+                              hipStream_t stream, bool *done);
 
 // Batched search of a tile of queries on the matrix cores with exact
 // rescoring (b = 4, chunks % 8 == 0, d <= 1792, k <= 256, at most 4096

@@ -1274,20 +1274,39 @@ size_t lut_search_workspace_bytes(const ScanShape &s, int64_t nq, int k, int gri
     return b + 256;
 }
 
+// The global bounds of a top-k search in its workspace: after the rotated
+// queries and the candidate lists of one query chunk.
+static int *search_bounds(void *ws, const ScanShape &s, int64_t nq, int k, int grid) {
+    const int64_t qc = query_chunk(s, nq, k, grid);
+    uint8_t *p8 = static_cast<uint8_t *>(ws);
+    p8 += ((size_t)nq * s.d * sizeof(float) + 255) & ~(size_t)255;
+    uint8_t *after = p8 + (size_t)qc * grid * k * (sizeof(float) + sizeof(int));
+    return reinterpret_cast<int *>((reinterpret_cast<uintptr_t>(after) + 255) & ~(uintptr_t)255);
+}
+
+hipError_t lut_search_prefill(const ScanShape &s, int64_t nq, int k, int grid, void *ws,
+                              hipStream_t stream, bool *done) {
+    *done = false;
+    if (nq <= 0 || k > kMaxTopK || query_chunk(s, nq, k, grid) < nq) return hipSuccess;
+    hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, search_bounds(ws, s, nq, k, grid),
+                       nq, (int)(0x807FFFFFu));   // order key of -inf
+    const hipError_t e = hipGetLastError();
+    *done = e == hipSuccess;
+    return e;
+}
+
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries, const float *cents32,
                       const float *Qrot, int64_t nq, int k, const SearchFilter &filter, int grid,
                       void *ws, size_t ws_bytes, int64_t *ids, float *scores,
-                      hipStream_t stream, const float *qconst) {
+                      hipStream_t stream, const float *qconst, bool bounds_ready) {
     const uint64_t *allow = filter.allow;
     const int64_t qc = query_chunk(s, nq, k, grid);
     uint8_t *p8 = static_cast<uint8_t *>(ws);
     p8 += ((size_t)nq * s.d * sizeof(float) + 255) & ~(size_t)255;   // rotated queries live here
     float *cand_s = reinterpret_cast<float *>(p8);
     int *cand_i = reinterpret_cast<int *>(cand_s + (size_t)qc * grid * k);
-    uint8_t *after = reinterpret_cast<uint8_t *>(cand_i + (size_t)qc * grid * k);
-    int *gbound = reinterpret_cast<int *>(
-        (reinterpret_cast<uintptr_t>(after) + 255) & ~(uintptr_t)255);
+    int *gbound = search_bounds(ws, s, nq, k, grid);
     (void)ws_bytes;
     if (k > kMaxTopK) {
         // every score, then a radix selection per query
@@ -1363,10 +1382,13 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         p.lut_words = lut_words_for(s);
         const bool split = use_split(s) && lds_bytes_for(s, S, true, filter.any()) <= 160 * 1024;
         const size_t lds = lds_bytes_for(s, S, split, filter.any());
-        hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
-                           (int)(0x807FFFFFu));   // order key of -inf
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        hipError_t e = hipSuccess;
+        if (!(bounds_ready && q0 == 0 && m == nq)) {
+            hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
+                               (int)(0x807FFFFFu));   // order key of -inf
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
         if (S == 1)
             e = launch_scan_mode<1>(p, grid, lds, split, stream);
         else if (S == 2)
