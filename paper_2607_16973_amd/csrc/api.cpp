@@ -1191,21 +1191,21 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq, int3
         if (e != hipSuccess) return hip_fail(e, "padding copy");
         return TQ_OK;
     }
-    // the LUT path's global bounds first: that launch and the scan's host
-    // work then overlap the query rotation
+    // the LUT path's global bounds are set by the query rotation's launch:
+    // the scan then follows the rotation with no launch in between
     bool bounds_ready = false;
-    if (!use_mfma(sh, k, base)) {
-        const hipError_t e = lut_search_prefill(sh, nq, k, grid, workspace_dev, s, &bounds_ready);
-        if (e != hipSuccess) return hip_fail(e, "search bounds");
-    }
     const float *Qrot = Q_dev;
     if (!prerotated) {
         const float *R = nullptr;
         st = rotation_dev(&idx->rot, &R);
         if (st != TQ_OK) return st;
         float *qr = static_cast<float *>(workspace_dev);
-        hipError_t e = rotate_rows_f32(Q_dev, nq, idx->d, R, qr, s);
+        int *bounds = use_mfma(sh, k, base) ? nullptr
+                                            : lut_search_bounds(sh, nq, k, grid, workspace_dev);
+        hipError_t e = rotate_rows_f32(Q_dev, nq, idx->d, R, qr, s, bounds, bounds ? nq : 0,
+                                       kBoundInit);
         if (e != hipSuccess) return hip_fail(e, "query rotation");
+        bounds_ready = bounds != nullptr;
         Qrot = qr;
     }
     float *qconst = nullptr;

@@ -750,8 +750,10 @@ constexpr int SPLIT_SLABS = 2048 / KB / SPLIT_WAVES;   // slabs per wave at most
 
 __global__ __launch_bounds__(SPLIT_WAVES * 64) void rot_small_kernel(
     const float *__restrict__ X, int64_t m, int d, const float *__restrict__ R,
-    float *__restrict__ Y) {
+    float *__restrict__ Y, int *__restrict__ fill, int nfill, int fill_value) {
     __shared__ f4 part[2048 / KB][64];   // [slab][lane]: the 16 x 16 partial of a slab
+    if (blockIdx.x == 0 && blockIdx.y == 0)
+        for (int i = threadIdx.x; i < nfill; i += SPLIT_WAVES * 64) fill[i] = fill_value;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int l16 = lane & 15;
@@ -893,14 +895,27 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
     return hipSuccess;
 }
 
+__global__ void fill_ints(int *p, int64_t n, int v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
 hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R, float *Y,
-                           hipStream_t stream) {
-    if (m <= 0) return hipSuccess;
-    if (m <= kSmallRows) {
+                           hipStream_t stream, int *fill, int64_t nfill, int fill_value) {
+    if (!fill) nfill = 0;
+    if (m > 0 && m <= kSmallRows && nfill <= kSmallRows) {
         const dim3 grid((unsigned)(d / 16), (unsigned)((m + 15) / 16));
-        hipLaunchKernelGGL(rot_small_kernel, grid, dim3(SPLIT_WAVES * 64), 0, stream, X, m, d, R, Y);
+        hipLaunchKernelGGL(rot_small_kernel, grid, dim3(SPLIT_WAVES * 64), 0, stream, X, m, d, R, Y,
+                           fill, (int)nfill, fill_value);
         return hipGetLastError();
     }
+    if (nfill > 0) {
+        hipLaunchKernelGGL(fill_ints, dim3(1), dim3(256), 0, stream, fill, nfill, fill_value);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (m <= 0) return hipSuccess;
     const int ncol = (d + BN - 1) / BN;
     const int nrt = (int)((m + BM - 1) / BM);
     const int groups = (nrt + 7) / 8;

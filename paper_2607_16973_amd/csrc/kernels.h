@@ -47,9 +47,13 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                        int *status_dev, hipStream_t stream,
                        const CalibDev &calib = CalibDev());
 
-// Y = X R^T in float32 (query rotation), X [m][d], Y [m][d].
+// Y = X R^T in float32 (query rotation), X [m][d], Y [m][d].  With fill,
+// the nfill ints at fill are also set to fill_value on the same stream (by
+// the rotation's own launch when m <= 64), so that a search's first kernel
+// can initialise its bounds without a launch of its own.
 hipError_t rotate_rows_f32(const float *X, int64_t m, int d, const float *R,
-                           float *Y, hipStream_t stream);
+                           float *Y, hipStream_t stream, int *fill = nullptr,
+                           int64_t nfill = 0, int fill_value = 0);
 
 // ------------------------------------------------------------- TQ+ (calib.hip)
 // Fits mu [d] and kappa [d] (float32, device) to the m >= 1 rows of X:
@@ -135,21 +139,23 @@ struct SearchFilter {
 };
 
 // qconst: [nq] constant terms of TQ+ calibrated scores (Qrot then holds
-// kappa * q'), or null.  bounds_ready: lut_search_prefill has set the
-// queries' global bounds already.
+// kappa * q'), or null.  bounds_ready: the queries' global bounds (at
+// lut_search_bounds) already hold kBoundInit.
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
                       const uint16_t *tenants, const uint64_t *summaries,
                       const float *cents32, const float *Qrot, int64_t nq, int k,
                       const SearchFilter &filter, int grid, void *ws, size_t ws_bytes,
                       int64_t *ids, float *scores, hipStream_t stream,
                       const float *qconst = nullptr, bool bounds_ready = false);
-// Sets the global bounds of a search that lut_search will run in one query
-// chunk (top-k path), ahead of it on the same stream: a search issues this
-// first, before the query rotation, so that its launch and the scan's host
-// work overlap the rotation instead of following it.  *done tells whether it
-// did (then lut_search takes bounds_ready = true).
-hipError_t lut_search_prefill(const ScanShape &s, int64_t nq, int k, int grid, void *ws,
-                              hipStream_t stream, bool *done);
+// The order key of -inf: the value the global bounds of a top-k search
+// start from.
+constexpr int kBoundInit = (int)0x807FFFFFu;
+// Where lut_search keeps the queries' global bounds (nq ints) when it runs
+// the top-k path in one query chunk, else null.  A search sets them to
+// kBoundInit ahead of the scan (in the query rotation's launch) and passes
+// bounds_ready = true, so that the scan's launch follows the rotation
+// without a launch of its own in between.
+int *lut_search_bounds(const ScanShape &s, int64_t nq, int k, int grid, void *ws);
 
 // Batched search of a tile of queries on the matrix cores with exact
 // rescoring (b = 4, chunks % 8 == 0, d <= 1792, k <= 256, at most 4096

@@ -935,17 +935,26 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
         ls[a] = -INFINITY;
         li[a] = INT_MAX;
     }
-    for (int g = wave; g < G; g += 4) {
-        float os[S];
-        int oi[S];
-        const int64_t base = ((int64_t)q * G + g) * k;
+    // wave w merges lists w, w + 4, ...; MERGE_LISTS of them are loaded
+    // together (one memory round trip per batch instead of one per list)
+    constexpr int MERGE_LISTS = 8;
+    for (int g0 = wave; g0 < G; g0 += 4 * MERGE_LISTS) {
+        float os[MERGE_LISTS][S];
+        int oi[MERGE_LISTS][S];
 #pragma unroll
-        for (int a = 0; a < S; ++a) {
-            const int r = a * 64 + lane;
-            os[a] = (r < k) ? cs[base + r] : -INFINITY;
-            oi[a] = (r < k) ? ci[base + r] : INT_MAX;
+        for (int u = 0; u < MERGE_LISTS; ++u) {
+            const int g = g0 + 4 * u;
+            const int64_t base = ((int64_t)q * G + (g < G ? g : 0)) * k;
+#pragma unroll
+            for (int a = 0; a < S; ++a) {
+                const int r = a * 64 + lane;
+                const bool in = g < G && r < k;
+                os[u][a] = in ? cs[base + r] : -INFINITY;
+                oi[u][a] = in ? ci[base + r] : INT_MAX;
+            }
         }
-        merge_lists<S>(ls, li, os, oi, lane);
+#pragma unroll
+        for (int u = 0; u < MERGE_LISTS; ++u) merge_lists<S>(ls, li, os[u], oi[u], lane);
     }
 #pragma unroll
     for (int a = 0; a < S; ++a) {
@@ -1284,15 +1293,9 @@ static int *search_bounds(void *ws, const ScanShape &s, int64_t nq, int k, int g
     return reinterpret_cast<int *>((reinterpret_cast<uintptr_t>(after) + 255) & ~(uintptr_t)255);
 }
 
-hipError_t lut_search_prefill(const ScanShape &s, int64_t nq, int k, int grid, void *ws,
-                              hipStream_t stream, bool *done) {
-    *done = false;
-    if (nq <= 0 || k > kMaxTopK || query_chunk(s, nq, k, grid) < nq) return hipSuccess;
-    hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, search_bounds(ws, s, nq, k, grid),
-                       nq, (int)(0x807FFFFFu));   // order key of -inf
-    const hipError_t e = hipGetLastError();
-    *done = e == hipSuccess;
-    return e;
+int *lut_search_bounds(const ScanShape &s, int64_t nq, int k, int grid, void *ws) {
+    if (nq <= 0 || k > kMaxTopK || query_chunk(s, nq, k, grid) < nq) return nullptr;
+    return search_bounds(ws, s, nq, k, grid);
 }
 
 hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *scales,
@@ -1384,8 +1387,7 @@ hipError_t lut_search(const ScanShape &s, const uint8_t *blocked, const float *s
         const size_t lds = lds_bytes_for(s, S, split, filter.any());
         hipError_t e = hipSuccess;
         if (!(bounds_ready && q0 == 0 && m == nq)) {
-            hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m,
-                               (int)(0x807FFFFFu));   // order key of -inf
+            hipLaunchKernelGGL(fill_keys, dim3(1), dim3(256), 0, stream, gbound, m, kBoundInit);
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
