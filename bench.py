@@ -341,8 +341,10 @@ def main() -> int:
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the bit-width sweep (encode and search at b = 2, 3, 4, 8)")
     ap.add_argument("--batched-calls", type=int, default=0,
-                    help="after timing, run this many batched (matrix-core) calls of 256 queries "
-                         "at k = 10 (for counter collection with --no-extra)")
+                    help="after timing, run this many batched (matrix-core) calls of "
+                         "--batched-size queries at k = 10 (for counter collection with --no-extra)")
+    ap.add_argument("--batched-size", type=int, default=256,
+                    help="queries per call of --batched-calls (32: one tile, 256: one wide pass)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run three 1 GiB device-to-device copies (a kernel of "
                          "known traffic for scaling the HBM byte counters)")
@@ -496,11 +498,11 @@ def main() -> int:
     if not args.no_extra and not args.no_sweep:
         extra["bit_width_sweep"] = bit_sweep(tq, rot, X, Qrot, k, n, d, stream)
     if args.batched_calls > 0:
-        qb = Qrot[:256].contiguous()
+        qb = Qrot[:args.batched_size].contiguous()
         for _ in range(args.batched_calls):
             idx.search(qb, 10, path="mfma", prerotated=True)
         torch.cuda.synchronize()
-        log("batched calls: %d of 256 queries at k = 10" % args.batched_calls)
+        log("batched calls: %d of %d queries at k = 10" % (args.batched_calls, qb.shape[0]))
     del X
     torch.cuda.empty_cache()
     if args.copy_calibration:

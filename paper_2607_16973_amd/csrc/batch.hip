@@ -70,6 +70,10 @@ constexpr int kTableBytes = 256 * 32 * 4;   // byte table, 32 replicas
 constexpr int SEL_THREADS = 256;
 constexpr int SEL_GROUPS = 32;     // select workgroups per query
 constexpr int kBoundStride = 32;  // ints between the global bounds of two queries
+constexpr int kTicketStride = 32;  // ints between two workgroups' ticket counters (own 128 B line)
+// Last word of a raw buffer resource (stride 0, byte offsets): 32-bit data
+// format, so untyped loads, stores and atomics are bounds-checked by bytes.
+constexpr int kBufferWord3 = 0x00020000;
 constexpr int kBuf = 8 * 64 + 64;  // per-wave candidate buffer: one load of 8 scores per lane + a partial 64
 constexpr int kKeepVmemB = 0x1 | 0x2 | 0x4 | 0x8 | 0x80 | 0x100 | 0x200 | 0x400;
 
@@ -106,11 +110,13 @@ struct QInfo {
 // certificate is checked.
 __global__ void prep_kernel(const float *__restrict__ Q, int nq, int d, const float *smax_p,
                             float cmax16, float dmax, _Float16 *__restrict__ q16,
-                            QInfo *__restrict__ info) {
+                            QInfo *__restrict__ info, int *__restrict__ zero, int nzero) {
     __shared__ float red_m[SEL_THREADS / 64];
     __shared__ double red_1[SEL_THREADS / 64], red_2[SEL_THREADS / 64];
     const int q = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (q == 0)
+        for (int i = tid; i < nzero; i += SEL_THREADS) zero[i] = 0;   // the score kernel's tickets
     const float *row = Q + (int64_t)q * d;
     float m = 0.f;
     double s1 = 0.0, s2 = 0.0;
@@ -181,8 +187,9 @@ struct ScoreParams {
     const _Float16 *q16;       // [nqt][d]
     const QInfo *info;         // [nqt]
     const float *cents;        // 16 levels
-    _Float16 *out;             // [kTile][npad] approximate scores / norm
+    _Float16 *out;             // [kTile][npad] approximate scores / norm (rows >= nqt: 0)
     _Float16 *bmax;            // [kTile][nblk] per-block maximum of out (vectors < n)
+    int *tickets;              // [grid * kTicketStride] block ticket counters, zero at launch
     int64_t n, nblk, npad;
     int d, chunks, nqt;
 };
@@ -190,40 +197,70 @@ struct ScoreParams {
 // Float16 centroids of the 8 4-bit fields of a stored word w (the canonical
 // word rotated left by 2): element t is coordinate t of the word.  The byte
 // table holds, for every byte value e, the pair (c[e & 15], c[e >> 4]) as
-// two float16 -- one lookup per two coordinates.  It is replicated 32 times
-// so that lane i reads only LDS bank i mod 32 (entry e of replica i is the
-// 32-bit word e * 32 + i): lookups of random bytes by different lanes never
-// meet in a bank.  `lb` is the lane's byte offset (lane mod 32) * 4.
-__device__ inline half8 dequant8(uint32_t w, uint32_t lb) {
+// two float16 -- one lookup per two coordinates.  It is replicated NR times
+// so that the lanes of a read meet distinct LDS banks whatever bytes they
+// look up (entry e of replica i is the 32-bit word e * NR + i, read by lane
+// i mod NR).
+//  NR = 64: the word address e * 256 + 4 * lane has the byte e in byte 1 and
+//    the lane's offset `lb` = 4 * lane in byte 0, so one byte permute of the
+//    canonical word and lb forms it (64 KiB of table).
+//  NR = 32: ((e << 7) | lb), lb = 4 * (lane mod 32), takes a shift or
+//    field extract and an and-or per lookup (32 KiB of table).
+template <int NR>
+__device__ inline half8 dequant8_canonical(uint32_t cw, uint32_t lb) {
     typedef __attribute__((address_space(3))) const uint32_t lds_u32;
-    const uint32_t cw = __builtin_amdgcn_alignbit(w, w, 2);   // canonical word
     union {
         uint32_t u[4];
         half8 h;
     } r;
-    r.u[0] = *(lds_u32 *)(uintptr_t)(((cw << 7) & 0x7F80u) | lb);
-    r.u[1] = *(lds_u32 *)(uintptr_t)(((cw >> 1) & 0x7F80u) | lb);
-    r.u[2] = *(lds_u32 *)(uintptr_t)(((cw >> 9) & 0x7F80u) | lb);
-    r.u[3] = *(lds_u32 *)(uintptr_t)(((cw >> 17) & 0x7F80u) | lb);
+    if constexpr (NR == 64) {
+        // v_perm selector: byte 0 <- lb byte 0, byte 1 <- cw byte b, bytes 2, 3 <- 0
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            r.u[b] = *(lds_u32 *)(uintptr_t)__builtin_amdgcn_perm(cw, lb, 0x0C0C0400u + (b << 8));
+    } else {
+        r.u[0] = *(lds_u32 *)(uintptr_t)(((cw << 7) & 0x7F80u) | lb);
+        r.u[1] = *(lds_u32 *)(uintptr_t)(((cw >> 1) & 0x7F80u) | lb);
+        r.u[2] = *(lds_u32 *)(uintptr_t)(((cw >> 9) & 0x7F80u) | lb);
+        r.u[3] = *(lds_u32 *)(uintptr_t)(((cw >> 17) & 0x7F80u) | lb);
+    }
     return r.h;
+}
+template <int NR>
+__device__ inline half8 dequant8(uint32_t w, uint32_t lb) {
+    return dequant8_canonical<NR>(__builtin_amdgcn_alignbit(w, w, 2), lb);   // canonical word
+}
+
+// Copies of a ring slot's four words into registers of their own.  The
+// exchanges below overwrite their operands in place; on the slot itself they
+// make the register allocator move the slot's refill into other registers
+// and copy it back at the loop's back edge, which waits for every load in
+// flight (the ring drains once per eight chunks).  An opaque copy frees the
+// slot for its refill at once.
+__device__ inline void copy4(const uint4 &v, uint32_t &a, uint32_t &b, uint32_t &c, uint32_t &d) {
+    asm volatile("v_mov_b32 %0, %4\n\tv_mov_b32 %1, %5\n\tv_mov_b32 %2, %6\n\tv_mov_b32 %3, %7"
+                 : "=v"(a), "=v"(b), "=v"(c), "=v"(d)
+                 : "v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w));
+}
+
+// Replicas of the score kernel's byte table: 64 where the table (64 KiB)
+// and the query tile (kTile x d float16) fit the 160 KiB of LDS together.
+__host__ __device__ constexpr int score_replicas(int d) {
+    return 64 * 1024 + kTile * d * 2 <= 160 * 1024 ? 64 : 32;
 }
 
 // One workgroup of 12 waves per compute unit.  The byte table and the query
-// tile (32 rows of d float16, rows padded by 16 bytes so the 16 rows read by
-// one instruction fall in distinct banks) stay in LDS.  Waves claim the workgroup's
-// 64-vector blocks one at a time from an LDS counter (one ahead, so the ring
-// of MF_RING chunk loads runs on into the next block).  For a chunk, lane 16m+i
-// (row m of 16 lanes) has loaded the 4 words of vector 16m+i; a 4 x 4
-// transpose across the rows (two v_permlane32_swap, then two
-// v_permlane16_swap) leaves word q of vectors i, 16+i, 32+i, 48+i in lane
-// 16q+i: the B operands (k = 8q..8q+7, column i) of the four 16-vector
-// MFMAs.
+// tile stay in LDS; the tile is stored in the A-operand order of the MFMAs
+// (chunk c, row tile t: 64 lanes x 16 bytes, lane 16 kq + i holding row
+// 16 t + i, k = 32 c + 8 kq .. + 7), so each operand read is one 16-byte read
+// per lane at consecutive addresses.  Waves claim the workgroup's 64-vector
+// blocks one at a time from the workgroup's ticket counter in memory (one
+// ahead, so the ring of MF_RING chunk loads runs on into the next block).
+template <int NR>
 __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    const int ld = p.d + 8;                                   // row stride in halves
-    uint32_t *T = reinterpret_cast<uint32_t *>(smem);          // byte table x 32, at 0
-    _Float16 *Qs = reinterpret_cast<_Float16 *>(smem + kTableBytes);   // [kTile][ld]
-    int *ctr = reinterpret_cast<int *>(smem + kTableBytes + (size_t)kTile * ld * 2);
+    uint32_t *T = reinterpret_cast<uint32_t *>(smem);                    // byte table, at 0
+    uint4 *Qf = reinterpret_cast<uint4 *>(smem + (size_t)NR * 256 * 4);   // [chunk][2][64]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -232,21 +269,22 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
     const int64_t gb0 = p.nblk * g / G, gb1 = p.nblk * (g + 1) / G;
     const int nbw = (int)(gb1 - gb0);
 
-    // query tile, zero rows past nqt
-    for (int e = tid; e < kTile * (p.d / 8); e += MF_THREADS) {
-        const int r = e / (p.d / 8), c8 = e - r * (p.d / 8);
+    // query tile in operand order, zero rows past nqt
+    for (int e = tid; e < CH * 128; e += MF_THREADS) {
+        const int c = e >> 7, t = (e >> 6) & 1, l = e & 63;
+        const int r = 16 * t + (l & 15);
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < p.nqt) v = reinterpret_cast<const uint4 *>(p.q16 + (int64_t)r * p.d)[c8];
-        *reinterpret_cast<uint4 *>(Qs + r * ld + c8 * 8) = v;
+        if (r < p.nqt)
+            v = *reinterpret_cast<const uint4 *>(p.q16 + (int64_t)r * p.d + 32 * c + 8 * (l >> 4));
+        Qf[e] = v;
     }
-    for (int e = tid; e < 256 * 32; e += MF_THREADS) {
-        const int v = e >> 5;   // byte value; e & 31 is the replica
+    for (int e = tid; e < 256 * NR; e += MF_THREADS) {
+        const int v = e / NR;   // byte value; e % NR is the replica
         const uint32_t lo = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v & 15]);
         const uint32_t hi = __builtin_bit_cast(uint16_t, (_Float16)p.cents[v >> 4]);
         T[e] = lo | (hi << 16);
     }
-    const uint32_t lb = (uint32_t)(lane & 31) * 4;
-    if (tid == 0) *ctr = 0;
+    const uint32_t lb = (uint32_t)(lane & (NR - 1)) * 4;
     // per-lane query factors: tile t, rows 4*(lane/16) + r
     float qf[2][4];
 #pragma unroll
@@ -259,15 +297,20 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
         }
     __syncthreads();
 
+    // The ticket is a buffer atomic issued by every lane, of which only lane
+    // 0's lies inside the 4-byte buffer: bounds checking drops the others'
+    // adds (their value is 0).  An atomic under a branch on lane 0 instead
+    // leaves the wait-count pass unsure of the loads in flight, and it then
+    // drains the chunk ring inside the chunk loop.
+    const __amdgpu_buffer_rsrc_t trs =
+        __builtin_amdgcn_make_buffer_rsrc(p.tickets + g * kTicketStride, 0, 4, kBufferWord3);
     auto take = [&]() {
-        int v = 0;
-        if (lane == 0) v = atomicAdd(ctr, 1);
-        return v;
+        return __builtin_amdgcn_raw_ptr_buffer_atomic_add_i32(1, trs, lane == 0 ? 0 : 4, 0, 0);
     };
     int cur = __builtin_amdgcn_readfirstlane(take());
     if (cur >= nbw) return;
     int nxt = __builtin_amdgcn_readfirstlane(take());
-    const uint4 *bsrc = p.codes + (gb0 + cur) * CH * 64;
+    const uint4 *bsrc = p.codes + (gb0 + cur) * CH * 64;   // uniform: the block's chunk 0
     // the ring: named registers (an array would end up in scratch)
     uint4 rb0, rb1, rb2, rb3, rb4, rb5, rb6, rb7;
 #define TQ_RING_LOAD(R, I)                          \
@@ -282,9 +325,8 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
     TQ_RING_LOAD(rb6, 6)
     TQ_RING_LOAD(rb7, 7)
 #undef TQ_RING_LOAD
+    const uint4 *qa = Qf + lane;
     const int qrow = lane & 15, kq = lane >> 4;
-    const _Float16 *qa0 = Qs + qrow * ld + kq * 8;
-    const _Float16 *qa1 = Qs + (16 + qrow) * ld + kq * 8;
     while (true) {
         const int64_t blk = gb0 + cur;
         // the block after this one (or this one again past the end: cache hits)
@@ -308,21 +350,28 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
             // W_q (row m) = word q of vector 16m+i.  permlane32_swap(a, b)
             // exchanges a's rows 2, 3 with b's rows 0, 1; permlane16_swap(a, b)
             // exchanges a's rows 1, 3 with b's rows 0, 2.  After both levels
-            // r[m] (row q) = W_q (row m).
-            const auto s02 = __builtin_amdgcn_permlane32_swap(slot.x, slot.z, false, false);
-            const auto s13 = __builtin_amdgcn_permlane32_swap(slot.y, slot.w, false, false);
+            // r[m] (row q) = W_q (row m): word q of vectors i, 16+i, 32+i,
+            // 48+i in lane 16q+i, the B operands (k = 8q..8q+7, column i) of
+            // the four 16-vector MFMAs.  The exchanges work on copies, and the
+            // slot is refilled right after the copy.
+            uint32_t cx, cy, cz, cw;
+            copy4(slot, cx, cy, cz, cw);
+            // refill MF_RING chunks ahead: this block, then the next one
+            {
+                const int nc = c + MF_RING;
+                slot = load_stream((nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64) + lane);
+                __builtin_amdgcn_sched_barrier(kKeepVmemB);
+            }
+            const auto s02 = __builtin_amdgcn_permlane32_swap(cx, cz, false, false);
+            const auto s13 = __builtin_amdgcn_permlane32_swap(cy, cw, false, false);
             const auto t01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
             const auto t23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
             const uint32_t r[4] = {t01[0], t01[1], t23[0], t23[1]};
-            // refill MF_RING chunks ahead: this block, then the next one
-            const int nc = c + MF_RING;
-            slot = load_stream((nc < CH ? bsrc + nc * 64 : nsrc + (nc - CH) * 64) + lane);
-            __builtin_amdgcn_sched_barrier(kKeepVmemB);
-            const half8 a0 = *reinterpret_cast<const half8 *>(qa0 + c * 32);
-            const half8 a1 = *reinterpret_cast<const half8 *>(qa1 + c * 32);
+            const half8 a0 = __builtin_bit_cast(half8, qa[c * 128]);
+            const half8 a1 = __builtin_bit_cast(half8, qa[c * 128 + 64]);
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-                const half8 b = dequant8(r[m], lb);
+                const half8 b = dequant8<NR>(r[m], lb);
                 acc[0][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, b, acc[0][m], 0, 0, 0);
                 acc[1][m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, b, acc[1][m], 0, 0, 0);
             }
@@ -338,7 +387,12 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
             chunk(c0 + 6, rb6);
             chunk(c0 + 7, rb7);
         }
-        // lane holds vectors 16m + qrow, queries 16t + 4*kq + r
+        // lane holds vectors 16m + qrow, queries 16t + 4*kq + r.  The stores
+        // are unconditional (rows past nqt are zero scores in rows that the
+        // workspace holds and nothing reads; the 16 lanes of a row store the
+        // same block maximum): a store under a branch leaves the wait-count
+        // pass unsure of the loads in flight, and it then drains the chunk
+        // ring inside the chunk loop.
         float mx[2][4];
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -354,7 +408,7 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
                 for (int r = 0; r < 4; ++r) {
                     const int q = 16 * t + 4 * kq + r;
                     const _Float16 h = (_Float16)(acc[t][m][r] * scl[m] * qf[t][r]);
-                    if (q < p.nqt) p.out[(int64_t)q * p.npad + v] = h;
+                    p.out[(int64_t)q * p.npad + v] = h;
                     mx[t][r] = fmaxf(mx[t][r], vin ? (float)h : -INFINITY);
                 }
         }
@@ -370,7 +424,7 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
                 x = fmaxf(x, dpp_f<kDppRowRor2>(x));
                 x = fmaxf(x, dpp_f<kDppRowRor1>(x));
                 const int q = 16 * t + 4 * kq + r;
-                if (qrow == 0 && q < p.nqt) p.bmax[(int64_t)q * p.nblk + blk] = (_Float16)x;
+                p.bmax[(int64_t)q * p.nblk + blk] = (_Float16)x;
             }
         if (nxt >= nbw) break;
         cur = nxt;
@@ -1208,10 +1262,10 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
             const uint4 w = sb[WS::pos(QF + g) + lane];
             const auto k0 = __builtin_amdgcn_permlane32_swap(w.x, w.y, false, false);
             const auto k1 = __builtin_amdgcn_permlane32_swap(w.z, w.w, false, false);
-            b[0] = dequant8(k0[0], lb);   // vectors 0..31, k-half 0
-            b[1] = dequant8(k1[0], lb);   // vectors 0..31, k-half 1
-            b[2] = dequant8(k0[1], lb);   // vectors 32..63, k-half 0
-            b[3] = dequant8(k1[1], lb);   // vectors 32..63, k-half 1
+            b[0] = dequant8<32>(k0[0], lb);   // vectors 0..31, k-half 0
+            b[1] = dequant8<32>(k1[0], lb);   // vectors 0..31, k-half 1
+            b[2] = dequant8<32>(k0[1], lb);   // vectors 32..63, k-half 0
+            b[3] = dequant8<32>(k1[1], lb);   // vectors 32..63, k-half 1
         };
 #pragma unroll 1
         for (int x = 0; x < PD; ++x) request();
@@ -1370,10 +1424,10 @@ __global__ __launch_bounds__(WD_THREADS) void wide_scores_kernel(WideParams p) {
                         if (grp == 0) {
                             const auto k0 = __builtin_amdgcn_permlane32_swap(wn.x, wn.y, false, false);
                             const auto k1 = __builtin_amdgcn_permlane32_swap(wn.z, wn.w, false, false);
-                            bnext[0] = dequant8(k0[0], lb);
-                            bnext[1] = dequant8(k1[0], lb);
-                            bnext[2] = dequant8(k0[1], lb);
-                            bnext[3] = dequant8(k1[1], lb);
+                            bnext[0] = dequant8<32>(k0[0], lb);
+                            bnext[1] = dequant8<32>(k1[0], lb);
+                            bnext[2] = dequant8<32>(k0[1], lb);
+                            bnext[3] = dequant8<32>(k1[1], lb);
                         }
                         if (grp == 1) {
                             request_base();
@@ -1739,7 +1793,7 @@ void with_slots(int KC, Fn fn) {
 }
 
 struct BatchLayout {
-    size_t q16, info, approx, bmax, cand_s, cand_i, top_i, amin, state, gbound, flags, rows, qc,
+    size_t q16, info, approx, bmax, cand_s, cand_i, top_i, amin, state, gbound, tickets, flags, rows, qc,
         allow_c, ids_c, scores_c, lut, total;
     // wide passes
     size_t w_q16, w_info, w_qfrag, w_qf, w_pil, w_theta, w_pcn, w_pci, w_pcs, w_cs, w_ci, w_cn,
@@ -1802,6 +1856,8 @@ BatchLayout batch_layout(const ScanShape &s, int64_t nq, int k, int grid) {
     o += align256((size_t)kTile * 4);
     L.gbound = o;
     o += align256(kTile * kBoundStride * 4);
+    L.tickets = o;
+    o += align256((size_t)grid * kTicketStride * 4);
     L.flags = o;
     o += align256((size_t)nq * 4);
     L.rows = o;
@@ -1876,13 +1932,13 @@ hipError_t launch_wide_scores(int QP, const WideParams &wp, int grid, hipStream_
 
 }  // namespace
 
-// LDS of the score kernel: replicated byte table, query tile, counter.
+// LDS of the score kernel: replicated byte table and query tile.
 size_t score_lds_bytes(int d) {
-    return kTableBytes + (size_t)kTile * (d + 8) * 2 + 16;
+    return (size_t)score_replicas(d) * 256 * 4 + (size_t)kTile * d * 2;
 }
 
 bool mfma_search_supported(const ScanShape &s, int k) {
-    return s.bits == 4 && s.chunks % 8 == 0 && k <= kMaxBatchK && s.W <= 64 &&
+    return s.bits == 4 && s.chunks % 8 == 0 && k <= kMaxBatchK && s.W <= 64 && s.d <= 1792 &&
            score_lds_bytes(s.d) <= 160 * 1024;
 }
 
@@ -1917,6 +1973,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     float *amin = reinterpret_cast<float *>(w8 + L.amin);
     int *state = reinterpret_cast<int *>(w8 + L.state);
     int *gbound = reinterpret_cast<int *>(w8 + L.gbound);
+    int *tickets = reinterpret_cast<int *>(w8 + L.tickets);
     int *flags = reinterpret_cast<int *>(w8 + L.flags);
     const int64_t npad = approx_row(s);
     const size_t lds_scores = score_lds_bytes(s.d);
@@ -1925,8 +1982,11 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
     const size_t lds_rescore = (size_t)s.chunks * 2048 + 16 * 4 + (size_t)KC * 12 + 16;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)mfma_scores_kernel,
+        hipError_t e = hipFuncSetAttribute((const void *)mfma_scores_kernel<64>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)mfma_scores_kernel<32>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         for (int S = 1; S <= 8 && e == hipSuccess; S *= 2)
             with_slots(64 * S, [&](auto sc) {
                 e = hipFuncSetAttribute((const void *)rescore_kernel<decltype(sc)::value>,
@@ -1991,7 +2051,8 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
             int *wstate = reinterpret_cast<int *>(w8 + L.w_state);
             const uint64_t *allow_p = allow ? allow + q0 * s.W : nullptr;
             hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream,
-                               Qrot + q0 * s.d, nqt, s.d, smax, cmax16, dmax, wq16, winfo);
+                               Qrot + q0 * s.d, nqt, s.d, smax, cmax16, dmax, wq16, winfo,
+                               nullptr, 0);
             const int64_t fr = (int64_t)(s.d / 32) * QP * 4;
             hipLaunchKernelGGL(frag_kernel, dim3((int)std::min<int64_t>((fr + 255) / 256, 1024)),
                                dim3(256), 0, stream, wq16, winfo, nqt, QP, s.d, wqfrag, wqf);
@@ -2065,7 +2126,7 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         }
         const int nqt = (int)std::min<int64_t>(nq - q0, kTile);
         hipLaunchKernelGGL(prep_kernel, dim3(nqt), dim3(SEL_THREADS), 0, stream, Qrot + q0 * s.d,
-                           nqt, s.d, smax, cmax16, dmax, q16, info);
+                           nqt, s.d, smax, cmax16, dmax, q16, info, tickets, grid * kTicketStride);
         ScoreParams sp{};
         sp.codes = reinterpret_cast<const uint4 *>(blocked);
         sp.scales = scales;
@@ -2080,7 +2141,13 @@ hipError_t mfma_search(const ScanShape &s, const uint8_t *blocked, const float *
         sp.d = s.d;
         sp.chunks = s.chunks;
         sp.nqt = nqt;
-        hipLaunchKernelGGL(mfma_scores_kernel, dim3(grid), dim3(MF_THREADS), lds_scores, stream, sp);
+        sp.tickets = tickets;
+        if (score_replicas(s.d) == 64)
+            hipLaunchKernelGGL(mfma_scores_kernel<64>, dim3(grid), dim3(MF_THREADS), lds_scores,
+                               stream, sp);
+        else
+            hipLaunchKernelGGL(mfma_scores_kernel<32>, dim3(grid), dim3(MF_THREADS), lds_scores,
+                               stream, sp);
         if (allow) {
             // the block maxima ignore the allowlist: select over every allowed score
             hipLaunchKernelGGL(fill_order_keys, dim3(1), dim3(64), 0, stream, gbound, nqt);
