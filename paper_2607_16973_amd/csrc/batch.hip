@@ -327,7 +327,9 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
 #undef TQ_RING_LOAD
     const uint4 *qa = Qf + lane;
     const int qrow = lane & 15, kq = lane >> 4;
-    while (true) {
+    // a wave scores at most the workgroup's nbw blocks: the bound ends the
+    // loop even if the tickets were to stop advancing
+    for (int iter = 1;; ++iter) {
         const int64_t blk = gb0 + cur;
         // the block after this one (or this one again past the end: cache hits)
         const uint4 *nsrc = nxt < nbw ? p.codes + (gb0 + nxt) * CH * 64 : bsrc;
@@ -426,7 +428,7 @@ __global__ __launch_bounds__(MF_THREADS) void mfma_scores_kernel(ScoreParams p) 
                 const int q = 16 * t + 4 * kq + r;
                 p.bmax[(int64_t)q * p.nblk + blk] = (_Float16)x;
             }
-        if (nxt >= nbw) break;
+        if (nxt >= nbw || iter >= nbw) break;
         cur = nxt;
         nxt = __builtin_amdgcn_readfirstlane(ticket);
         bsrc = nsrc;
