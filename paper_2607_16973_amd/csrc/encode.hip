@@ -501,56 +501,106 @@ __device__ inline int exact_code(double S, double nrm, int j, int d, const doubl
     return c;
 }
 
-// Exact recomputation of flagged coordinates, one thread per flag (one
-// wave per output tile): the sequential float64 sum of the definition
-// (products of float32 values are exact in float64, so fused and unfused
-// multiply-adds agree).  Each thread streams its X row and R row AHEAD
-// 16-byte pieces ahead, so that the loads of a flag overlap instead of
-// following one another (d/4 is a multiple of AHEAD).
-constexpr int FIX_AHEAD = 16;
+// Exact recomputation of flagged coordinates (b <= 4): the sequential
+// float64 sum of the definition (products of float32 values are exact in
+// float64, so fused and unfused multiply-adds agree).  One wave per output
+// tile takes the tile's flags in batches of FX_FB, and for each slab of FX_KS
+// coordinates every lane loads 16-byte pieces of the batch's X rows and R
+// rows (lane l: piece 4 i + l / 16 of the row of flag l mod 16, so that one
+// load instruction reads 64 contiguous bytes of 16 rows).  The pieces are
+// staged in LDS piece-major (piece q of flag f at 16 (q FX_FB + f) bytes:
+// the 16 lanes that sum read one piece at contiguous addresses) and lane f
+// adds its flag's products in k order.  Two slabs are in registers while
+// one is summed.
+constexpr int FX_FB = 16;                    // flags per batch
+constexpr int FX_KS = 64;                    // coordinates per slab (d is a multiple of 64)
+constexpr int FX_PQ = FX_KS / 4;             // 16-byte pieces of a row slab
+constexpr int FX_LD = FX_FB * FX_PQ / 64;    // load instructions per operand and slab
 
-__global__ __launch_bounds__(64) void fixup_kernel(
+struct FxSlab {
+    f4 x[FX_LD], r[FX_LD];
+};
+
+__global__ __launch_bounds__(64) void fixup_batch_kernel(
     const float *__restrict__ X, const float *__restrict__ R, int d, int ncol,
     const double *__restrict__ bounds, const double *__restrict__ athr, int levels,
     const double *__restrict__ norms,
     const uint32_t *__restrict__ flags, const unsigned int *__restrict__ tile_count,
     uint8_t *__restrict__ codes_tmp) {
+    __shared__ f4 xs[FX_FB * FX_PQ], rs[FX_FB * FX_PQ];
     const int tile = blockIdx.x;
+    const int lane = threadIdx.x;
     const int64_t row0 = (int64_t)(tile / ncol) * BM;
     const int col0 = (tile % ncol) * BN;
-    const unsigned int cnt = tile_count[tile];
+    const int cnt = (int)tile_count[tile];
     const uint32_t *tflags = flags + (int64_t)tile * (BM * BN);
-    const int nq = d / 4;
-    for (unsigned int e = threadIdx.x; e < cnt; e += 64) {
-        const uint32_t f = tflags[e];
-        const int64_t row = row0 + (f >> 7);
-        const int j = col0 + (int)(f & 127);
-        const f4 *xr = reinterpret_cast<const f4 *>(X + row * d);
-        const f4 *rr = reinterpret_cast<const f4 *>(R + (int64_t)j * d);
-        f4 bx[FIX_AHEAD], br[FIX_AHEAD];
+    const int ns = d / FX_KS;
+    for (int e0 = 0; e0 < cnt; e0 += FX_FB) {
+        const int nb = cnt - e0 < FX_FB ? cnt - e0 : FX_FB;
+        // the flag whose rows this lane loads, and the one it sums
+        const int lf = (lane & (FX_FB - 1)) < nb ? (lane & (FX_FB - 1)) : nb - 1;
+        const uint32_t fl = tflags[e0 + lf];
+        const float *xrow = X + (row0 + (fl >> 7)) * d + 4 * (lane / FX_FB);
+        const float *rrow = R + (int64_t)(col0 + (int)(fl & 127)) * d + 4 * (lane / FX_FB);
+        const bool act = lane < nb;
+        const uint32_t mf = tflags[e0 + (act ? lane : 0)];
+        auto load = [&](int sl, FxSlab &b) {
 #pragma unroll
-        for (int u = 0; u < FIX_AHEAD; ++u) {
-            bx[u] = xr[u];
-            br[u] = rr[u];
-        }
+            for (int i = 0; i < FX_LD; ++i) {
+                b.x[i] = *reinterpret_cast<const f4 *>(xrow + sl * FX_KS + 16 * i);
+                b.r[i] = *reinterpret_cast<const f4 *>(rrow + sl * FX_KS + 16 * i);
+            }
+        };
+        // the barriers order the lanes' LDS accesses (a lane sums pieces
+        // that other lanes staged): the previous slab's reads, the writes,
+        // then the reads of the new slab; they leave the loads in flight
+        auto stage = [&](const FxSlab &b) {
+            lds_barrier();
+#pragma unroll
+            for (int i = 0; i < FX_LD; ++i) {
+                xs[64 * i + lane] = b.x[i];
+                rs[64 * i + lane] = b.r[i];
+            }
+            lds_barrier();
+            // the refill of these registers stays after the writes: moved
+            // ahead, it would take other registers and the loop would copy
+            // them back at its back edge, waiting for every load in flight
+            __builtin_amdgcn_sched_barrier(0);
+        };
         double S = 0.0;
-        for (int q0 = 0; q0 < nq; q0 += FIX_AHEAD) {
+        auto sum = [&]() {
+            if (act) {
 #pragma unroll
-            for (int u = 0; u < FIX_AHEAD; ++u) {
-                const f4 a = br[u];
-                const f4 b = bx[u];
-                if (q0 + FIX_AHEAD + u < nq) {
-                    bx[u] = xr[q0 + FIX_AHEAD + u];
-                    br[u] = rr[q0 + FIX_AHEAD + u];
-                }
+                for (int q = 0; q < FX_PQ; ++q) {
+                    const f4 a = rs[q * FX_FB + lane];
+                    const f4 b = xs[q * FX_FB + lane];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const double prod = (double)a[c] * (double)b[c];
-                    S = S + prod;
+                    for (int c = 0; c < 4; ++c) {
+                        const double prod = (double)a[c] * (double)b[c];
+                        S = S + prod;
+                    }
                 }
             }
+        };
+        // the loads are unconditional (clamped slab), so the waits count
+        // them exactly
+        FxSlab b0, b1;
+        load(0, b0);
+        __builtin_amdgcn_sched_barrier(0);   // b0's loads all ahead of b1's
+        load(ns > 1 ? 1 : 0, b1);
+        for (int sl = 0; sl < ns; sl += 2) {
+            stage(b0);
+            load(sl + 2 < ns ? sl + 2 : ns - 1, b0);
+            sum();
+            if (sl + 1 < ns) stage(b1);
+            load(sl + 3 < ns ? sl + 3 : ns - 1, b1);
+            if (sl + 1 < ns) sum();
         }
-        codes_tmp[row * d + j] = (uint8_t)exact_code(S, norms[row], j, d, bounds, athr, levels);
+        if (act) {
+            const int64_t row = row0 + (mf >> 7);
+            const int j = col0 + (int)(mf & 127);
+            codes_tmp[row * d + j] = (uint8_t)exact_code(S, norms[row], j, d, bounds, athr, levels);
+        }
     }
 }
 
@@ -878,8 +928,8 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                                X + r0 * d, m, R, d, ncol, bounds, calib.athr, cb.levels, norms,
                                flags, tile_count, codes_tmp);
         else
-            hipLaunchKernelGGL(fixup_kernel, dim3(nrt * ncol), dim3(64), 0, stream, X + r0 * d, R,
-                               d, ncol, bounds, calib.athr, cb.levels, norms, flags, tile_count,
+            hipLaunchKernelGGL(fixup_batch_kernel, dim3(nrt * ncol), dim3(64), 0, stream, X + r0 * d,
+                               R, d, ncol, bounds, calib.athr, cb.levels, norms, flags, tile_count,
                                codes_tmp);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
