@@ -511,13 +511,13 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
     if (p.nq == 0) return;
     QueryRegs<MODE> qv;
     load_query<MODE>(table_shape(p), p.qrot, qv);
+    const float qc0 = qconst_of(p, 0);
     query_abs_sum<MODE>(red, qv);
-    __syncthreads();
-    int sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qconst_of(p, 0));
     __syncthreads();
 
     // this wave's current and next work items, and the ring holding the
-    // current one's 8 chunks
+    // current one's 8 chunks: claimed and requested before the first table
+    // is built, so that the build overlaps the first loads
     int tk = __builtin_amdgcn_readfirstlane(take(misc + 1));
     int nxt = __builtin_amdgcn_readfirstlane(take(misc + 1));
     // wave-uniform base of a group; each lane adds its 16-byte slot
@@ -530,6 +530,8 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
             __builtin_amdgcn_sched_barrier(kKeepVmem);
         }
     }
+    int sh = build_int_table<MODE>(lds, red, cents_s, table_shape(p), qv, qc0);
+    __syncthreads();
     for (int qi = 0; qi < p.nq; ++qi) {
         WaveTopK<S> top;
         top.reset();
