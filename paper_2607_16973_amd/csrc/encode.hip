@@ -668,7 +668,84 @@ __global__ __launch_bounds__(GEMM_THREADS) void fixup_tile_kernel(
     }
 }
 
-// Packs PACK_ROWS rows per workgroup: scale, canonical bitstream, blocked layout.
+// Packs one row per thread, 64 rows per one-wave workgroup, for the bit
+// widths whose 16-byte blocked chunk holds 128 / BITS codes as 4 words of
+// 32 / BITS codes (BITS in {1, 2, 4, 8}; the canonical words are the same
+// words): each lane walks its row's chunks in j order, adds fl64(c_code^2)
+// (or the calibrated reconstruction's square) to the scale sum of the
+// definition in j order, and writes the chunk's 16 bytes to the canonical
+// and blocked layouts.  Every row of a chunk of rows is in flight at once,
+// so the sequential sums (one dependent float64 add per code) overlap; the
+// next chunk's codes are loaded while one is summed.
+template <int BITS>
+__global__ __launch_bounds__(64) void pack_rows_kernel(
+    const uint8_t *__restrict__ codes_tmp, int64_t m, int d,
+    const double *__restrict__ cent_sq, const double *__restrict__ ysq,
+    const double *__restrict__ norms,
+    uint8_t *__restrict__ canon, float *__restrict__ scales,
+    uint8_t *__restrict__ blocked, float *__restrict__ blocked_scales, int64_t base,
+    int chunks) {
+    constexpr int L = 1 << BITS;
+    constexpr int CPC = 128 / BITS;   // codes per chunk
+    constexpr int LPC = CPC / 16;     // 16-byte loads of one-byte codes per chunk
+    constexpr int PER = 32 / BITS;    // codes per word
+    __shared__ double csq_s[L];
+    const int lane = threadIdx.x;
+    for (int i = lane; i < L; i += 64) csq_s[i] = ysq ? 0.0 : cent_sq[i];
+    __syncthreads();
+    const int64_t r = (int64_t)blockIdx.x * 64 + lane;
+    if (r >= m) return;
+    const uint4 *src = reinterpret_cast<const uint4 *>(codes_tmp + r * d);
+    const int64_t v = base + r;
+    uint8_t *bdst = blocked ? blocked + (v >> 6) * chunks * 1024 + (v & 63) * 16 : nullptr;
+    uint8_t *cdst = canon ? canon + r * (int64_t)(d * BITS / 8) : nullptr;
+    double h2 = 0.0;
+    auto run = [&](auto cal_t) {
+        constexpr bool CAL = decltype(cal_t)::value;
+        uint4 cur[LPC], nxt[LPC];
+#pragma unroll
+        for (int i = 0; i < LPC; ++i) cur[i] = src[i];
+        for (int ch = 0; ch < chunks; ++ch) {
+            const int cn = ch + 1 < chunks ? ch + 1 : ch;
+#pragma unroll
+            for (int i = 0; i < LPC; ++i) nxt[i] = src[cn * LPC + i];
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int t = 0; t < CPC; ++t) {
+                const uint4 &q = cur[t >> 4];
+                const int u = (t >> 2) & 3;
+                const uint32_t word = u == 0 ? q.x : u == 1 ? q.y : u == 2 ? q.z : q.w;
+                const uint32_t code = (word >> (8 * (t & 3))) & 255u;
+                w[t / PER] |= code << (BITS * (t % PER));
+                double sq;
+                if constexpr (CAL)
+                    sq = ysq[(int64_t)(ch * CPC + t) * L + code];
+                else
+                    sq = csq_s[code];
+                h2 = h2 + sq;
+            }
+            if (cdst) *reinterpret_cast<uint4 *>(cdst + ch * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+            if (bdst) {
+                if (blocked_rotated(BITS))
+                    for (int u = 0; u < 4; ++u) w[u] = rotl2(w[u]);
+                *reinterpret_cast<uint4 *>(bdst + ch * 1024) = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+#pragma unroll
+            for (int i = 0; i < LPC; ++i) cur[i] = nxt[i];
+        }
+    };
+    if (ysq)
+        run(std::true_type{});
+    else
+        run(std::false_type{});
+    const double nrm = norms[r];
+    const float s = (nrm == 0.0) ? 0.0f : (float)(nrm / std::sqrt(h2));
+    if (scales) scales[r] = s;
+    if (blocked_scales) blocked_scales[base + r] = s;
+}
+
+// Packs PACK_ROWS rows per workgroup (3-bit codes): scale, canonical
+// bitstream, blocked layout.
 // The codes are staged in LDS with a row stride of d + 16 bytes, so that the
 // scale threads (one per row, reading 16 codes at a time) meet different
 // banks.
@@ -933,12 +1010,31 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
                                codes_tmp);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
-        const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);
-        hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * (d + 16), stream,
-                           codes_tmp, m, d, cb.bits, cent_sq, calib.ysq, norms,
-                           out.canonical ? out.canonical + r0 * (int64_t)(d * cb.bits / 8) : nullptr,
-                           out.scales ? out.scales + r0 : nullptr, out.blocked,
-                           out.blocked_scales, out.base + r0, chunks);
+        uint8_t *canon_p = out.canonical ? out.canonical + r0 * (int64_t)(d * cb.bits / 8) : nullptr;
+        float *scales_p = out.scales ? out.scales + r0 : nullptr;
+        const dim3 prow((unsigned)((m + 63) / 64));
+        if (cb.bits == 3) {
+            const int packs = (int)((m + PACK_ROWS - 1) / PACK_ROWS);
+            hipLaunchKernelGGL(pack_kernel, dim3(packs), dim3(256), PACK_ROWS * (d + 16), stream,
+                               codes_tmp, m, d, cb.bits, cent_sq, calib.ysq, norms, canon_p, scales_p,
+                               out.blocked, out.blocked_scales, out.base + r0, chunks);
+        } else if (cb.bits == 1) {
+            hipLaunchKernelGGL(pack_rows_kernel<1>, prow, dim3(64), 0, stream, codes_tmp, m, d, cent_sq,
+                               calib.ysq, norms, canon_p, scales_p, out.blocked, out.blocked_scales,
+                               out.base + r0, chunks);
+        } else if (cb.bits == 2) {
+            hipLaunchKernelGGL(pack_rows_kernel<2>, prow, dim3(64), 0, stream, codes_tmp, m, d, cent_sq,
+                               calib.ysq, norms, canon_p, scales_p, out.blocked, out.blocked_scales,
+                               out.base + r0, chunks);
+        } else if (cb.bits == 4) {
+            hipLaunchKernelGGL(pack_rows_kernel<4>, prow, dim3(64), 0, stream, codes_tmp, m, d, cent_sq,
+                               calib.ysq, norms, canon_p, scales_p, out.blocked, out.blocked_scales,
+                               out.base + r0, chunks);
+        } else {
+            hipLaunchKernelGGL(pack_rows_kernel<8>, prow, dim3(64), 0, stream, codes_tmp, m, d, cent_sq,
+                               calib.ysq, norms, canon_p, scales_p, out.blocked, out.blocked_scales,
+                               out.base + r0, chunks);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
