@@ -506,12 +506,9 @@ __device__ inline int exact_code(double S, double nrm, int j, int d, const doubl
 // float64, so fused and unfused multiply-adds agree).  One wave per output
 // tile takes the tile's flags in batches of FX_FB, and for each slab of FX_KS
 // coordinates every lane loads 16-byte pieces of the batch's X rows and R
-// rows (lane l: piece 4 i + l / 16 of the row of flag l mod 16, so that one
-// load instruction reads 64 contiguous bytes of 16 rows).  The pieces are
-// staged in LDS piece-major (piece q of flag f at 16 (q FX_FB + f) bytes:
-// the 16 lanes that sum read one piece at contiguous addresses) and lane f
-// adds its flag's products in k order.  Two slabs are in registers while
-// one is summed.
+// rows (one load instruction reads the 256-byte slabs of 4 flags' rows).
+// The slabs are staged in LDS and lane f adds its flag's products in k
+// order.  Two slabs are in registers while one is summed.
 constexpr int FX_FB = 16;                    // flags per batch
 constexpr int FX_KS = 64;                    // coordinates per slab (d is a multiple of 64)
 constexpr int FX_PQ = FX_KS / 4;             // 16-byte pieces of a row slab
@@ -527,7 +524,10 @@ __global__ __launch_bounds__(64) void fixup_batch_kernel(
     const double *__restrict__ norms,
     const uint32_t *__restrict__ flags, const unsigned int *__restrict__ tile_count,
     uint8_t *__restrict__ codes_tmp) {
-    __shared__ f4 xs[FX_FB * FX_PQ], rs[FX_FB * FX_PQ];
+    // flag f's slab at [f][FX_PQ + 1]: the padding puts the 16 summing
+    // lanes' reads of one piece 17 pieces apart, in distinct banks
+    constexpr int PS = FX_PQ + 1;
+    __shared__ f4 xs[FX_FB * PS], rs[FX_FB * PS];
     const int tile = blockIdx.x;
     const int lane = threadIdx.x;
     const int64_t row0 = (int64_t)(tile / ncol) * BM;
@@ -537,18 +537,23 @@ __global__ __launch_bounds__(64) void fixup_batch_kernel(
     const int ns = d / FX_KS;
     for (int e0 = 0; e0 < cnt; e0 += FX_FB) {
         const int nb = cnt - e0 < FX_FB ? cnt - e0 : FX_FB;
-        // the flag whose rows this lane loads, and the one it sums
-        const int lf = (lane & (FX_FB - 1)) < nb ? (lane & (FX_FB - 1)) : nb - 1;
-        const uint32_t fl = tflags[e0 + lf];
-        const float *xrow = X + (row0 + (fl >> 7)) * d + 4 * (lane / FX_FB);
-        const float *rrow = R + (int64_t)(col0 + (int)(fl & 127)) * d + 4 * (lane / FX_FB);
+        // load i of a slab: lanes 16 g .. 16 g + 15 read the 256 contiguous
+        // bytes of flag 4 i + g's row slab (piece lane mod 16)
+        const float *xrow[FX_LD], *rrow[FX_LD];
+#pragma unroll
+        for (int i = 0; i < FX_LD; ++i) {
+            const int f = 4 * i + (lane >> 4);
+            const uint32_t fl = tflags[e0 + (f < nb ? f : nb - 1)];
+            xrow[i] = X + (row0 + (fl >> 7)) * d + 4 * (lane & 15);
+            rrow[i] = R + (int64_t)(col0 + (int)(fl & 127)) * d + 4 * (lane & 15);
+        }
         const bool act = lane < nb;
         const uint32_t mf = tflags[e0 + (act ? lane : 0)];
         auto load = [&](int sl, FxSlab &b) {
 #pragma unroll
             for (int i = 0; i < FX_LD; ++i) {
-                b.x[i] = *reinterpret_cast<const f4 *>(xrow + sl * FX_KS + 16 * i);
-                b.r[i] = *reinterpret_cast<const f4 *>(rrow + sl * FX_KS + 16 * i);
+                b.x[i] = *reinterpret_cast<const f4 *>(xrow[i] + sl * FX_KS);
+                b.r[i] = *reinterpret_cast<const f4 *>(rrow[i] + sl * FX_KS);
             }
         };
         // the barriers order the lanes' LDS accesses (a lane sums pieces
@@ -558,8 +563,9 @@ __global__ __launch_bounds__(64) void fixup_batch_kernel(
             lds_barrier();
 #pragma unroll
             for (int i = 0; i < FX_LD; ++i) {
-                xs[64 * i + lane] = b.x[i];
-                rs[64 * i + lane] = b.r[i];
+                const int at = (4 * i + (lane >> 4)) * PS + (lane & 15);
+                xs[at] = b.x[i];
+                rs[at] = b.r[i];
             }
             lds_barrier();
             // the refill of these registers stays after the writes: moved
@@ -572,8 +578,8 @@ __global__ __launch_bounds__(64) void fixup_batch_kernel(
             if (act) {
 #pragma unroll
                 for (int q = 0; q < FX_PQ; ++q) {
-                    const f4 a = rs[q * FX_FB + lane];
-                    const f4 b = xs[q * FX_FB + lane];
+                    const f4 a = rs[lane * PS + q];
+                    const f4 b = xs[lane * PS + q];
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
                         const double prod = (double)a[c] * (double)b[c];
