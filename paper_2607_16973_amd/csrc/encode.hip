@@ -199,36 +199,81 @@ __global__ __launch_bounds__(GEMM_THREADS) void rot_gemm(
 // ------------------------------------------------------------- row norms
 // n = sqrt(sum_k x_k^2) of every row of the chunk: one thread per row adds
 // the squares in k order in float64 (x^2 is exact in float64, so the fused
-// multiply-add rounds exactly as add(fl(x^2))), streaming its row AHEAD
-// 16-byte pieces ahead (d/4 is a multiple of AHEAD).  A non-finite input
-// makes the sum non-finite (x^2 of a finite float32 cannot overflow
-// float64), which sets *status.
-template <int AHEAD>
+// multiply-add rounds exactly as add(fl(x^2))).  A wave takes 64 rows in
+// slabs of RN_KS coordinates: every load instruction reads the 256-byte
+// slabs of 4 rows, the slab passes through LDS (rows padded to 17 pieces, so
+// the summing lanes read distinct banks), and lane r adds row r's squares;
+// two slabs are in registers while one is summed.  A non-finite input makes
+// the sum non-finite (x^2 of a finite float32 cannot overflow float64),
+// which sets *status.
+constexpr int RN_KS = 64;               // coordinates per slab (d is a multiple of 64)
+constexpr int RN_PQ = RN_KS / 4;        // 16-byte pieces of a row slab
+constexpr int RN_LD = 64 * RN_PQ / 64;  // load instructions per slab (4 rows each)
+
+struct RnSlab {
+    f4 v[RN_LD];
+};
+
 __global__ __launch_bounds__(64) void row_norm_kernel(const float *__restrict__ X, int64_t m,
                                                       int d, double *__restrict__ norms,
                                                       int *__restrict__ status) {
-    const int64_t r = (int64_t)blockIdx.x * 64 + threadIdx.x;
-    if (r >= m) return;
-    const f4 *p = reinterpret_cast<const f4 *>(X + r * d);
-    const int nq = d / 4;
-    f4 buf[AHEAD];
+    constexpr int PS = RN_PQ + 1;
+    __shared__ f4 xs[64 * PS];
+    const int lane = threadIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.x * 64;
+    const int ns = d / RN_KS;
+    // load i: lanes 16 g .. 16 g + 15 read row 4 i + g (rows past m: the last)
+    auto row_ptr = [&](int i) {
+        int64_t r = r0 + 4 * i + (lane >> 4);
+        r = r < m ? r : m - 1;
+        return X + r * d + 4 * (lane & 15);
+    };
+    auto load = [&](int sl, RnSlab &b) {
 #pragma unroll
-    for (int u = 0; u < AHEAD; ++u) buf[u] = p[u];
+        for (int i = 0; i < RN_LD; ++i)
+            b.v[i] = *reinterpret_cast<const f4 *>(row_ptr(i) + sl * RN_KS);
+    };
+    // the barriers order the lanes' LDS accesses (a lane sums what other
+    // lanes staged) and leave the loads in flight
+    auto stage = [&](const RnSlab &b) {
+        lds_barrier();
+#pragma unroll
+        for (int i = 0; i < RN_LD; ++i) xs[(4 * i + (lane >> 4)) * PS + (lane & 15)] = b.v[i];
+        lds_barrier();
+        // the refill of these registers stays after the writes: moved ahead,
+        // it would take other registers and the loop would copy them back
+        // at its back edge, waiting for every load in flight
+        __builtin_amdgcn_sched_barrier(0);
+    };
     double s2 = 0.0;
-    for (int q0 = 0; q0 < nq; q0 += AHEAD) {
+    auto sum = [&]() {
 #pragma unroll
-        for (int u = 0; u < AHEAD; ++u) {
-            const f4 v = buf[u];
-            if (q0 + AHEAD + u < nq) buf[u] = p[q0 + AHEAD + u];
+        for (int q = 0; q < RN_PQ; ++q) {
+            const f4 v = xs[lane * PS + q];
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const double x = (double)v[c];
                 s2 = __builtin_fma(x, x, s2);
             }
         }
+    };
+    RnSlab b0, b1;
+    load(0, b0);
+    __builtin_amdgcn_sched_barrier(0);   // b0's loads all ahead of b1's
+    load(ns > 1 ? 1 : 0, b1);
+    for (int sl = 0; sl < ns; sl += 2) {
+        stage(b0);
+        load(sl + 2 < ns ? sl + 2 : ns - 1, b0);
+        sum();
+        if (sl + 1 < ns) stage(b1);
+        load(sl + 3 < ns ? sl + 3 : ns - 1, b1);
+        if (sl + 1 < ns) sum();
     }
-    norms[r] = std::sqrt(s2);
-    if (!std::isfinite(s2)) atomicOr(status, 1);
+    const int64_t r = r0 + lane;
+    if (r < m) {
+        norms[r] = std::sqrt(s2);
+        if (!std::isfinite(s2)) atomicOr(status, 1);
+    }
 }
 
 // ------------------------------------------------------------- encode_gemm
@@ -992,12 +1037,8 @@ hipError_t encode_rows(const float *X, int64_t n, int d, const float *R,
         // every output tile of the chunk writes its flag count
         QuantArgs qa{bounds, calib.athr, cb.levels, codes_tmp, norms, flags, tile_count, status_dev};
         // one wave per 64 rows, spread over the CUs
-        if (d % 128 == 0)
-            hipLaunchKernelGGL(row_norm_kernel<32>, dim3((unsigned)((m + 63) / 64)), dim3(64), 0,
-                               stream, X + r0 * d, m, d, norms, status_dev);
-        else
-            hipLaunchKernelGGL(row_norm_kernel<16>, dim3((unsigned)((m + 63) / 64)), dim3(64), 0,
-                               stream, X + r0 * d, m, d, norms, status_dev);
+        hipLaunchKernelGGL(row_norm_kernel, dim3((unsigned)((m + 63) / 64)), dim3(64), 0, stream,
+                           X + r0 * d, m, d, norms, status_dev);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(encode_gemm, dim3(groups * 8 * ncol), dim3(GEMM_THREADS), 0,
