@@ -852,9 +852,24 @@ __global__ __launch_bounds__(256) void merge_kernel(const float *__restrict__ cs
         // Each workgroup's list is sorted, and its k best are k distinct
         // vectors: the k-th entry of any list is also a lower bound on the
         // query's k-th best score, and usually a much tighter one.
-        for (int g = threadIdx.x; g < G; g += 256) {
-            const int64_t e = base + (int64_t)g * k + (k - 1);
-            if (ci[e] != INT_MAX) atomicMax(&lkey, fkey(cs[e]));
+        // And the lists hold disjoint vectors, so the k-th largest of any
+        // lists' best entries is one too: each wave sorts the best entries
+        // of 64 lists and offers its k-th.
+        for (int g0 = 0; g0 < G; g0 += 256) {
+            const int g = g0 + threadIdx.x;
+            const int64_t e = base + (int64_t)(g < G ? g : 0) * k;
+            const bool in = g < G;
+            const int last_i = in ? ci[e + (k - 1)] : INT_MAX;
+            const float last_s = in ? cs[e + (k - 1)] : -INFINITY;
+            const int top_i = in ? ci[e] : INT_MAX;
+            float top_s = in && top_i != INT_MAX ? cs[e] : -INFINITY;
+            int top_g = g;
+            if (last_i != INT_MAX) atomicMax(&lkey, fkey(last_s));
+            if (k > 1) {   // at k = 1 a list's best entry is its k-th
+                wave_sort64(top_s, top_g, lane);
+                const float kth = __shfl(top_s, k - 1);
+                if (lane == 0 && kth > -INFINITY) atomicMax(&lkey, fkey(kth));
+            }
         }
         __syncthreads();
         const float bound = unfkey(lkey);
