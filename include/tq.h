@@ -26,6 +26,10 @@
  *    codebook and rotation constructors are host-only and work without one.
  *  - Sizes: 64 <= d <= 2048 with d % 64 == 0; bits in {1, 2, 3, 4, 8}
  *    (bits == 3 additionally needs d % 128 == 0); k in 1..4096.
+ *  - Environment: TQ_SCAN_GRID=<n> (1..65535) sets the number of workgroups
+ *    of the search kernels, read at each call (default: one per compute
+ *    unit; other values are ignored).  Results do not depend on it; it
+ *    exists to test large per-workgroup shares of the index at small sizes.
  */
 #ifndef TQ_H
 #define TQ_H

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -1079,7 +1080,16 @@ static ScanShape shape_of(const tq_index *x) {
     return s;
 }
 
+// Workgroups of the search kernels: one per compute unit, or TQ_SCAN_GRID
+// (1..65535) when set, which gives each workgroup a larger share of the
+// blocks (at one workgroup, a 300K-row index spans several list windows of
+// the filtered scan).
 static int scan_grid() {
+    if (const char *e = getenv("TQ_SCAN_GRID")) {
+        char *end = nullptr;
+        const long v = strtol(e, &end, 10);
+        if (end != e && *end == '\0' && v >= 1 && v <= 65535) return (int)v;
+    }
     const int cus = device_cu_count();
     return cus > 0 ? cus : 256;
 }

@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
+import synth
 from tests.conftest import gpu_available
 from tests.parity import check_topk, oracle_tables
 
@@ -100,3 +101,50 @@ def test_other_dimensions(d, bits):
     masks = [oracle.allowed_mask(tenants, bm[b]) for b in range(nq)]
     check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, qrot, qn, 10,
                ref_i, ref_s, allowed=masks)
+
+
+@pytest.mark.parametrize("grid", [1, 2])
+def test_one_workgroup_share_spans_list_windows(monkeypatch, grid):
+    """With one or two workgroups, each covers more than 4,096 blocks: the
+    filtered scan lists its blocks in several windows and the unfiltered split
+    scan runs over 64 passes per query.  Codes and scales are random (the scan
+    does not depend on how they were made); d = 256, b = 4 takes the split
+    scans (8 chunks per vector)."""
+    d, bits, T, nq = 256, 4, 100, 6
+    n = 2 * 4096 * 64 + 3 * 64 + 17
+    print("scan grid=%d n=%d" % (grid, n), flush=True)
+    rng = np.random.default_rng(77)
+    codes = rng.integers(0, 16, size=(n, d), dtype=np.uint8)
+    scales = rng.uniform(0.5, 1.5, n).astype(np.float32)
+    tenants = synth.zipf_tenants(n, T, seed=78)
+    rot = tq.Rotation(d, 5)
+    R32 = rot.matrix()
+    cb = tq.Codebook(d, bits)
+    ocb = oracle_tables(cb)
+    Q = rng.standard_normal((nq, d)).astype(np.float32)
+    idx = tq.Index(cb, rot, n_tenants=T)
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, bits)).cuda(),
+                  torch.from_numpy(scales).cuda(),
+                  torch.from_numpy(tenants.view(np.int16)).cuda())
+    Qd = torch.from_numpy(Q).cuda()
+    qrot = oracle.rotate_queries(R32, Q)
+    qn = np.linalg.norm(Q.astype(np.float64), axis=1)
+    monkeypatch.setenv("TQ_SCAN_GRID", str(grid))
+    for k in (10, 100):
+        ids, sc = idx.search(Qd, k)
+        ref_i, ref_s = oracle.search(codes, scales, ocb.cents, R32, Q, k)
+        check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, qrot, qn, k,
+                   ref_i, ref_s)
+    for mode in ("selective", "broad"):
+        bm = synth.allowlist_bitmap(synth.allowlists(nq, T, mode, seed=79), T)
+        ids, sc = idx.search(Qd, 10, allow=torch.from_numpy(bm.view(np.int64)).cuda())
+        ref_i, ref_s = oracle.search(codes, scales, ocb.cents, R32, Q, 10, tenants, bm)
+        masks = [oracle.allowed_mask(tenants, bm[b]) for b in range(nq)]
+        check_topk(ids.cpu().numpy(), sc.cpu().numpy(), codes, scales, ocb.cents, qrot, qn, 10,
+                   ref_i, ref_s, allowed=masks)
+    monkeypatch.delenv("TQ_SCAN_GRID")
+    # the default launch returns the same lists
+    ids1, sc1 = idx.search(Qd, 100)
+    monkeypatch.setenv("TQ_SCAN_GRID", str(grid))
+    ids2, sc2 = idx.search(Qd, 100)
+    assert torch.equal(ids1, ids2) and torch.equal(sc1, sc2)
