@@ -561,9 +561,6 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
                 // past the last item the refills read this group again:
                 // cache hits, no HBM traffic
                 const uint4 *nsrc = nxt < total ? wg_src + (int64_t)(nxt % NGq) * 8 * 64 : csrc;
-                // the ticket after next is taken now and read after the
-                // group's lookups, which hide its LDS round trip
-                const int ticket = take(misc + 1);
                 const char *Lb = lut + c0 * kChunkTableBytes<MODE>;
                 int acc = 0;
 #pragma unroll
@@ -574,7 +571,6 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
                     __builtin_amdgcn_sched_barrier(kKeepVmem);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                const int nxt2 = __builtin_amdgcn_readfirstlane(ticket);
                 atomicAdd(&accb[bl * 64 + lane], acc);
                 // LDS executes each wave's operations in order, so when the
                 // count reaches GPB every group's sum is in the slot
@@ -592,6 +588,9 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_scan_kernel(ScanParams p) 
                     top.offer_seen(inside ? sc : -INFINITY, inside ? (int)vid : INT_MAX, lane, p.k,
                                    misc, p.gbound + qi, gk);
                 }
+                // the ticket after next, taken as late as possible: near the
+                // end of a query a wave holds no more than two groups
+                const int nxt2 = __builtin_amdgcn_readfirstlane(take(misc + 1));
                 tk = nxt;
                 nxt = nxt2;
                 csrc = nsrc;
@@ -749,7 +748,6 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                                                    __HIP_MEMORY_SCOPE_AGENT);
                         }
                         const uint4 *nsrc = nxt < ng ? group_src(nxt) : csrc;
-                        const int ticket = take(ctr);
                         const char *Lb = lut + c0 * kChunkTableBytes<MODE>;
                         int acc = 0;
 #pragma unroll
@@ -759,7 +757,6 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                             __builtin_amdgcn_sched_barrier(kKeepVmem);
                         }
                         __builtin_amdgcn_sched_barrier(0);
-                        const int nxt2 = __builtin_amdgcn_readfirstlane(ticket);
                         atomicAdd(&accb[bl * 64 + lane], acc);
                         const int fin = __builtin_amdgcn_readfirstlane(take(done + bl));
                         if (fin == GPB - 1) {
@@ -780,6 +777,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void split_filtered_kernel(ScanParams
                                            misc, p.gbound + qi, gk);
                         }
                         if (nxt >= ng) break;
+                        const int nxt2 = __builtin_amdgcn_readfirstlane(take(ctr));
                         cur = nxt;
                         nxt = nxt2;
                         csrc = nsrc;
