@@ -387,9 +387,11 @@ def main() -> int:
     idx.reserve(n)
     stream = torch.cuda.current_stream()
     # untimed warm-up on a throwaway index: the first calls load the kernels'
-    # code and upload the rotation, one-time costs outside the encode rate
+    # code, and the GPU needs about 25 ms of this load to reach its working
+    # clock (a first encode after idle time runs 4-5% slower); the timed
+    # index's rotation is uploaded by its reserve
     warm = tq.Index(cb, rot, n_tenants=1)
-    warm.add(X[:4096])
+    warm.add(X[:min(n, 20 * 32768)])
     del warm
     torch.cuda.synchronize()
     log("encoding the corpus on the GPU")

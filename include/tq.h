@@ -136,7 +136,9 @@ tq_status tq_rotate_queries(const tq_rotation *rot, const float *Q_dev,
 tq_status tq_index_create(const tq_codebook *cb, const tq_rotation *rot,
                           int32_t n_tenants, tq_index **out);
 
-/* Pre-allocates device storage for `capacity` vectors. */
+/* Pre-allocates device storage for `capacity` vectors and uploads the
+ * index's rotation matrix to the current device (a one-time set-up that the
+ * first add would otherwise do). */
 tq_status tq_index_reserve(tq_index *idx, int64_t capacity);
 
 /* add(): encodes X_dev [n][d] float32 exactly as tq_rotate_quantize and

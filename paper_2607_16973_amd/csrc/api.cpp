@@ -452,7 +452,12 @@ tq_status tq_index_create(const tq_codebook *cb, const tq_rotation *rot, int32_t
 tq_status tq_index_reserve(tq_index *idx, int64_t capacity) {
     if (!idx) return fail(TQ_EINVAL, "NULL index");
     if (capacity < 0) return fail(TQ_EINVAL, "capacity < 0");
-    return index_grow(idx, capacity, nullptr);
+    tq_status st = index_grow(idx, capacity, nullptr);
+    if (st != TQ_OK) return st;
+    // the encoder's copy of the rotation on the current device (otherwise
+    // uploaded by the first add)
+    const float *R = nullptr;
+    return rotation_dev(&idx->rot, &R);
 }
 
 static tq_status finish_add(tq_index *x, const uint16_t *tenants_dev, int64_t n, hipStream_t s) {
