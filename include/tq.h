@@ -373,8 +373,9 @@ tq_status tq_search_ex(const tq_index *idx, const float *Q_dev, int64_t nq,
  * Queries are taken in as many consecutive launches as the array needs; a
  * search whose single query needs more than the array (k > 256 over a very
  * large index) returns TQ_EUNSUPPORTED.  The index's rotation must already
- * be on the current device -- it is uploaded by the first tq_index_add,
- * tq_index_calibrate or allocating search on the index -- else TQ_EINVAL.
+ * be on the current device -- it is uploaded by tq_index_reserve, the first
+ * tq_index_add, tq_index_calibrate or allocating search on the index -- else
+ * TQ_EINVAL.
  * Every call on one GPU shares that GPU's array: calls that overlap in time
  * on one GPU (two streams or threads) race and must be serialised by the
  * caller; consecutive calls on one stream are safe. */
