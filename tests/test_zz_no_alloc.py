@@ -100,6 +100,20 @@ def test_rotation_must_be_resident_first(env):
     _same(idx.search_noalloc(env.Qd[:4].contiguous(), 10), ref)
 
 
+def test_reserve_makes_the_rotation_resident(env):
+    """tq_index_reserve uploads the index's rotation, so an index filled from
+    codes after a reserve takes the no-alloc search at once."""
+    rot = tq.Rotation(D, 42)
+    idx = tq.Index(env.cb, rot, n_tenants=1)
+    idx.reserve(500)
+    codes, _, scales = oracle.encode(env.X[:500], rot.matrix(), oracle.Codebook(
+        d=D, bits=4, bounds=env.cb.bounds, cents=env.cb.cents, iterations=0, converged=True))
+    idx.add_codes(torch.from_numpy(oracle.pack_codes(codes, 4)).cuda(),
+                  torch.from_numpy(scales).cuda())
+    got = idx.search_noalloc(env.Qd[:4].contiguous(), 10)
+    _same(got, idx.search_alloc(env.Qd[:4].contiguous(), 10))
+
+
 def test_argument_errors(env):
     L = _lib.lib
     import ctypes
