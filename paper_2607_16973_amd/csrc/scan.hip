@@ -20,6 +20,7 @@
 //    per-workgroup lists of each query.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdint>
@@ -1264,10 +1265,19 @@ hipError_t launch_scan_mode(const ScanParams &p, int grid, size_t lds, bool spli
 
 }  // namespace
 
+// The compute-unit count is asked of the runtime once per device and kept:
+// every search call needs it (grid size and workspace layout), and the query
+// costs about as much as a kernel launch on the host.
 int device_cu_count() {
+    static std::atomic<int> cached[64];
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (dev >= 0 && dev < 64) {
+        const int c = cached[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (dev >= 0 && dev < 64 && cus > 0) cached[dev].store(cus, std::memory_order_relaxed);
     return cus;
 }
 
