@@ -312,8 +312,9 @@ class Index:
             ids = torch.empty((nq, k), dtype=torch.int64, device=Q.device)
         if scores is None:
             scores = torch.empty((nq, k), dtype=torch.float32, device=Q.device)
-        need = self.workspace_bytes(nq, k, path)
         if workspace is None:
+            # a workspace the caller passes is checked by the library itself
+            need = self.workspace_bytes(nq, k, path)
             if self._ws is None or self._ws.numel() < need:
                 self._ws = torch.empty((need,), dtype=torch.uint8, device=Q.device)
             workspace = self._ws
